@@ -1,0 +1,255 @@
+"""CPU oracle for the candidate-screening path (ctypes over oracle/libkbo.so).
+
+TEST INFRASTRUCTURE ONLY.  The test suite, the smoke check and the
+benchmark's CPU-baseline leg are its only users; the product package never
+imports it.  See kbo.c for what each function computes and how it is pinned.
+
+Arrays are numpy arrays holding raw storage: float32 for f32, and uint16 (or
+float16) bit patterns for f16 and bf16.
+"""
+import ctypes
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+from . import build as _build
+
+F32, F16, BF16, U32 = 0, 1, 2, 3
+DIST_U32, DIST_UNIFORM, DIST_NORMAL = 0, 1, 2
+EQUAL_NAN = 1
+DTYPES = {"f32": F32, "f16": F16, "bf16": BF16, "u32": U32}
+NP_STORAGE = {F32: np.float32, F16: np.uint16, BF16: np.uint16, U32: np.uint32}
+
+
+class Partial(ctypes.Structure):
+    _fields_ = [("numel", ctypes.c_uint64), ("mismatches", ctypes.c_uint64),
+                ("nan_count", ctypes.c_uint64), ("pos_inf_count", ctypes.c_uint64),
+                ("neg_inf_count", ctypes.c_uint64),
+                ("sum_sq_diff", ctypes.c_double), ("sum_sq_diff_comp", ctypes.c_double),
+                ("sum_sq_ref", ctypes.c_double), ("sum_sq_ref_comp", ctypes.c_double),
+                ("max_abs_err", ctypes.c_float), ("max_rel_err", ctypes.c_float),
+                ("bitdiff", ctypes.c_uint32), ("_pad", ctypes.c_uint32)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("numel", ctypes.c_uint64), ("mismatches", ctypes.c_uint64),
+                ("nan_count", ctypes.c_uint64), ("pos_inf_count", ctypes.c_uint64),
+                ("neg_inf_count", ctypes.c_uint64),
+                ("sum_sq_diff", ctypes.c_double), ("sum_sq_ref", ctypes.c_double),
+                ("rel_l2", ctypes.c_double),
+                ("max_abs_err", ctypes.c_float), ("max_rel_err", ctypes.c_float),
+                ("bitwise_equal", ctypes.c_int32), ("passed", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib():
+    """Load oracle/libkbo.so, building it first if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB)
+        u32, u64, f32, vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p
+        L.kbo_philox4x32_10.argtypes = [ctypes.POINTER(u32), ctypes.POINTER(u32),
+                                        ctypes.POINTER(u32)]
+        L.kbo_stream_block.argtypes = [u64, u32, u32, u64, ctypes.POINTER(u32)]
+        L.kbo_u01.argtypes = [u32]
+        L.kbo_u01.restype = f32
+        L.kbo_uniform.argtypes = [u32, f32, f32]
+        L.kbo_uniform.restype = f32
+        L.kbo_normal01.argtypes = [u32, u32, ctypes.c_int]
+        L.kbo_normal01.restype = f32
+        L.kbo_f32_to_f16.argtypes = [f32]
+        L.kbo_f32_to_f16.restype = ctypes.c_uint16
+        L.kbo_f32_to_bf16.argtypes = [f32]
+        L.kbo_f32_to_bf16.restype = ctypes.c_uint16
+        L.kbo_f16_to_f32.argtypes = [ctypes.c_uint16]
+        L.kbo_f16_to_f32.restype = f32
+        L.kbo_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.kbo_bf16_to_f32.restype = f32
+        L.kbo_gen.argtypes = [vp, ctypes.c_int, u64, ctypes.c_int, f32, f32, u64, u32, u32, u64]
+        L.kbo_gen.restype = ctypes.c_int
+        L.kbo_partial_init.argtypes = [ctypes.POINTER(Partial)]
+        L.kbo_screen_range.argtypes = [ctypes.c_int, vp, vp, u64, u64, f32, f32, u32,
+                                       ctypes.POINTER(Partial)]
+        L.kbo_screen_range.restype = ctypes.c_int
+        L.kbo_merge.argtypes = [ctypes.POINTER(Partial), ctypes.POINTER(Partial)]
+        L.kbo_finalize.argtypes = [ctypes.POINTER(Partial), ctypes.POINTER(Stats)]
+        L.kbo_screen.argtypes = [ctypes.c_int, vp, vp, u64, f32, f32, u32, ctypes.POINTER(Stats)]
+        L.kbo_screen.restype = ctypes.c_int
+        L.kbo_match.argtypes = [f32, f32, f32, f32, u32]
+        L.kbo_match.restype = ctypes.c_int
+        for name in ("kbo_f32_to_f16_n", "kbo_f32_to_bf16_n", "kbo_f16_to_f32_n",
+                     "kbo_bf16_to_f32_n"):
+            getattr(L, name).argtypes = [vp, vp, u64]
+        L.kbo_uniform_n.argtypes = [vp, f32, f32, vp, u64]
+        L.kbo_match16_n.argtypes = [ctypes.c_int, vp, vp, f32, f32, u32, vp, u64]
+        _lib = L
+    return _lib
+
+
+def _code(dtype):
+    return DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+
+
+def philox4x32_10(counter, key):
+    c = (ctypes.c_uint32 * 4)(*counter)
+    k = (ctypes.c_uint32 * 2)(*key)
+    o = (ctypes.c_uint32 * 4)()
+    lib().kbo_philox4x32_10(c, k, o)
+    return tuple(o)
+
+
+def stream_block(seed, stream_id, sub, b):
+    o = (ctypes.c_uint32 * 4)()
+    lib().kbo_stream_block(seed, stream_id, sub, b, o)
+    return tuple(o)
+
+
+def u01(x):
+    return lib().kbo_u01(x)
+
+
+def uniform(x, a, b):
+    return lib().kbo_uniform(x, a, b)
+
+
+def normal01(xa, xb, odd):
+    return lib().kbo_normal01(xa, xb, odd)
+
+
+def gen(dtype, n, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0):
+    """Elements offset..offset+n-1 of a stream, as a numpy storage array."""
+    code = _code(dtype)
+    out = np.empty(n, dtype=NP_STORAGE[code])
+    rc = lib().kbo_gen(out.ctypes.data, code, n, dist, p0, p1, seed, stream_id, sub, offset)
+    if rc != 0:
+        raise ValueError("invalid (dtype, dist) pair")
+    return out
+
+
+def _storage(a, code):
+    a = np.ascontiguousarray(a)
+    want = 4 if code == F32 else 2
+    if a.dtype.itemsize != want:
+        raise TypeError("storage itemsize %d does not fit dtype code %d" % (a.dtype.itemsize, code))
+    return a
+
+
+def screen_partial(ref, cand, dtype, atol, rtol, flags=0, lo=0, hi=None):
+    code = _code(dtype)
+    ref = _storage(ref, code)
+    cand = _storage(cand, code)
+    if hi is None:
+        hi = ref.size
+    p = Partial()
+    lib().kbo_partial_init(ctypes.byref(p))
+    rc = lib().kbo_screen_range(code, ref.ctypes.data, cand.ctypes.data, lo, hi, atol, rtol,
+                                flags, ctypes.byref(p))
+    if rc != 0:
+        raise ValueError("bad dtype")
+    return p
+
+
+def merge(parts):
+    acc = Partial()
+    lib().kbo_partial_init(ctypes.byref(acc))
+    for p in parts:
+        lib().kbo_merge(ctypes.byref(acc), ctypes.byref(p))
+    return acc
+
+
+def finalize(p):
+    s = Stats()
+    lib().kbo_finalize(ctypes.byref(p), ctypes.byref(s))
+    return s.as_dict()
+
+
+def screen(ref, cand, dtype, atol, rtol, flags=0, chunk=None, threads=1):
+    """Statistics of one candidate against the reference.
+
+    With chunk set, [0, n) is cut into chunks screened independently (on up
+    to `threads` host threads; ctypes releases the GIL) and merged in chunk
+    order, which is the merge law applied to a partition of the elements.
+    """
+    code = _code(dtype)
+    ref = _storage(ref, code)
+    cand = _storage(cand, code)
+    n = ref.size
+    if cand.size != n:
+        raise ValueError("size mismatch")
+    if not chunk or chunk >= n:
+        return finalize(screen_partial(ref, cand, code, atol, rtol, flags))
+    bounds = [(lo, min(n, lo + chunk)) for lo in range(0, n, chunk)]
+    if threads > 1:
+        with ThreadPoolExecutor(threads) as ex:
+            parts = list(ex.map(lambda b: screen_partial(ref, cand, code, atol, rtol, flags,
+                                                          b[0], b[1]), bounds))
+    else:
+        parts = [screen_partial(ref, cand, code, atol, rtol, flags, lo, hi) for lo, hi in bounds]
+    return finalize(merge(parts))
+
+
+def match(c, r, atol, rtol, flags=0):
+    return bool(lib().kbo_match(c, r, atol, rtol, flags))
+
+
+def f32_to_f16(x):
+    return lib().kbo_f32_to_f16(x)
+
+
+def f32_to_bf16(x):
+    return lib().kbo_f32_to_bf16(x)
+
+
+def f16_to_f32(h):
+    return lib().kbo_f16_to_f32(h)
+
+
+def bf16_to_f32(h):
+    return lib().kbo_bf16_to_f32(h)
+
+
+def _bulk(name, inp, out_dtype):
+    inp = np.ascontiguousarray(inp)
+    out = np.empty(inp.size, dtype=out_dtype)
+    getattr(lib(), name)(inp.ctypes.data, out.ctypes.data, inp.size)
+    return out
+
+
+def f32_to_f16_n(x):
+    return _bulk("kbo_f32_to_f16_n", np.asarray(x, dtype=np.float32), np.uint16)
+
+
+def f32_to_bf16_n(x):
+    return _bulk("kbo_f32_to_bf16_n", np.asarray(x, dtype=np.float32), np.uint16)
+
+
+def f16_to_f32_n(h):
+    return _bulk("kbo_f16_to_f32_n", np.asarray(h, dtype=np.uint16), np.float32)
+
+
+def bf16_to_f32_n(h):
+    return _bulk("kbo_bf16_to_f32_n", np.asarray(h, dtype=np.uint16), np.float32)
+
+
+def uniform_n(x, a, b):
+    x = np.ascontiguousarray(x, dtype=np.uint32)
+    out = np.empty(x.size, dtype=np.float32)
+    lib().kbo_uniform_n(x.ctypes.data, a, b, out.ctypes.data, x.size)
+    return out
+
+
+def match16_n(dtype, c, r, atol, rtol, flags=0):
+    c = np.ascontiguousarray(c, dtype=np.uint16)
+    r = np.ascontiguousarray(r, dtype=np.uint16)
+    out = np.empty(c.size, dtype=np.uint8)
+    lib().kbo_match16_n(_code(dtype), c.ctypes.data, r.ctypes.data, atol, rtol, flags,
+                        out.ctypes.data, c.size)
+    return out

@@ -1,0 +1,123 @@
+/*
+ * kbo.h -- plain CPU oracle for the candidate-screening path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  The test suite, the package smoke check and the
+ * benchmark's CPU-baseline leg are the only callers.  The HIP library never
+ * includes, links or calls anything declared here, and this file includes
+ * nothing from the HIP library: the two sides are written independently and
+ * compared.
+ *
+ * What the oracle computes (paper: "KernelBrain", Section 3):
+ *   - the correctness indicator K(p) of Section 3.1 for one output tensor,
+ *     i.e. the numeric check of the Verifier in Section 3.4 ("Evaluation
+ *     Plane"), evaluated element by element against a reference output under
+ *     |c - r| <= atol + rtol*|r|, with the per-candidate statistics listed on
+ *     kbo_partial below;
+ *   - the seeded inputs such tests run on: a Philox4x32-10 counter-based
+ *     stream (Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as
+ *     1, 2, 3", SC'11) mapped to uniform and normal floats.
+ *
+ * Enumerations use the same numeric codes as the library's C interface so
+ * that a test can pass one code to both sides; that interface is the only
+ * thing the two sides have in common.
+ */
+#ifndef KBO_H
+#define KBO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { KBO_F32 = 0, KBO_F16 = 1, KBO_BF16 = 2, KBO_U32 = 3 };
+enum { KBO_DIST_U32 = 0, KBO_DIST_UNIFORM = 1, KBO_DIST_NORMAL = 2 };
+enum { KBO_EQUAL_NAN = 1u };
+
+/* Philox4x32-10 block function (SC'11, Section 4 "Philox"): ten rounds of
+ * two 32x32->64 multiplies and xors, key bumped by the Weyl constants between
+ * rounds.  in = counter (x0..x3), key = (k0, k1). */
+void kbo_philox4x32_10(const uint32_t in[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Block b of stream (stream_id, sub) under seed: key = (lo32(seed),
+ * hi32(seed)), counter = (lo32(b), hi32(b), sub, stream_id). */
+void kbo_stream_block(uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t b,
+                      uint32_t out[4]);
+
+/* u = (x >> 8) * 2^-24, exact, in [0, 1). */
+float kbo_u01(uint32_t x);
+/* U(a, b) value: fmaf(u, fl32(b - a), a), one rounding. */
+float kbo_uniform(uint32_t x, float a, float b);
+/* Standard normal from one word pair by the Box-Muller transform, in
+ * binary64 then rounded once to binary32.  odd = 0 takes the cosine branch,
+ * odd = 1 the sine branch. */
+float kbo_normal01(uint32_t xa, uint32_t xb, int odd);
+
+/* IEEE 754 conversions, round to nearest even. */
+uint16_t kbo_f32_to_f16(float f);
+uint16_t kbo_f32_to_bf16(float f);
+float kbo_f16_to_f32(uint16_t h);
+float kbo_bf16_to_f32(uint16_t h);
+
+/* Fill dst[0..n) with elements offset..offset+n-1 of the stream.
+ * dist U32 needs dtype U32; UNIFORM takes [p0, p1); NORMAL takes mean p0,
+ * standard deviation p1.  16-bit dtypes round the binary32 value to nearest
+ * even.  Returns 0, or -1 for an invalid (dtype, dist) pair. */
+int kbo_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
+            uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset);
+
+/* Mergeable per-candidate screening state over a range of elements.  Sums are
+ * Neumaier-compensated binary64 (value = sum + comp). */
+typedef struct {
+    uint64_t numel;
+    uint64_t mismatches;
+    uint64_t nan_count;
+    uint64_t pos_inf_count;
+    uint64_t neg_inf_count;
+    double sum_sq_diff, sum_sq_diff_comp;
+    double sum_sq_ref, sum_sq_ref_comp;
+    float max_abs_err;
+    float max_rel_err;
+    uint32_t bitdiff;  /* OR over elements of (storage bits of c) ^ (storage bits of r) */
+    uint32_t _pad;
+} kbo_partial;
+
+/* Final per-candidate statistics. */
+typedef struct {
+    uint64_t numel, mismatches, nan_count, pos_inf_count, neg_inf_count;
+    double sum_sq_diff, sum_sq_ref, rel_l2;
+    float max_abs_err, max_rel_err;
+    int32_t bitwise_equal;
+    int32_t passed;
+} kbo_stats;
+
+void kbo_partial_init(kbo_partial* p);
+/* Accumulate elements [lo, hi) of (ref, cand) into p.  dtype F32, F16 or
+ * BF16; both buffers hold raw storage of that dtype. */
+int kbo_screen_range(int dtype, const void* ref, const void* cand, uint64_t lo, uint64_t hi,
+                     float atol, float rtol, uint32_t flags, kbo_partial* p);
+/* into <- into (+) from: counts add, maxima take the max, bit differences OR,
+ * sums add. */
+void kbo_merge(kbo_partial* into, const kbo_partial* from);
+void kbo_finalize(const kbo_partial* p, kbo_stats* out);
+/* Whole-tensor convenience: init, one range [0, n), finalize. */
+int kbo_screen(int dtype, const void* ref, const void* cand, uint64_t n, float atol, float rtol,
+               uint32_t flags, kbo_stats* out);
+
+/* The single-element match predicate. */
+int kbo_match(float c, float r, float atol, float rtol, uint32_t flags);
+
+/* Elementwise bulk forms of the maps above, for exhaustive sweeps. */
+void kbo_f32_to_f16_n(const float* in, uint16_t* out, uint64_t n);
+void kbo_f32_to_bf16_n(const float* in, uint16_t* out, uint64_t n);
+void kbo_f16_to_f32_n(const uint16_t* in, float* out, uint64_t n);
+void kbo_bf16_to_f32_n(const uint16_t* in, float* out, uint64_t n);
+void kbo_uniform_n(const uint32_t* x, float a, float b, float* out, uint64_t n);
+/* out[i] = match(widen(c[i]), widen(r[i])) for 16-bit storage c, r. */
+void kbo_match16_n(int dtype, const uint16_t* c, const uint16_t* r, float atol, float rtol,
+                   uint32_t flags, uint8_t* out, uint64_t n);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KBO_H */
