@@ -227,6 +227,10 @@ int kbo_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
  * ------------------------------------------------------------------------- */
 static void neumaier_add(double* sum, double* comp, double x) {
     double t = *sum + x;
+    if (isinf(t)) { /* an infinite term (an overflowed difference): the sum is +inf */
+        *sum = t;
+        return;
+    }
     if (fabs(*sum) >= fabs(x)) *comp += (*sum - t) + x;
     else *comp += (x - t) + *sum;
     *sum = t;
@@ -309,8 +313,8 @@ void kbo_merge(kbo_partial* into, const kbo_partial* from) {
 }
 
 void kbo_finalize(const kbo_partial* p, kbo_stats* out) {
-    double ssd = p->sum_sq_diff + p->sum_sq_diff_comp;
-    double ssr = p->sum_sq_ref + p->sum_sq_ref_comp;
+    double ssd = isinf(p->sum_sq_diff) ? p->sum_sq_diff : p->sum_sq_diff + p->sum_sq_diff_comp;
+    double ssr = isinf(p->sum_sq_ref) ? p->sum_sq_ref : p->sum_sq_ref + p->sum_sq_ref_comp;
     out->numel = p->numel;
     out->mismatches = p->mismatches;
     out->nan_count = p->nan_count;

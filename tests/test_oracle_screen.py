@@ -180,6 +180,17 @@ def test_h16_relative_error_uses_the_reference():
     assert s["max_rel_err"] == float(np.float32(1.0) / np.float32(3.0))
 
 
+def test_overflowing_difference_is_an_infinite_squared_error():
+    # both values finite, c - r overflows binary32: the term is +inf, and so
+    # is the sum and the relative L2 error (not NaN)
+    fmax = 3.4028234663852886e38
+    s = scr(f32a(fmax, 1.0), f32a(-fmax, 1.0), 1e-5, 1e-5)
+    assert_stats(s, mismatches=1, max_abs_err=INF, max_rel_err=INF, sum_sq_diff=INF,
+                 sum_sq_ref=fmax * fmax + 1.0, rel_l2=INF)
+    parts = oracle.screen(f32a(fmax, 1.0, 2.0), f32a(-fmax, 1.0, 2.5), "f32", 1e-5, 1e-5, chunk=1)
+    assert parts["sum_sq_diff"] == INF and parts["rel_l2"] == INF
+
+
 def test_rel_l2_closed_form():
     s = scr(f32a(3.0, 4.0), f32a(3.5, 4.0), 0.0, 0.0)
     assert s["sum_sq_diff"] == 0.25 and s["sum_sq_ref"] == 25.0
