@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""Screening throughput on one MI355X: candidate GB/s screened.
+
+One step is one pass of the screening hot path over one batch of candidate
+outputs already resident in HBM: the policy gate, the screening kernel (one
+coalesced read of the reference and the K candidates, per-candidate
+statistics) and the readback of the K records with the pass/fail verdict.
+value = K * numel * element bytes / step time (GB/s).
+
+The JSON line also carries the roofline of the screening kernel (HIP events
+on the launch stream around each launch inside the timed region; the
+algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
+read of every candidate and the reference once), the CPU oracle timed on a
+bounded sample of the same workload, and the generator's throughput.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+WORKLOADS = {
+    "c1": "K=4 candidates, N=65,536 fp32, atol=rtol=1e-5",
+    "c2": "K=16 candidates, 4096x4096 bf16 (GEMM-output shape), atol=rtol=1e-2",
+    "c3": "K=1024 candidates, 256x1024 fp32 softmax rows, atol=1e-6 rtol=1e-5",
+    "c4": "K=64 candidates, 8x2048x4096 fp16 (attention-output shape), atol=rtol=1e-3",
+    "c5": "K=8 candidates, 2^30 fp32 (4 GiB each), atol=1e-8 rtol=1e-6",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, seconds):
+    """The oracle, single-threaded, on the first S elements of every candidate,
+    S chosen from a probe so that the sample takes about `seconds`."""
+    import oracle
+    from tests.helpers import dtype_name, storage
+
+    dt = dtype_name(w.ref)
+    n = w.numel
+    probe = min(n, 1 << 18)
+    r = storage(w.ref.reshape(-1)[:probe])
+    c = storage(w.cands[0].reshape(-1)[:probe])
+    t = time.perf_counter()
+    oracle.screen(r, c, dt, w.atol, w.rtol)
+    per_elem = max(1e-10, (time.perf_counter() - t) / probe)
+    per_cand = max(1, min(n, int(seconds / per_elem / len(w.cands))))
+    r = storage(w.ref.reshape(-1)[:per_cand])
+    cs = [storage(x.reshape(-1)[:per_cand]) for x in w.cands]
+    t = time.perf_counter()
+    for x in cs:
+        oracle.screen(r, x, dt, w.atol, w.rtol)
+    el = time.perf_counter() - t
+    nbytes = len(cs) * per_cand * w.dtype_bytes
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d elements of each of the %d candidates (%.1f MB screened, %.1f s)"
+                      % (per_cand, len(cs), nbytes / 1e6, el)}
+
+
+def gen_throughput(dev, kb, n, dtype):
+    import torch
+    out = torch.empty(n, dtype=dtype, device=dev)
+    res = {}
+    for name, dist in (("normal", kb.KB_DIST_NORMAL), ("uniform", kb.KB_DIST_UNIFORM)):
+        kb.kb_gen_inputs(out, dist, 0.0, 1.0, seed=0, stream_id=0x7701)
+        torch.cuda.synchronize()
+        reps = 5
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for i in range(reps):
+            kb.kb_gen_inputs(out, dist, 0.0, 1.0, seed=0, stream_id=0x7701, sub=i)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / reps
+        res[name] = {"n": n, "ms": round(ms, 4), "Gsamples_per_s": round(n / ms / 1e6, 2),
+                     "GB_per_s_written": round(n * out.element_size() / ms / 1e6, 1)}
+    del out
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gen", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the screening path is built and measured on a single "
+              "MI355X (multi-GPU sharding is a design note, not part of this build); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import __graft_entry__
+    __graft_entry__._ensure_built()
+    import torch
+
+    import paper_2608_02611_amd as kb
+    import synth
+
+    dev = torch.device("cuda:0")
+    log("building workload", args.config)
+    w = synth.build(args.config, dev, seed=0)
+    torch.cuda.synchronize()
+    K, n, b = len(w.cands), w.numel, w.dtype_bytes
+    scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol)
+    plan = scr.launch_plan()
+
+    log("warmup", args.warmup)
+    for _ in range(args.warmup):
+        scr.launch()
+        scr.read()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    log("timing", args.steps, "steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record()
+        scr.launch()
+        ends[i].record()
+        summary = scr.read()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern_ms = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / args.steps
+    screened = K * n * b
+    algorithmic = (K + 1) * n * b
+    value = screened / (ms_per_step * 1e-3) / 1e9
+    achieved = algorithmic / (kern_ms * 1e-3) / 1e9
+    summ = {k: summary.as_dict()[k] for k in ("n_passed", "n_failed", "n_rejected")}
+    log("summary", summ)
+
+    out = {
+        "metric": "candidate GB/s screened (K x N x dtype bytes/s) and % of MI355X HBM peak",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (args.config, WORKLOADS[args.config]), "K": K,
+                   "numel": n, "storage_dtype": str(w.ref.dtype).replace("torch.", ""),
+                   "atol": w.atol, "rtol": w.rtol, "launch": plan,
+                   "verdicts": summ},
+        "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "kernel_ms": round(kern_ms, 5),
+                     "algorithmic_bytes_per_launch": algorithmic},
+    }
+    if not args.no_gen:
+        log("generator throughput")
+        out["gen"] = gen_throughput(dev, kb, n, w.ref.dtype)
+    if not args.no_cpu_baseline:
+        log("cpu baseline")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

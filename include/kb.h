@@ -1,0 +1,251 @@
+/*
+ * kb.h -- C interface of the MI355X candidate-screening library (libkb.so).
+ *
+ * The library is the data-parallel hot path of the low-cost screening stage of
+ * a budget-aware, multi-fidelity kernel search ("KernelBrain", Section 3).
+ * There, every candidate first passes a policy check V(p) -- its output must
+ * satisfy the shape and dtype constraints of the reference (Section 3.2,
+ * "Policy check") -- and the Verifier then checks its output against the
+ * reference output (Section 3.4, "Evaluation Plane"); the result is the
+ * correctness indicator K(p) of the problem formulation (Section 3.1), and
+ * Algorithm 1 discards a candidate that fails either gate before any
+ * benchmarking budget is spent.  Section 3.3 (Observation 2) relies on such
+ * wrong outputs being rejected in milliseconds.  This library does that check
+ * for K candidate outputs at once, in one coalesced pass over HBM, on the
+ * seeded inputs it can also generate.
+ *
+ * Three subsystems:
+ *   kb_gen_inputs   seeded inputs: a Philox4x32-10 counter-based stream
+ *                   (Salmon et al., SC'11) mapped to u32, uniform or normal
+ *                   values (fp32, fp16, bf16);
+ *   kb_screen       policy gate + one pass over the reference and the K
+ *                   candidates computing, per candidate, the mismatch count
+ *                   under |c - r| <= atol + rtol*|r|, max abs and max rel
+ *                   error, NaN / +Inf / -Inf counts, a bitwise-identity flag
+ *                   and the relative L2 error;
+ *   kb_screen_stats reads the per-candidate records back and gives the
+ *                   pass/fail verdict of each candidate.
+ *
+ * Conventions
+ *   - Every function is extern "C" and returns an int status: KB_OK (0) or a
+ *     negative KB_ERR_* code.  On error nothing is launched and
+ *     kb_last_error() describes the problem.  No C++ exception crosses the
+ *     interface.
+ *   - Pointers marked "device" are HIP device memory on the current device;
+ *     "host" pointers are ordinary host memory.  The caller owns every
+ *     buffer and keeps it alive until the stream reaches the call.
+ *   - kb_gen_inputs and kb_screen are asynchronous and stream-ordered on the
+ *     given hipStream_t (NULL = the default stream).  kb_screen_stats
+ *     synchronizes that stream.
+ *   - The library allocates no device memory.  It keeps one small pinned
+ *     host staging ring per process for the launch tables it uploads.
+ *   - Device buffers must be 16-byte aligned (hipMalloc and torch
+ *     allocations are); element counts may be anything, including 0.
+ *   - A "data pointer" of a tensor points at element 0; strides are in
+ *     elements.
+ */
+#ifndef KB_H
+#define KB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KB_MAX_DIMS 8
+
+/* Element types.  KB_U32 exists for the generator's raw word stream only. */
+typedef enum kb_dtype { KB_F32 = 0, KB_F16 = 1, KB_BF16 = 2, KB_U32 = 3 } kb_dtype;
+
+/* Generator distributions. */
+typedef enum kb_dist { KB_DIST_U32 = 0, KB_DIST_UNIFORM = 1, KB_DIST_NORMAL = 2 } kb_dist;
+
+/* Call-level status codes (function return values). */
+enum {
+    KB_OK = 0,
+    KB_ERR_INVALID_ARG = -1, /* null pointer, bad count, bad tolerance, bad flags */
+    KB_ERR_DTYPE = -2,       /* unknown dtype, or a dtype the call does not take */
+    KB_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+    KB_ERR_ALIGNMENT = -4,   /* a device pointer is not 16-byte aligned */
+    KB_ERR_HIP = -5          /* a HIP runtime call failed (text in kb_last_error) */
+};
+
+/* Per-candidate policy status (kb_stats.status); a candidate that fails the
+ * gate is not read and is reported with zero statistics and passed = 0. */
+enum {
+    KB_STATUS_OK = 0,
+    KB_REJECT_NULL = 1,   /* candidate data pointer is NULL (and it is not empty) */
+    KB_REJECT_DTYPE = 2,  /* dtype differs from the reference */
+    KB_REJECT_SHAPE = 3,  /* ndim or a dimension differs from the reference */
+    KB_REJECT_LAYOUT = 4  /* not dense row-major (strides of a contiguous tensor) */
+};
+
+/* kb_screen flags. */
+enum {
+    KB_EQUAL_NAN = 1u << 0 /* a NaN candidate element matches a NaN reference element */
+};
+
+/* A tensor view.  data: device pointer to element 0 (may be NULL for a
+ * candidate, which the policy gate then rejects).  dtype: a kb_dtype.
+ * shape[0..ndim) and strides[0..ndim) in elements; ndim in [0, KB_MAX_DIMS]
+ * (ndim = 0 is a scalar with one element). */
+typedef struct kb_tensor {
+    const void* data;
+    int32_t dtype;
+    int32_t ndim;
+    int64_t shape[KB_MAX_DIMS];
+    int64_t strides[KB_MAX_DIMS];
+} kb_tensor;
+
+/* Per-candidate screening record, 80 bytes, written to device memory by
+ * kb_screen.  For a candidate that passed the policy gate:
+ *   numel          elements compared (= reference numel);
+ *   mismatches     elements with NOT match, where match means c == r
+ *                  (IEEE equality: +0 == -0, equal infinities), or
+ *                  |c - r| <= atol + rtol*|r| with a finite r, or -- with
+ *                  KB_EQUAL_NAN -- c and r both NaN.  c and r are the exact
+ *                  binary32 widenings of the stored values; c - r, rtol*|r|
+ *                  and the sum are each rounded to binary32 (no fused
+ *                  multiply-add);
+ *   nan_count, pos_inf_count, neg_inf_count   non-finite candidate elements;
+ *   sum_sq_diff    sum of (c - r)^2 over elements where c and r are finite,
+ *                  each term the binary64 square of the binary32 difference;
+ *   sum_sq_ref     sum of r^2 over elements where r is finite (the same for
+ *                  every candidate);
+ *   rel_l2         sqrt(sum_sq_diff / sum_sq_ref); 0 if both are 0, +inf if
+ *                  only sum_sq_ref is 0;
+ *   max_abs_err    max over elements of |c - r| (binary32), NaN ignored,
+ *                  0 if none;
+ *   max_rel_err    max over elements of |c - r| / |r| (binary32 division),
+ *                  NaN quotients (0/0, inf/inf) ignored, 0 if none;
+ *   bitwise_equal  1 iff every stored element is bit-identical;
+ *   status         KB_STATUS_OK.
+ * Counts, flags and maxima are exact; the two sums are binary64 sums in a
+ * fixed order (deterministic from call to call, within 1e-6 relative of the
+ * exact sums).  A rejected candidate has status = KB_REJECT_* and every
+ * other field zero. */
+typedef struct kb_stats {
+    uint64_t numel;
+    uint64_t mismatches;
+    uint64_t nan_count;
+    uint64_t pos_inf_count;
+    uint64_t neg_inf_count;
+    double sum_sq_diff;
+    double sum_sq_ref;
+    double rel_l2;
+    float max_abs_err;
+    float max_rel_err;
+    int32_t bitwise_equal;
+    int32_t status;
+} kb_stats;
+
+/* Verdict summary over the candidates of one call. */
+typedef struct kb_summary {
+    int32_t n_candidates;
+    int32_t n_passed;     /* status OK and mismatches == 0: K(p) = 1 */
+    int32_t n_rejected;   /* failed the policy gate */
+    int32_t n_failed;     /* passed the gate, mismatches > 0 */
+    int32_t first_passed; /* lowest index that passed, -1 if none */
+    int32_t first_failed; /* lowest index rejected or failed, -1 if none */
+} kb_summary;
+
+/* Launch configuration of a kb_screen call (reported, for measurement). */
+typedef struct kb_launch {
+    int32_t group_size;       /* candidates per work-group (KG) */
+    int32_t n_groups;         /* candidate groups */
+    int32_t blocks_per_group; /* work-groups per candidate group */
+    int32_t threads;          /* threads per work-group */
+    int64_t grid;             /* total work-groups */
+} kb_launch;
+
+/* ------------------------------------------------------------------ gate -- */
+
+/* Policy gate V(p) of Section 3.2 restricted to what an output tensor shows:
+ * for each candidate, status[k] = KB_STATUS_OK, or the first failing check in
+ * the order NULL, DTYPE, SHAPE, LAYOUT.  Host only; launches nothing.
+ *   ref, cands: host arrays of descriptors (cands has n_cands entries);
+ *   status: host array of n_cands int32.
+ * Errors: KB_ERR_INVALID_ARG (null arrays, n_cands < 0, ref ndim out of
+ * range, ref data NULL with numel > 0), KB_ERR_DTYPE (reference dtype not
+ * F32/F16/BF16). */
+int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
+                    int32_t* status);
+
+/* ---------------------------------------------------------------- screen -- */
+
+/* Bytes of device workspace kb_screen needs for n_cands candidates of numel
+ * elements of dtype (0 on invalid arguments). */
+size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype);
+
+/* The launch kb_screen would use for these sizes (KB_ERR_* on bad args). */
+int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
+
+/* Screen n_cands candidate outputs against one reference output (Section 3.1
+ * correctness indicator, Section 3.4 Verifier), stream-ordered on `stream`.
+ *   ref          host descriptor of the reference; device data, contiguous,
+ *                dtype F32, F16 or BF16;
+ *   cands        host array of n_cands descriptors (n_cands >= 1); each is
+ *                gated by kb_policy_check and, if accepted, read once;
+ *   atol, rtol   finite, >= 0 (binary32);
+ *   flags        0 or KB_EQUAL_NAN;
+ *   workspace    device scratch of workspace_bytes >=
+ *                kb_screen_workspace_bytes(n_cands, numel, dtype); its
+ *                contents need no initialisation; one workspace must not be
+ *                used by two calls that can run concurrently;
+ *   d_stats      device array of n_cands kb_stats, written by the call.
+ * Candidate k's record goes to d_stats[k].  Returns KB_OK once the work is
+ * enqueued.  Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_DTYPE,
+ * KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT (reference, accepted candidate,
+ * workspace or d_stats not 16-byte aligned), KB_ERR_HIP. */
+int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+              float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
+              kb_stats* d_stats, hipStream_t stream);
+
+/* Copy n_cands records from device d_stats to host h_stats (may be NULL),
+ * synchronize `stream`, and fill *summary (may be NULL).  This is the
+ * readback and verdict step of Algorithm 1's reject-on-failure gates.
+ * Errors: KB_ERR_INVALID_ARG, KB_ERR_HIP. */
+int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats,
+                    kb_summary* summary, hipStream_t stream);
+
+/* ------------------------------------------------------------- generator -- */
+
+/* Fill device dst[0..n) with elements offset .. offset+n-1 of the seeded
+ * stream (seed, stream_id, sub):
+ *   Philox4x32-10 block b has key (lo32(seed), hi32(seed)) and counter
+ *   (lo32(b), hi32(b), sub, stream_id); element g is word g mod 4 of block
+ *   g / 4.  So any element can be regenerated on its own (random access), and
+ *   disjoint (stream_id, sub) pairs give independent streams.
+ *   KB_DIST_U32      dtype KB_U32: the word itself;
+ *   KB_DIST_UNIFORM  u = (x >> 8) * 2^-24 in [0, 1), value fmaf(u, p1 - p0, p0)
+ *                    with p1 - p0 rounded to binary32 (a value in [p0, p1]);
+ *   KB_DIST_NORMAL   Box-Muller on the word pair of g's half-block (words 0,1
+ *                    or 2,3): u1 = (x_a + 1) 2^-32, u2 = x_b 2^-32,
+ *                    z = sqrt(-2 ln u1) * (cos or sin)(2 pi u2) in binary64
+ *                    (cosine for even g, sine for odd g), rounded to
+ *                    binary32; value fmaf(z, p1, p0) (mean p0, std dev p1).
+ *   F16 / BF16 dtypes round the binary32 value to nearest even.
+ * dst: device, 16-byte aligned.  Errors: KB_ERR_INVALID_ARG (null dst with
+ * n > 0, non-finite p0/p1), KB_ERR_DTYPE (U32 with a float distribution or
+ * the reverse), KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
+                  uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
+                  hipStream_t stream);
+
+/* ----------------------------------------------------------------- misc -- */
+
+/* Text of the last error on the calling thread (empty if none); valid until
+ * the next kb_* call on this thread. */
+const char* kb_last_error(void);
+
+/* Interface version: major * 10000 + minor * 100 + patch. */
+int kb_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KB_H */

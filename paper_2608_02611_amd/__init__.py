@@ -1,0 +1,290 @@
+"""Python binding of the MI355X candidate-screening library (libkb.so).
+
+Argument marshalling only: every step of generation and screening runs in the
+library's HIP kernels; torch provides device memory, tensor metadata and the
+current stream.  The names mirror the C interface in include/kb.h:
+
+    kb_policy_check, kb_screen_workspace_bytes, kb_screen_launch, kb_screen,
+    kb_screen_stats, kb_gen_inputs, kb_last_error, kb_version
+
+plus `screen(...)`, which chains the gate, the kernel and the readback for the
+common case.  Loading fails loudly (KbError) when libkb.so has not been built;
+there is no fallback implementation.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkb.so")
+
+# Codes shared with include/kb.h.
+KB_F32, KB_F16, KB_BF16, KB_U32 = 0, 1, 2, 3
+KB_DIST_U32, KB_DIST_UNIFORM, KB_DIST_NORMAL = 0, 1, 2
+KB_OK = 0
+KB_ERR_INVALID_ARG, KB_ERR_DTYPE, KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT, KB_ERR_HIP = -1, -2, -3, -4, -5
+KB_STATUS_OK, KB_REJECT_NULL, KB_REJECT_DTYPE, KB_REJECT_SHAPE, KB_REJECT_LAYOUT = 0, 1, 2, 3, 4
+KB_EQUAL_NAN = 1
+KB_MAX_DIMS = 8
+
+ERROR_NAMES = {KB_ERR_INVALID_ARG: "KB_ERR_INVALID_ARG", KB_ERR_DTYPE: "KB_ERR_DTYPE",
+               KB_ERR_WORKSPACE: "KB_ERR_WORKSPACE", KB_ERR_ALIGNMENT: "KB_ERR_ALIGNMENT",
+               KB_ERR_HIP: "KB_ERR_HIP"}
+
+
+class KbError(RuntimeError):
+    def __init__(self, code, message):
+        super().__init__("%s (%d): %s" % (ERROR_NAMES.get(code, "KB_ERR"), code, message))
+        self.code = code
+
+
+class KbTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * KB_MAX_DIMS), ("strides", ctypes.c_int64 * KB_MAX_DIMS)]
+
+
+class KbStats(ctypes.Structure):
+    _fields_ = [("numel", ctypes.c_uint64), ("mismatches", ctypes.c_uint64),
+                ("nan_count", ctypes.c_uint64), ("pos_inf_count", ctypes.c_uint64),
+                ("neg_inf_count", ctypes.c_uint64), ("sum_sq_diff", ctypes.c_double),
+                ("sum_sq_ref", ctypes.c_double), ("rel_l2", ctypes.c_double),
+                ("max_abs_err", ctypes.c_float), ("max_rel_err", ctypes.c_float),
+                ("bitwise_equal", ctypes.c_int32), ("status", ctypes.c_int32)]
+
+    def as_dict(self):
+        d = {name: getattr(self, name) for name, _ in self._fields_}
+        d["passed"] = int(d["status"] == KB_STATUS_OK and d["mismatches"] == 0)
+        return d
+
+
+class KbSummary(ctypes.Structure):
+    _fields_ = [("n_candidates", ctypes.c_int32), ("n_passed", ctypes.c_int32),
+                ("n_rejected", ctypes.c_int32), ("n_failed", ctypes.c_int32),
+                ("first_passed", ctypes.c_int32), ("first_failed", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class KbLaunch(ctypes.Structure):
+    _fields_ = [("group_size", ctypes.c_int32), ("n_groups", ctypes.c_int32),
+                ("blocks_per_group", ctypes.c_int32), ("threads", ctypes.c_int32),
+                ("grid", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+assert ctypes.sizeof(KbStats) == 80
+assert ctypes.sizeof(KbTensor) == 144
+
+EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_launch", "kb_screen",
+           "kb_screen_stats", "kb_gen_inputs", "kb_last_error", "kb_version")
+
+_lib = None
+
+
+def lib():
+    """The loaded libkb.so; raises KbError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise KbError(KB_ERR_HIP, "%s is not built (run __graft_entry__.build())" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, u32, u64, f32 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64,
+                                  ctypes.c_float)
+        L.kb_policy_check.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32,
+                                      ctypes.POINTER(ctypes.c_int32)]
+        L.kb_policy_check.restype = i32
+        L.kb_screen_workspace_bytes.argtypes = [i32, u64, i32]
+        L.kb_screen_workspace_bytes.restype = ctypes.c_size_t
+        L.kb_screen_launch.argtypes = [i32, u64, i32, ctypes.POINTER(KbLaunch)]
+        L.kb_screen_launch.restype = i32
+        L.kb_screen.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
+                                u32, vp, ctypes.c_size_t, vp, vp]
+        L.kb_screen.restype = i32
+        L.kb_screen_stats.argtypes = [vp, i32, ctypes.POINTER(KbStats), ctypes.POINTER(KbSummary),
+                                      vp]
+        L.kb_screen_stats.restype = i32
+        L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
+        L.kb_gen_inputs.restype = i32
+        L.kb_last_error.argtypes = []
+        L.kb_last_error.restype = ctypes.c_char_p
+        L.kb_version.argtypes = []
+        L.kb_version.restype = i32
+        _lib = L
+    return _lib
+
+
+def kb_last_error():
+    return lib().kb_last_error().decode()
+
+
+def kb_version():
+    return lib().kb_version()
+
+
+def _check(rc):
+    if rc != KB_OK:
+        raise KbError(rc, kb_last_error())
+    return rc
+
+
+# ------------------------------------------------------------ marshalling ---
+
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(t):
+    torch = _torch()
+    m = {torch.float32: KB_F32, torch.float16: KB_F16, torch.bfloat16: KB_BF16,
+         torch.int32: KB_U32}
+    if hasattr(torch, "uint32"):
+        m[torch.uint32] = KB_U32
+    if t.dtype not in m:
+        return -1
+    return m[t.dtype]
+
+
+def describe(t, dtype=None):
+    """kb_tensor descriptor of a torch tensor (or None -> a NULL candidate)."""
+    d = KbTensor()
+    if t is None:
+        d.data = None
+        d.dtype = -1 if dtype is None else dtype
+        d.ndim = 0
+        return d
+    if t.dim() > KB_MAX_DIMS:
+        raise ValueError("more than %d dimensions" % KB_MAX_DIMS)
+    d.data = t.data_ptr() if t.numel() > 0 or t.data_ptr() else None
+    d.dtype = dtype_code(t) if dtype is None else dtype
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.strides[i] = t.stride(i)
+    return d
+
+
+def _stream_handle(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ------------------------------------------------------------- interface ---
+
+def kb_policy_check(ref, cands):
+    """Per-candidate policy status (list of ints) for torch tensors / None."""
+    r = describe(ref)
+    arr = (KbTensor * max(1, len(cands)))(*[describe(c) for c in cands])
+    status = (ctypes.c_int32 * max(1, len(cands)))()
+    _check(lib().kb_policy_check(ctypes.byref(r), arr, len(cands), status))
+    return list(status)[:len(cands)]
+
+
+def kb_screen_workspace_bytes(n_cands, numel, dtype):
+    return lib().kb_screen_workspace_bytes(n_cands, numel, dtype)
+
+
+def kb_screen_launch(n_cands, numel, dtype):
+    out = KbLaunch()
+    _check(lib().kb_screen_launch(n_cands, numel, dtype, ctypes.byref(out)))
+    return out.as_dict()
+
+
+def alloc_workspace(n_cands, numel, dtype, device):
+    torch = _torch()
+    nbytes = kb_screen_workspace_bytes(n_cands, numel, dtype)
+    if nbytes == 0:
+        raise KbError(KB_ERR_INVALID_ARG, "no workspace size for these arguments")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def alloc_stats(n_cands, device):
+    torch = _torch()
+    return torch.empty(n_cands * ctypes.sizeof(KbStats), dtype=torch.uint8, device=device)
+
+
+def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, stream=None):
+    """Enqueue the screen of `cands` (torch tensors or None) against `ref`.
+
+    Returns (d_stats, workspace) device buffers; read the records with
+    kb_screen_stats.
+    """
+    n = len(cands)
+    r = describe(ref)
+    arr = (KbTensor * max(1, n))(*[describe(c) for c in cands])
+    if workspace is None:
+        workspace = alloc_workspace(max(1, n), ref.numel(), r.dtype if r.dtype >= 0 else 0,
+                                    ref.device)
+    if d_stats is None:
+        d_stats = alloc_stats(max(1, n), ref.device)
+    _check(lib().kb_screen(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
+                           ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                           ctypes.c_void_p(d_stats.data_ptr()), _stream_handle(stream)))
+    return d_stats, workspace
+
+
+def kb_screen_stats(d_stats, n_cands, stream=None):
+    """Read back n_cands records (synchronizes the stream): (list of dicts, summary dict)."""
+    host = (KbStats * max(1, n_cands))()
+    summ = KbSummary()
+    _check(lib().kb_screen_stats(ctypes.c_void_p(d_stats.data_ptr()), n_cands, host,
+                                 ctypes.byref(summ), _stream_handle(stream)))
+    return [host[k].as_dict() for k in range(n_cands)], summ.as_dict()
+
+
+def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):
+    """Fill torch tensor dst (contiguous) with elements offset.. of the seeded stream."""
+    if not dst.is_contiguous():
+        raise ValueError("dst must be contiguous")
+    _check(lib().kb_gen_inputs(ctypes.c_void_p(dst.data_ptr()), dtype_code(dst), dst.numel(),
+                               int(dist), float(p0), float(p1), int(seed), int(stream_id),
+                               int(sub), int(offset), _stream_handle(stream)))
+    return dst
+
+
+def screen(ref, cands, atol, rtol, flags=0, stream=None):
+    """Gate + screen + readback: (list of per-candidate dicts, summary dict)."""
+    d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)
+    return kb_screen_stats(d_stats, len(cands), stream=stream)
+
+
+class Screener:
+    """Repeated screening of one fixed set of buffers with the argument
+    marshalling done once: descriptors, workspace, device records and the
+    host readback buffer are built at construction and reused by every
+    launch()/read() pair."""
+
+    def __init__(self, ref, cands, atol, rtol, flags=0, stream=None):
+        self.ref, self.cands = ref, list(cands)
+        self.n = len(self.cands)
+        self.atol, self.rtol, self.flags = float(atol), float(rtol), int(flags)
+        self._ref = describe(ref)
+        self._arr = (KbTensor * max(1, self.n))(*[describe(c) for c in self.cands])
+        self.workspace = alloc_workspace(max(1, self.n), ref.numel(), self._ref.dtype, ref.device)
+        self.d_stats = alloc_stats(max(1, self.n), ref.device)
+        self._host = (KbStats * max(1, self.n))()
+        self._summary = KbSummary()
+        self.stream = stream
+        self._stream = _stream_handle(stream)
+        self._ws = ctypes.c_void_p(self.workspace.data_ptr())
+        self._st = ctypes.c_void_p(self.d_stats.data_ptr())
+        self._L = lib()
+
+    def launch(self):
+        _check(self._L.kb_screen(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
+                                 self.flags, self._ws, self.workspace.numel(), self._st,
+                                 self._stream))
+
+    def read(self):
+        _check(self._L.kb_screen_stats(self._st, self.n, self._host, ctypes.byref(self._summary),
+                                       self._stream))
+        return self._summary
+
+    def records(self):
+        return [self._host[k].as_dict() for k in range(self.n)]
+
+    def launch_plan(self):
+        return kb_screen_launch(max(1, self.n), self.ref.numel(), self._ref.dtype)

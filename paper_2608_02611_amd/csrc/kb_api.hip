@@ -1,0 +1,379 @@
+// kb_api.hip -- host side of the C interface (include/kb.h): argument
+// validation, the policy gate, launch planning, the launch-table upload and
+// the statistics readback.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kb_device.hpp"
+#include "kb_internal.hpp"
+
+namespace kb {
+namespace {
+
+thread_local std::string g_error;
+
+void clear_error() { g_error.clear(); }
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return code;
+}
+
+int fail_hip(hipError_t e, const char* what) {
+    return fail(KB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool is_float_dtype(int dt) { return dt == DT_F32 || dt == DT_F16 || dt == DT_BF16; }
+size_t elem_size(int dt) { return dt == DT_F32 || dt == DT_U32 ? 4 : 2; }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+uint64_t tensor_numel(const kb_tensor& t) {
+    uint64_t n = 1;
+    for (int i = 0; i < t.ndim; ++i) n *= (uint64_t)t.shape[i];
+    return n;
+}
+
+bool shape_valid(const kb_tensor& t) {
+    if (t.ndim < 0 || t.ndim > KB_MAX_DIMS) return false;
+    for (int i = 0; i < t.ndim; ++i)
+        if (t.shape[i] < 0) return false;
+    return true;
+}
+
+// Dense row-major: the stride of every dimension of size > 1 is the product
+// of the sizes after it.
+bool is_contiguous(const kb_tensor& t) {
+    if (tensor_numel(t) == 0) return true;
+    int64_t expect = 1;
+    for (int i = t.ndim - 1; i >= 0; --i) {
+        if (t.shape[i] != 1 && t.strides[i] != expect) return false;
+        expect *= t.shape[i];
+    }
+    return true;
+}
+
+int32_t gate_one(const kb_tensor& ref, const kb_tensor& c) {
+    // NULL data is a missing output, unless the candidate is a valid empty tensor
+    if (c.data == nullptr && !(shape_valid(c) && tensor_numel(c) == 0)) return KB_REJECT_NULL;
+    if (c.dtype != ref.dtype) return KB_REJECT_DTYPE;
+    if (!shape_valid(c) || c.ndim != ref.ndim) return KB_REJECT_SHAPE;
+    for (int i = 0; i < ref.ndim; ++i)
+        if (c.shape[i] != ref.shape[i]) return KB_REJECT_SHAPE;
+    if (!is_contiguous(c)) return KB_REJECT_LAYOUT;
+    return KB_STATUS_OK;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Pinned host staging ring for launch-table uploads.  A slot is reused only
+// after the copy that last read it has completed (its event), so callers may
+// return immediately and the copies stay asynchronous.
+// ---------------------------------------------------------------------------
+class Staging {
+public:
+    // Fill a pinned slot of `bytes` bytes with fill(host) and enqueue its copy
+    // to device dst on `stream`.
+    template <class Fill>
+    int upload(size_t bytes, Fill fill, void* dst, hipStream_t stream) {
+        std::lock_guard<std::mutex> lock(mu_);
+        Slot& sl = slots_[next_];
+        next_ = (next_ + 1) % kSlots;
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+        if (sl.ev != nullptr) {
+            e = hipEventSynchronize(sl.ev);
+            if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize(staging)");
+            if (sl.dev != dev) {
+                (void)hipEventDestroy(sl.ev);
+                sl.ev = nullptr;
+            }
+        }
+        if (sl.ev == nullptr) {
+            e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+            if (e != hipSuccess) return fail_hip(e, "hipEventCreateWithFlags");
+            sl.dev = dev;
+        }
+        if (sl.cap < bytes) {
+            if (sl.host) (void)hipHostFree(sl.host);
+            sl.host = nullptr;
+            sl.cap = 0;
+            const size_t cap = align_up(bytes < 65536 ? 65536 : bytes, 4096);
+            e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
+            if (e != hipSuccess) return fail_hip(e, "hipHostMalloc(staging)");
+            sl.cap = cap;
+        }
+        fill(sl.host);
+        e = hipMemcpyAsync(dst, sl.host, bytes, hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync(launch table)");
+        e = hipEventRecord(sl.ev, stream);
+        if (e != hipSuccess) return fail_hip(e, "hipEventRecord(staging)");
+        return KB_OK;
+    }
+
+private:
+    static constexpr int kSlots = 8;
+    struct Slot {
+        void* host = nullptr;
+        size_t cap = 0;
+        hipEvent_t ev = nullptr;
+        int dev = -1;
+    };
+    std::mutex mu_;
+    Slot slots_[kSlots];
+    int next_ = 0;
+};
+
+// Intentionally leaked: pinned memory and events must not be released from a
+// static destructor after the HIP runtime has shut down.
+Staging& staging() {
+    static Staging* s = new Staging();
+    return *s;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Launch plan.
+// ---------------------------------------------------------------------------
+bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, ScreenPlan* plan) {
+    if (n_cands < 1 || n_acc < 0 || n_acc > n_cands || !is_float_dtype(dtype)) return false;
+    ScreenPlan P{};
+    P.dtype = dtype;
+    P.n_cands = n_cands;
+    P.n_acc = n_acc;
+    P.threads = 256;
+    P.numel = numel;
+    const uint64_t vec = 16 / elem_size(dtype);
+    P.n_vec = numel / vec;
+    // Candidates per group: all of them when few, else 8.  Chosen from
+    // n_cands so that the workspace sized for n_cands always suffices.
+    int kg = 1;
+    while (kg < n_cands && kg < 8) kg *= 2;
+    P.kg = kg;
+    const int groups_max = (n_cands + kg - 1) / kg;
+    P.n_groups = n_acc > 0 ? (n_acc + kg - 1) / kg : 0;
+    // Work-groups per candidate group: about 2048 in total, a multiple of 8
+    // (XCDs), no more than there are 256-vector stripes, and enough that one
+    // work-group sees fewer than 2^31 elements (32-bit partial counts).
+    const uint64_t target_total = 2048;
+    uint64_t C = (target_total + groups_max - 1) / groups_max;
+    const uint64_t stripes = (P.n_vec + 255) / 256;
+    if (C > stripes) C = stripes;
+    const uint64_t min_c = numel / (1ull << 31) + 1;
+    if (C < min_c) C = min_c;
+    C = align_up(C < 8 ? 8 : C, 8);
+    if (C > (1u << 20)) return false;
+    P.blocks_per_group = (int)C;
+    // Workspace layout, sized for the group count of n_cands.
+    size_t off = 0;
+    P.off_tickets = off;
+    off = align_up(off + (size_t)groups_max * 4, 256);
+    P.off_table = off;
+    off = align_up(off + (size_t)n_cands * sizeof(CandEntry), 256);
+    P.off_part_u32 = off;
+    off = align_up(off + (size_t)PF_COUNT * n_cands * C * 4, 256);
+    P.off_part_ssd = off;
+    off = align_up(off + (size_t)n_cands * C * 8, 256);
+    P.off_part_ssr = off;
+    off = align_up(off + (size_t)groups_max * C * 8, 256);
+    P.total = off;
+    *plan = P;
+    return true;
+}
+
+}  // namespace kb
+
+using namespace kb;
+
+extern "C" {
+
+const char* kb_last_error(void) { return g_error.c_str(); }
+
+int kb_version(void) { return 100; }
+
+int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands, int32_t* status) {
+    clear_error();
+    if (ref == nullptr || status == nullptr || n_cands < 0 || (n_cands > 0 && cands == nullptr))
+        return fail(KB_ERR_INVALID_ARG, "kb_policy_check: null argument or negative count");
+    if (!shape_valid(*ref)) return fail(KB_ERR_INVALID_ARG, "reference shape invalid");
+    if (ref->data == nullptr && tensor_numel(*ref) != 0)
+        return fail(KB_ERR_INVALID_ARG, "reference data is NULL");
+    if (!is_float_dtype(ref->dtype))
+        return fail(KB_ERR_DTYPE, "reference dtype %d is not F32, F16 or BF16", ref->dtype);
+    for (int k = 0; k < n_cands; ++k) status[k] = gate_one(*ref, cands[k]);
+    return KB_OK;
+}
+
+size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype) {
+    ScreenPlan P;
+    if (!make_plan(n_cands, n_cands, numel, dtype, &P)) return 0;
+    return P.total;
+}
+
+int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out) {
+    clear_error();
+    if (out == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_screen_launch: out is NULL");
+    if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "dtype %d not screenable", dtype);
+    ScreenPlan P;
+    if (!make_plan(n_cands, n_cands, numel, dtype, &P))
+        return fail(KB_ERR_INVALID_ARG, "no launch plan for n_cands=%d numel=%llu", n_cands,
+                    (unsigned long long)numel);
+    out->group_size = P.kg;
+    out->n_groups = P.n_groups;
+    out->blocks_per_group = P.blocks_per_group;
+    out->threads = P.threads;
+    out->grid = (int64_t)P.n_groups * P.blocks_per_group;
+    return KB_OK;
+}
+
+int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
+              uint32_t flags, void* workspace, size_t workspace_bytes, kb_stats* d_stats,
+              hipStream_t stream) {
+    clear_error();
+    if (ref == nullptr || cands == nullptr || d_stats == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen: null ref, cands or d_stats");
+    if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "kb_screen: n_cands = %d < 1", n_cands);
+    if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen: atol and rtol must be finite and >= 0");
+    if (flags & ~(uint32_t)KB_EQUAL_NAN)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen: unknown flags 0x%x", flags);
+    std::vector<int32_t> status((size_t)n_cands);
+    int rc = kb_policy_check(ref, cands, n_cands, status.data());
+    if (rc != KB_OK) return rc;
+    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "reference is not contiguous");
+    const uint64_t numel = tensor_numel(*ref);
+    const int dtype = ref->dtype;
+    int n_acc = 0;
+    for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
+
+    ScreenPlan P;
+    if (!make_plan(n_cands, n_acc, numel, dtype, &P))
+        return fail(KB_ERR_INVALID_ARG, "kb_screen: no launch plan (numel=%llu)",
+                    (unsigned long long)numel);
+    if (workspace == nullptr || workspace_bytes < P.total)
+        return fail(KB_ERR_WORKSPACE, "kb_screen: workspace of %zu bytes, %zu needed",
+                    workspace_bytes, P.total);
+    if (!aligned16(ref->data) || !aligned16(workspace) || !aligned16(d_stats))
+        return fail(KB_ERR_ALIGNMENT, "kb_screen: reference, workspace or d_stats not 16-byte aligned");
+    for (int k = 0; k < n_cands; ++k)
+        if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
+            return fail(KB_ERR_ALIGNMENT, "kb_screen: candidate %d data not 16-byte aligned", k);
+
+    // Launch table: tickets (zeroed) then accepted candidates, then rejected.
+    const size_t upload = P.off_table + (size_t)n_cands * sizeof(CandEntry);
+    rc = staging().upload(
+        upload,
+        [&](void* host) {
+            std::memset(host, 0, P.off_table);
+            CandEntry* tab = (CandEntry*)((char*)host + P.off_table);
+            int w = 0;
+            for (int k = 0; k < n_cands; ++k)
+                if (status[k] == KB_STATUS_OK) tab[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
+            for (int k = 0; k < n_cands; ++k)
+                if (status[k] != KB_STATUS_OK) tab[w++] = CandEntry{nullptr, k, status[k]};
+        },
+        workspace, stream);
+    if (rc != KB_OK) return rc;
+
+    char* ws = (char*)workspace;
+    const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
+    hipError_t e;
+    if (n_acc == 0 || numel == 0) {
+        e = launch_records_only(d_table, n_cands, numel, d_stats, stream);
+        if (e != hipSuccess) return fail_hip(e, "kb_screen: records launch");
+        return KB_OK;
+    }
+    ScreenParams p{};
+    p.ref = ref->data;
+    p.table = d_table;
+    p.numel = numel;
+    p.n_vec = P.n_vec;
+    p.atol = atol;
+    p.rtol = rtol;
+    p.flags = flags;
+    p.n_acc = n_acc;
+    p.n_cands = n_cands;
+    p.n_groups = P.n_groups;
+    p.blocks_per_group = P.blocks_per_group;
+    p.tickets = (uint32_t*)(ws + P.off_tickets);
+    p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
+    p.part_ssd = (double*)(ws + P.off_part_ssd);
+    p.part_ssr = (double*)(ws + P.off_part_ssr);
+    p.stats = d_stats;
+    e = launch_screen(P, p, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen: kernel launch");
+    return KB_OK;
+}
+
+int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats, kb_summary* summary,
+                    hipStream_t stream) {
+    clear_error();
+    if (d_stats == nullptr || n_cands < 0)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_stats: null d_stats or negative count");
+    std::vector<kb_stats> tmp;
+    kb_stats* dst = h_stats;
+    if (dst == nullptr) {
+        tmp.resize((size_t)n_cands);
+        dst = tmp.data();
+    }
+    if (n_cands > 0) {
+        hipError_t e = hipMemcpyAsync(dst, d_stats, (size_t)n_cands * sizeof(kb_stats),
+                                      hipMemcpyDeviceToHost, stream);
+        if (e != hipSuccess) return fail_hip(e, "kb_screen_stats: hipMemcpyAsync");
+    }
+    hipError_t e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen_stats: hipStreamSynchronize");
+    if (summary) {
+        kb_summary s{n_cands, 0, 0, 0, -1, -1};
+        for (int k = 0; k < n_cands; ++k) {
+            const kb_stats& st = dst[k];
+            if (st.status != KB_STATUS_OK) {
+                s.n_rejected++;
+            } else if (st.mismatches == 0) {
+                s.n_passed++;
+                if (s.first_passed < 0) s.first_passed = k;
+                continue;
+            } else {
+                s.n_failed++;
+            }
+            if (s.first_failed < 0) s.first_failed = k;
+        }
+        *summary = s;
+    }
+    return KB_OK;
+}
+
+int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1, uint64_t seed,
+                  uint32_t stream_id, uint32_t sub, uint64_t offset, hipStream_t stream) {
+    clear_error();
+    if (dtype < DT_F32 || dtype > DT_U32) return fail(KB_ERR_DTYPE, "unknown dtype %d", dtype);
+    if (dist < KB_DIST_U32 || dist > KB_DIST_NORMAL)
+        return fail(KB_ERR_INVALID_ARG, "unknown distribution %d", dist);
+    if ((dist == KB_DIST_U32) != (dtype == DT_U32))
+        return fail(KB_ERR_DTYPE, "distribution %d does not produce dtype %d", dist, dtype);
+    if (!std::isfinite(p0) || !std::isfinite(p1))
+        return fail(KB_ERR_INVALID_ARG, "p0 and p1 must be finite");
+    if (n == 0) return KB_OK;
+    if (dst == nullptr) return fail(KB_ERR_INVALID_ARG, "dst is NULL");
+    if (!aligned16(dst)) return fail(KB_ERR_ALIGNMENT, "dst not 16-byte aligned");
+    if (offset + n < offset) return fail(KB_ERR_INVALID_ARG, "offset + n overflows");
+    hipError_t e = launch_gen(dst, dtype, n, dist, p0, p1, seed, stream_id, sub, offset, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_gen_inputs: kernel launch");
+    return KB_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+"""Shared helpers for the GPU parity tests: building, host copies of device
+tensors, chunked oracle screening, and record comparison."""
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+import oracle
+
+EXACT_FIELDS = ("numel", "mismatches", "nan_count", "pos_inf_count", "neg_inf_count",
+                "max_abs_err", "max_rel_err", "bitwise_equal", "passed")
+SUM_FIELDS = ("sum_sq_diff", "sum_sq_ref", "rel_l2")
+SUM_RTOL = 1e-6  # relative tolerance of the binary64 sums and the relative L2 error
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def ensure_built():
+    import __graft_entry__
+    __graft_entry__._ensure_built()
+
+
+def dtype_name(t):
+    import torch
+    return {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[t.dtype]
+
+
+def storage(t):
+    """Host numpy array of the raw storage of a (device) tensor."""
+    import torch
+    t = t.detach().contiguous().view(-1)
+    if t.dtype == torch.float32:
+        return t.cpu().numpy()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def oracle_records(ref, cands, atol, rtol, flags=0, chunk=1 << 24):
+    """Oracle statistics of every candidate (chunked over elements and run on
+    host threads for large tensors; merged in chunk order)."""
+    dt = dtype_name(ref)
+    n = ref.numel()
+    if n <= chunk:
+        r = storage(ref)
+        return [oracle.screen(r, storage(c), dt, atol, rtol, flags) for c in cands]
+    bounds = [(lo, min(n, lo + chunk)) for lo in range(0, n, chunk)]
+    partials = [[None] * len(bounds) for _ in cands]
+    rflat = ref.reshape(-1)
+    with ThreadPoolExecutor(THREADS) as ex:
+        for bi, (lo, hi) in enumerate(bounds):
+            r = storage(rflat[lo:hi])
+            cs = [storage(c.reshape(-1)[lo:hi]) for c in cands]
+            futs = [ex.submit(oracle.screen_partial, r, cs[k], dt, atol, rtol, flags)
+                    for k in range(len(cands))]
+            for k, f in enumerate(futs):
+                partials[k][bi] = f.result()
+    return [oracle.finalize(oracle.merge(p)) for p in partials]
+
+
+def close(a, b, rtol=SUM_RTOL):
+    if math.isnan(a) or math.isnan(b):
+        return math.isnan(a) and math.isnan(b)
+    if math.isinf(a) or math.isinf(b):
+        return a == b
+    return abs(a - b) <= rtol * abs(b)
+
+
+def assert_records_match(gpu, orc, label=""):
+    assert len(gpu) == len(orc)
+    bad = []
+    for k, (g, o) in enumerate(zip(gpu, orc)):
+        assert g["status"] == 0, (label, k, g)
+        for f in EXACT_FIELDS:
+            if g[f] != o[f] and not (isinstance(o[f], float) and math.isnan(o[f]) and math.isnan(g[f])):
+                bad.append((k, f, g[f], o[f]))
+        for f in SUM_FIELDS:
+            if not close(g[f], o[f]):
+                bad.append((k, f, g[f], o[f]))
+    assert not bad, "%s: %d mismatching fields, first %s" % (label, len(bad), bad[:8])

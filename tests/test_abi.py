@@ -1,0 +1,179 @@
+"""The C interface without a GPU: library loading, exported symbols, and the
+argument checks and policy gate that run on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_02611_amd as kb
+from tests.helpers import ensure_built
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    ensure_built()
+    return kb.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "kb.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kb_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(L):
+    names = declared_functions()
+    assert set(kb.EXPORTS) <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_version(L):
+    assert kb.kb_version() == 100
+
+
+def desc(data, dtype, shape, strides=None):
+    t = kb.KbTensor()
+    t.data = data
+    t.dtype = dtype
+    t.ndim = len(shape)
+    if strides is None:
+        strides, acc = [], 1
+        for s in reversed(shape):
+            strides.insert(0, acc)
+            acc *= s
+    for i, (s, st) in enumerate(zip(shape, strides)):
+        t.shape[i] = s
+        t.strides[i] = st
+    return t
+
+
+def gate(ref, cands):
+    arr = (kb.KbTensor * len(cands))(*cands)
+    st = (ctypes.c_int32 * len(cands))()
+    rc = kb.lib().kb_policy_check(ctypes.byref(ref), arr, len(cands), st)
+    return rc, list(st)
+
+
+def test_policy_gate_statuses(L):
+    ref = desc(0x10000, kb.KB_F32, (4, 8))
+    cands = [
+        desc(0x20000, kb.KB_F32, (4, 8)),                     # ok
+        desc(None, kb.KB_F32, (4, 8)),                        # null
+        desc(0x30000, kb.KB_F16, (4, 8)),                     # dtype
+        desc(0x40000, kb.KB_F32, (8, 4)),                     # shape
+        desc(0x50000, kb.KB_F32, (32,)),                      # ndim
+        desc(0x60000, kb.KB_F32, (4, 8), strides=(16, 2)),    # layout
+        desc(0x70000, kb.KB_F32, (4, 8), strides=(1, 4)),     # transposed layout
+        desc(0x80000, kb.KB_F32, (4, 1, 8), ),                # ndim differs
+    ]
+    rc, st = gate(ref, cands)
+    assert rc == kb.KB_OK
+    assert st == [kb.KB_STATUS_OK, kb.KB_REJECT_NULL, kb.KB_REJECT_DTYPE, kb.KB_REJECT_SHAPE,
+                  kb.KB_REJECT_SHAPE, kb.KB_REJECT_LAYOUT, kb.KB_REJECT_LAYOUT,
+                  kb.KB_REJECT_SHAPE]
+
+
+def test_policy_gate_size_one_dims_and_empty(L):
+    ref = desc(0x10000, kb.KB_BF16, (1, 5, 1))
+    ok = desc(0x20000, kb.KB_BF16, (1, 5, 1), strides=(999, 1, 7))  # size-1 strides free
+    rc, st = gate(ref, [ok])
+    assert rc == kb.KB_OK and st == [kb.KB_STATUS_OK]
+    ref0 = desc(0x10000, kb.KB_F16, (0, 3))
+    rc, st = gate(ref0, [desc(0x20000, kb.KB_F16, (0, 3), strides=(5, 5))])
+    assert rc == kb.KB_OK and st == [kb.KB_STATUS_OK]
+
+
+def test_policy_gate_call_errors(L):
+    ref = desc(0x10000, kb.KB_U32, (4,))
+    rc, _ = gate(ref, [desc(0x20000, kb.KB_U32, (4,))])
+    assert rc == kb.KB_ERR_DTYPE and "dtype" in kb.kb_last_error()
+    ref = desc(None, kb.KB_F32, (4,))
+    rc, _ = gate(ref, [desc(0x20000, kb.KB_F32, (4,))])
+    assert rc == kb.KB_ERR_INVALID_ARG
+
+
+def screen_rc(ref, cands, atol=1e-5, rtol=1e-5, flags=0, ws=0x100000, ws_bytes=1 << 30,
+              stats=0x200000):
+    arr = (kb.KbTensor * max(1, len(cands)))(*cands)
+    return kb.lib().kb_screen(ctypes.byref(ref) if ref is not None else None, arr, len(cands),
+                              atol, rtol, flags, ws, ws_bytes, stats, None)
+
+
+def test_screen_argument_errors(L):
+    ref = desc(0x10000, kb.KB_F32, (64,))
+    good = [desc(0x20000, kb.KB_F32, (64,))]
+    assert screen_rc(None, good) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, []) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, atol=-1.0) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, rtol=float("nan")) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, atol=float("inf")) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, flags=2) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, stats=None) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(desc(0x10000, kb.KB_U32, (64,)), good) == kb.KB_ERR_DTYPE
+    assert screen_rc(ref, good, ws_bytes=16) == kb.KB_ERR_WORKSPACE
+    assert screen_rc(ref, good, ws=None) == kb.KB_ERR_WORKSPACE
+    assert screen_rc(desc(0x10004, kb.KB_F32, (64,)), good) == kb.KB_ERR_ALIGNMENT
+    assert screen_rc(ref, [desc(0x20008, kb.KB_F32, (64,))]) == kb.KB_ERR_ALIGNMENT
+    assert screen_rc(ref, good, ws=0x100008) == kb.KB_ERR_ALIGNMENT
+    assert screen_rc(ref, good, stats=0x200004) == kb.KB_ERR_ALIGNMENT
+    assert screen_rc(desc(0x10000, kb.KB_F32, (8, 8), strides=(1, 8)), good) == kb.KB_ERR_INVALID_ARG
+    assert "contiguous" in kb.kb_last_error()
+
+
+def test_rejected_misaligned_candidate_is_not_an_error_source(L):
+    # a candidate that fails the gate is not read, so its pointer may be anything
+    ref = desc(0x10000, kb.KB_F32, (64,))
+    bad = desc(0x20002, kb.KB_F16, (64,))
+    # the call still fails later for lack of a GPU, but not with an alignment error
+    rc = screen_rc(ref, [bad], ws_bytes=16)
+    assert rc == kb.KB_ERR_WORKSPACE
+
+
+def test_workspace_and_launch_plan(L):
+    for K, n, dt in [(4, 65536, kb.KB_F32), (16, 4096 * 4096, kb.KB_BF16),
+                     (1024, 256 * 1024, kb.KB_F32), (64, 8 * 2048 * 4096, kb.KB_F16),
+                     (8, 1 << 30, kb.KB_F32), (1, 0, kb.KB_F32), (3, 7, kb.KB_F16)]:
+        ws = kb.kb_screen_workspace_bytes(K, n, dt)
+        assert ws > 0 and ws % 256 == 0
+        plan = kb.kb_screen_launch(K, n, dt)
+        assert plan["blocks_per_group"] % 8 == 0
+        assert plan["group_size"] * plan["n_groups"] >= K
+        assert plan["grid"] == plan["n_groups"] * plan["blocks_per_group"]
+        # one work-group never holds 2^31 or more elements of one candidate
+        assert n / plan["blocks_per_group"] < 2 ** 31
+    assert kb.kb_screen_workspace_bytes(0, 10, kb.KB_F32) == 0
+    assert kb.kb_screen_workspace_bytes(4, 10, kb.KB_U32) == 0
+    with pytest.raises(kb.KbError):
+        kb.kb_screen_launch(4, 10, kb.KB_U32)
+
+
+def test_gen_argument_errors(L):
+    g = kb.lib().kb_gen_inputs
+    assert g(0x1000, kb.KB_F32, 16, kb.KB_DIST_U32, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_DTYPE
+    assert g(0x1000, kb.KB_U32, 16, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_DTYPE
+    assert g(0x1000, 7, 16, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_DTYPE
+    assert g(0x1000, kb.KB_F32, 16, 9, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert g(0x1000, kb.KB_F32, 16, kb.KB_DIST_NORMAL, float("nan"), 1.0, 0, 0, 0, 0,
+             None) == kb.KB_ERR_INVALID_ARG
+    assert g(None, kb.KB_F32, 16, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert g(0x1004, kb.KB_F32, 16, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_ALIGNMENT
+    assert g(0x1000, kb.KB_F32, 16, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 2**64 - 4,
+             None) == kb.KB_ERR_INVALID_ARG
+    # n = 0 is a no-op: no launch, no error
+    assert g(None, kb.KB_F32, 0, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_OK
+
+
+def test_stats_argument_errors(L):
+    assert kb.lib().kb_screen_stats(None, 4, None, None, None) == kb.KB_ERR_INVALID_ARG
+    assert kb.lib().kb_screen_stats(0x1000, -1, None, None, None) == kb.KB_ERR_INVALID_ARG
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(kb, "_lib", None)
+    monkeypatch.setattr(kb, "LIB_PATH", "/nonexistent/libkb.so")
+    with pytest.raises(kb.KbError):
+        kb.lib()

@@ -1,0 +1,274 @@
+"""Parity of the HIP screening path with the CPU oracle (GPU).
+
+Every case hands the same bytes to the library (on the GPU, through the C
+interface) and to the oracle (host copy), then compares every record field:
+counts, flags and maxima exactly, the binary64 sums and the relative L2 error
+within 1e-6 relative.
+"""
+import math
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_02611_amd as kb
+import synth
+from tests.helpers import THREADS, assert_records_match, ensure_built, oracle_records, storage
+
+pytestmark = pytest.mark.gpu
+
+TORCH_DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    ensure_built()
+    return torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(arr, dt, dev):
+    """numpy storage (float32 or uint16 bits) -> device tensor of dtype dt."""
+    if dt == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(dev)
+    bits = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint16).view(np.int16)).to(dev)
+    return bits.view(TORCH_DT[dt])
+
+
+def run_case(ref, cands, atol, rtol, flags=0, label=""):
+    recs, _ = kb.screen(ref, cands, atol, rtol, flags)
+    orc = oracle_records(ref, cands, atol, rtol, flags)
+    assert_records_match(recs, orc, label)
+    return recs
+
+
+# ------------------------------------------------------------ hand cases ---
+
+INF, NAN = float("inf"), float("nan")
+HAND = [
+    # (dtype, ref values, cand values, atol, rtol, flags)
+    ("f32", [0.0], [-0.0], 0.0, 0.0, 0),
+    ("f32", [1.0], [NAN], 1e-5, 1e-5, 0),
+    ("f32", [INF], [INF], 1e-5, 1e-5, 0),
+    ("f32", [INF], [-INF], 1e-5, 1e-5, 0),
+    ("f32", [INF], [5.0], 1e-5, 1e-5, 0),
+    ("f32", [0.0], [1.0], 0.0, 0.5, 0),
+    ("f32", [1.0, 1.0], [1.0 + 2**-10, 1.0 + 2**-10 + 2**-23], 0.0, 2**-10, 0),
+    ("f32", [2.0**-149], [0.0], 0.0, 0.5, 0),
+    ("f32", [2.0**-149], [2.0**-148], 1e-8, 0.0, 0),
+    ("f32", [1, 2, 3, 4, 5, 6, 7, 8], [1, NAN, INF, -INF, 5.1, 6, 7, 8], 1e-5, 1e-5, 0),
+    ("f32", [NAN], [NAN], 1e-5, 1e-5, 0),
+    ("f32", [NAN], [NAN], 1e-5, 1e-5, kb.KB_EQUAL_NAN),
+    ("f32", [1.0], [NAN], 1e-5, 1e-5, kb.KB_EQUAL_NAN),
+    ("f32", [1000.0, 1e-3], [1001.0, 2e-3], 0.0, 0.0, 0),
+    ("f32", [3.0, 4.0], [3.5, 4.0], 0.0, 0.0, 0),
+    ("f32", [3.4028234663852886e38, -3.4028234663852886e38], [-3.4028234663852886e38, INF], 1e-5, 1e-5, 0),
+]
+
+
+@pytest.mark.parametrize("case", range(len(HAND)))
+def test_hand_cases(dev, case):
+    dt, r, c, atol, rtol, flags = HAND[case]
+    say("hand case", case, HAND[case])
+    ref = to_dev(np.array(r, dtype=np.float32), dt, dev)
+    cand = to_dev(np.array(c, dtype=np.float32), dt, dev)
+    run_case(ref, [cand], atol, rtol, flags, "hand %d" % case)
+
+
+def test_hand_16bit(dev):
+    say("hand 16-bit cases")
+    ref = to_dev(np.array([0x7BFF], dtype=np.uint16), "f16", dev)
+    cand = to_dev(np.array([0x7C00], dtype=np.uint16), "f16", dev)
+    run_case(ref, [cand], 1e-3, 1e-3, 0, "f16 overflow")
+    ref = to_dev(np.array([0x3F80], dtype=np.uint16), "bf16", dev)
+    cand = to_dev(np.array([0x3F81], dtype=np.uint16), "bf16", dev)
+    run_case(ref, [cand], 1e-2, 1e-2, 0, "bf16 ulp")
+
+
+# ------------------------------------------------------ random, ragged ---
+
+SPECIAL_F32 = np.array([0.0, -0.0, 2.0**-149, -(2.0**-149), 2.0**-126, 1e-30, np.inf, -np.inf,
+                        np.nan, 3.4028234663852886e38, 65504.0, 1e-8], dtype=np.float32)
+
+
+def random_pair(rng, dt, n, K):
+    """Reference and K candidates with perturbations at many scales and
+    injected special values."""
+    if dt == "f32":
+        r = (rng.standard_normal(n) * np.exp(rng.uniform(-8, 8, n))).astype(np.float32)
+    else:
+        r32 = rng.standard_normal(n).astype(np.float32) * np.float32(4.0)
+        r = oracle.f32_to_f16_n(r32) if dt == "f16" else oracle.f32_to_bf16_n(r32)
+    spec_idx = rng.random(n) < 0.01
+    if dt == "f32":
+        r[spec_idx] = rng.choice(SPECIAL_F32, size=int(spec_idx.sum()))
+    else:
+        r[spec_idx] = rng.integers(0, 1 << 16, size=int(spec_idx.sum())).astype(np.uint16)
+    cands = []
+    for k in range(K):
+        c = r.copy()
+        mode = k % 5
+        if dt == "f32":
+            if mode == 1:
+                c = (r * (1 + rng.uniform(-1e-5, 1e-5, n))).astype(np.float32)
+            elif mode == 2:
+                c = (r + rng.standard_normal(n).astype(np.float32) * np.float32(1e-3)).astype(np.float32)
+            elif mode == 3:
+                m = rng.random(n) < 0.02
+                c[m] = rng.choice(SPECIAL_F32, size=int(m.sum()))
+            elif mode == 4:
+                c = c.view(np.uint32) ^ (rng.random(n) < 0.05).astype(np.uint32)
+                c = c.view(np.float32)
+        else:
+            if mode in (1, 2):
+                flip = rng.random(n) < (0.05 if mode == 1 else 0.5)
+                c = c ^ (flip * rng.integers(1, 1 << (3 + mode * 3), size=n)).astype(np.uint16)
+            elif mode == 3:
+                m = rng.random(n) < 0.02
+                c[m] = rng.integers(0, 1 << 16, size=int(m.sum())).astype(np.uint16)
+            elif mode == 4:
+                c = c ^ (rng.random(n) < 0.001).astype(np.uint16)
+        cands.append(c)
+    return r, cands
+
+
+SIZES = [1, 3, 7, 8, 9, 63, 255, 256, 257, 1023, 4095, 4096, 4099, 65536 + 5, (1 << 20) + 13]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_random_ragged(dev, dt):
+    rng = np.random.default_rng({"f32": 1, "f16": 2, "bf16": 3}[dt])
+    for n in SIZES:
+        for K in (1, 3, 9, 17):
+            if n > 100000 and K > 9:
+                continue
+            say("random", dt, "n", n, "K", K)
+            r, cs = random_pair(rng, dt, n, K)
+            atol, rtol = (1e-5, 1e-5) if dt == "f32" else (1e-3, 1e-3)
+            ref = to_dev(r, dt, dev)
+            cands = [to_dev(c, dt, dev) for c in cs]
+            run_case(ref, cands, atol, rtol, int(rng.integers(0, 2)), "%s n=%d K=%d" % (dt, n, K))
+
+
+# ----------------------------------------------- the five workloads ---
+
+SCALED = [("c1", 1.0, None), ("c2", 1 / 64, None), ("c3", 1.0, None), ("c4", 1 / 64, None),
+          ("c5", 1 / 256, None)]
+
+
+@pytest.mark.parametrize("name,scale,K", SCALED)
+def test_workloads_scaled(dev, name, scale, K):
+    say("workload", name, "scale", scale)
+    w = synth.build(name, dev, seed=0, scale=scale, K=K)
+    run_case(w.ref, w.cands, w.atol, w.rtol, 0, name)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_workloads_full_size(dev, name):
+    # the exact sizes and launch configuration the benchmark times
+    say("full-size workload", name, kb.kb_screen_launch(synth.SPECS[name]["K"],
+                                                       math.prod(synth.SPECS[name]["shape"]),
+                                                       {torch.float32: 0, torch.float16: 1,
+                                                        torch.bfloat16: 2}[synth.SPECS[name]["dtype"]]))
+    w = synth.build(name, dev, seed=0)
+    torch.cuda.synchronize()
+    run_case(w.ref, w.cands, w.atol, w.rtol, 0, name + " full")
+    del w
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------- policy gate ---
+
+def test_policy_gate_rejects_and_others_unaffected(dev):
+    say("policy gate")
+    g = torch.Generator(device=dev).manual_seed(5)
+    ref = torch.randn(1000, generator=g, device=dev)
+    good = ref + 1e-7
+    wide = torch.randn(2000, generator=g, device=dev)
+    cands = [good, ref.half(), ref[:999].clone(), ref.view(10, 100).clone(), wide[::2], None,
+             ref.clone()]
+    recs, summ = kb.screen(ref, cands, 1e-5, 1e-5)
+    assert [r["status"] for r in recs] == [0, kb.KB_REJECT_DTYPE, kb.KB_REJECT_SHAPE,
+                                          kb.KB_REJECT_SHAPE, kb.KB_REJECT_LAYOUT,
+                                          kb.KB_REJECT_NULL, 0]
+    for k in (1, 2, 3, 4, 5):
+        r = recs[k]
+        assert r["numel"] == 0 and r["mismatches"] == 0 and r["bitwise_equal"] == 0
+        assert r["passed"] == 0
+    assert summ == {"n_candidates": 7, "n_passed": 2, "n_rejected": 5, "n_failed": 0,
+                    "first_passed": 0, "first_failed": 1}
+    orc = oracle_records(ref, [good, cands[6]], 1e-5, 1e-5)
+    assert_records_match([recs[0], recs[6]], orc, "gate survivors")
+
+
+def test_all_rejected_and_empty(dev):
+    say("all rejected / empty")
+    ref = torch.zeros(16, device=dev)
+    recs, summ = kb.screen(ref, [None, ref.half()], 0.0, 0.0)
+    assert [r["status"] for r in recs] == [kb.KB_REJECT_NULL, kb.KB_REJECT_DTYPE]
+    assert summ["n_rejected"] == 2
+    e = torch.empty(0, device=dev)
+    recs, summ = kb.screen(e, [e.clone(), e.clone()], 1e-5, 1e-5)
+    for r in recs:
+        assert r["status"] == 0 and r["numel"] == 0 and r["bitwise_equal"] == 1 and r["passed"] == 1
+    assert summ["n_passed"] == 2
+
+
+# --------------------------------------------------- determinism & reuse ---
+
+def test_determinism_and_dirty_workspace(dev):
+    say("determinism")
+    w = synth.build("c2", dev, seed=1, scale=1 / 16)
+    K = len(w.cands)
+    ws = kb.alloc_workspace(K, w.numel, kb.KB_BF16, dev)
+    st = kb.alloc_stats(K, dev)
+    first = None
+    for it in range(20):
+        ws.fill_(0xFF if it % 2 else 0x5A)  # contents must not matter
+        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, 0, ws, st)
+        recs, _ = kb.kb_screen_stats(st, K)
+        if first is None:
+            first = recs
+        else:
+            assert recs == first, it
+    assert_records_match(first, oracle_records(w.ref, w.cands, w.atol, w.rtol), "c2 1/16")
+
+
+def test_stream_ordering_with_side_stream(dev):
+    say("side stream")
+    s = torch.cuda.Stream()
+    w = synth.build("c1", dev, seed=3)
+    with torch.cuda.stream(s):
+        recs, _ = kb.screen(w.ref, w.cands, w.atol, w.rtol, stream=s)
+    assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), "side stream")
+
+
+# ------------------------------------------------ exhaustive 16-bit pairs ---
+
+@pytest.mark.parametrize("dt,tol", [("f16", 1e-3), ("bf16", 1e-2)])
+def test_exhaustive_16bit_pairs(dev, dt, tol):
+    """All 2^16 x 2^16 (candidate, reference) bit patterns: the reference holds
+    every pattern once; candidate k is the constant pattern k."""
+    say("exhaustive", dt)
+    allbits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ref = to_dev(allbits, dt, dev)
+    batch = 4096
+    bits_dev = torch.from_numpy(allbits.view(np.int16)).to(dev)
+    for b0 in range(0, 1 << 16, batch):
+        rows = bits_dev[b0:b0 + batch].view(-1, 1).expand(-1, 1 << 16).contiguous()
+        cands = [rows[i].view(TORCH_DT[dt]) for i in range(rows.shape[0])]
+        recs, _ = kb.screen(ref, cands, tol, tol)
+
+        def one(i):
+            return oracle.screen(allbits, np.full(1 << 16, b0 + i, dtype=np.uint16), dt, tol, tol)
+
+        with ThreadPoolExecutor(THREADS) as ex:
+            orc = list(ex.map(one, range(rows.shape[0])))
+        assert_records_match(recs, orc, "%s exhaustive batch %d" % (dt, b0))
