@@ -178,8 +178,20 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
 /* ---------------------------------------------------------------- screen -- */
 
 /* Bytes of device workspace kb_screen needs for n_cands candidates of numel
- * elements of dtype (0 on invalid arguments). */
+ * elements of dtype (0 on invalid arguments).  A pure function of its
+ * arguments (no device query). */
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype);
+
+/* Zero-fill a workspace (a fill kernel, stream-ordered; no memset node, so
+ * it may be captured in a graph).  A workspace must be initialised this way
+ * (or zero-filled otherwise) after it is allocated, and again before it is
+ * used for a call with different (n_cands, numel, dtype) or after anything
+ * else wrote to it: kb_screen keeps cross-work-group counters in it and
+ * leaves them zero when the call completes, so consecutive calls with the
+ * same sizes need no re-initialisation.
+ *   workspace: device, 16-byte aligned; workspace_bytes: multiple of 16.
+ * Errors: KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_screen_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* The launch kb_screen would use for these sizes (KB_ERR_* on bad args). */
 int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
@@ -193,10 +205,14 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
  *   atol, rtol   finite, >= 0 (binary32);
  *   flags        0 or KB_EQUAL_NAN;
  *   workspace    device scratch of workspace_bytes >=
- *                kb_screen_workspace_bytes(n_cands, numel, dtype); its
- *                contents need no initialisation; one workspace must not be
- *                used by two calls that can run concurrently;
- *   d_stats      device array of n_cands kb_stats, written by the call.
+ *                kb_screen_workspace_bytes(n_cands, numel, dtype),
+ *                initialised by kb_screen_workspace_init (see there); one
+ *                workspace must not be used by two calls that can run
+ *                concurrently;
+ *   d_stats      n_cands kb_stats written by the kernel: device memory, or
+ *                pinned host memory mapped for the device (hipHostMalloc),
+ *                which lets a pipelined caller read the records without a
+ *                copy once the stream has passed the call.
  * Candidate k's record goes to d_stats[k].  Returns KB_OK once the work is
  * enqueued.  Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_DTYPE,
  * KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT (reference, accepted candidate,
@@ -204,6 +220,9 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
 int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
               float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
               kb_stats* d_stats, hipStream_t stream);
+
+/* Verdict summary of n_cands records already in host memory (host only). */
+int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary);
 
 /* Copy n_cands records from device d_stats to host h_stats (may be NULL),
  * synchronize `stream`, and fill *summary (may be NULL).  This is the

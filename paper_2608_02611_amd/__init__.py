@@ -77,8 +77,9 @@ class KbLaunch(ctypes.Structure):
 assert ctypes.sizeof(KbStats) == 80
 assert ctypes.sizeof(KbTensor) == 144
 
-EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_launch", "kb_screen",
-           "kb_screen_stats", "kb_gen_inputs", "kb_last_error", "kb_version")
+EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
+           "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
+           "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -97,6 +98,10 @@ def lib():
         L.kb_policy_check.restype = i32
         L.kb_screen_workspace_bytes.argtypes = [i32, u64, i32]
         L.kb_screen_workspace_bytes.restype = ctypes.c_size_t
+        L.kb_screen_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
+        L.kb_screen_workspace_init.restype = i32
+        L.kb_summarize.argtypes = [ctypes.POINTER(KbStats), i32, ctypes.POINTER(KbSummary)]
+        L.kb_summarize.restype = i32
         L.kb_screen_launch.argtypes = [i32, u64, i32, ctypes.POINTER(KbLaunch)]
         L.kb_screen_launch.restype = i32
         L.kb_screen.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
@@ -193,12 +198,21 @@ def kb_screen_launch(n_cands, numel, dtype):
     return out.as_dict()
 
 
-def alloc_workspace(n_cands, numel, dtype, device):
+def kb_screen_workspace_init(workspace, stream=None):
+    """Zero-fill a workspace tensor with the library's fill kernel."""
+    _check(lib().kb_screen_workspace_init(ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                          _stream_handle(stream)))
+    return workspace
+
+
+def alloc_workspace(n_cands, numel, dtype, device, stream=None):
+    """A workspace for these sizes, initialised (zero-filled) by the library."""
     torch = _torch()
     nbytes = kb_screen_workspace_bytes(n_cands, numel, dtype)
     if nbytes == 0:
         raise KbError(KB_ERR_INVALID_ARG, "no workspace size for these arguments")
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return kb_screen_workspace_init(ws, stream)
 
 
 def alloc_stats(n_cands, device):
@@ -217,7 +231,7 @@ def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, str
     arr = (KbTensor * max(1, n))(*[describe(c) for c in cands])
     if workspace is None:
         workspace = alloc_workspace(max(1, n), ref.numel(), r.dtype if r.dtype >= 0 else 0,
-                                    ref.device)
+                                    ref.device, stream)
     if d_stats is None:
         d_stats = alloc_stats(max(1, n), ref.device)
     _check(lib().kb_screen(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
@@ -245,6 +259,21 @@ def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=
     return dst
 
 
+def kb_summarize(records):
+    """Verdict summary (dict) of a list of record dicts or a KbStats array."""
+    if isinstance(records, list):
+        arr = (KbStats * max(1, len(records)))()
+        for k, r in enumerate(records):
+            for name, _ in KbStats._fields_:
+                setattr(arr[k], name, r[name])
+        n = len(records)
+    else:
+        arr, n = records, len(records)
+    summ = KbSummary()
+    _check(lib().kb_summarize(arr, n, ctypes.byref(summ)))
+    return summ.as_dict()
+
+
 def screen(ref, cands, atol, rtol, flags=0, stream=None):
     """Gate + screen + readback: (list of per-candidate dicts, summary dict)."""
     d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)
@@ -253,38 +282,63 @@ def screen(ref, cands, atol, rtol, flags=0, stream=None):
 
 class Screener:
     """Repeated screening of one fixed set of buffers with the argument
-    marshalling done once: descriptors, workspace, device records and the
-    host readback buffer are built at construction and reused by every
-    launch()/read() pair."""
+    marshalling done once: descriptors, workspace, record buffers and the
+    stream handle are built at construction and reused by every launch.
 
-    def __init__(self, ref, cands, atol, rtol, flags=0, stream=None):
+    host_slots > 0 places the records in that many pinned host buffers that
+    the kernel writes directly (a pipelined caller launches into one slot and
+    summarizes another after an event); otherwise they go to device memory
+    and read() copies them back."""
+
+    def __init__(self, ref, cands, atol, rtol, flags=0, stream=None, host_slots=0):
+        torch = _torch()
         self.ref, self.cands = ref, list(cands)
         self.n = len(self.cands)
         self.atol, self.rtol, self.flags = float(atol), float(rtol), int(flags)
-        self._ref = describe(ref)
-        self._arr = (KbTensor * max(1, self.n))(*[describe(c) for c in self.cands])
-        self.workspace = alloc_workspace(max(1, self.n), ref.numel(), self._ref.dtype, ref.device)
-        self.d_stats = alloc_stats(max(1, self.n), ref.device)
-        self._host = (KbStats * max(1, self.n))()
-        self._summary = KbSummary()
         self.stream = stream
         self._stream = _stream_handle(stream)
+        self._ref = describe(ref)
+        self._arr = (KbTensor * max(1, self.n))(*[describe(c) for c in self.cands])
+        self.workspace = alloc_workspace(max(1, self.n), ref.numel(), self._ref.dtype, ref.device,
+                                         stream)
         self._ws = ctypes.c_void_p(self.workspace.data_ptr())
-        self._st = ctypes.c_void_p(self.d_stats.data_ptr())
+        nbytes = max(1, self.n) * ctypes.sizeof(KbStats)
+        if host_slots > 0:
+            self.slots = [torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+                          for _ in range(host_slots)]
+            self._views = [ctypes.cast(ctypes.c_void_p(t.data_ptr()), ctypes.POINTER(KbStats))
+                           for t in self.slots]
+        else:
+            self.slots = [alloc_stats(max(1, self.n), ref.device)]
+            self._views = None
+        self._slot_ptr = [ctypes.c_void_p(t.data_ptr()) for t in self.slots]
+        self._host = (KbStats * max(1, self.n))()
+        self._summary = KbSummary()
         self._L = lib()
 
-    def launch(self):
-        _check(self._L.kb_screen(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
-                                 self.flags, self._ws, self.workspace.numel(), self._st,
-                                 self._stream))
+    @property
+    def d_stats(self):
+        return self.slots[0]
 
-    def read(self):
-        _check(self._L.kb_screen_stats(self._st, self.n, self._host, ctypes.byref(self._summary),
-                                       self._stream))
+    def launch(self, slot=0):
+        _check(self._L.kb_screen(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
+                                 self.flags, self._ws, self.workspace.numel(),
+                                 self._slot_ptr[slot], self._stream))
+
+    def read(self, slot=0):
+        """Copy the records back (synchronizes the stream); returns the summary."""
+        _check(self._L.kb_screen_stats(self._slot_ptr[slot], self.n, self._host,
+                                       ctypes.byref(self._summary), self._stream))
         return self._summary
 
-    def records(self):
-        return [self._host[k].as_dict() for k in range(self.n)]
+    def summarize(self, slot):
+        """Summary of a pinned host slot; the caller has synchronized past the launch."""
+        _check(self._L.kb_summarize(self._views[slot], self.n, ctypes.byref(self._summary)))
+        return self._summary
+
+    def records(self, slot=None):
+        src = self._host if slot is None else self._views[slot]
+        return [src[k].as_dict() for k in range(self.n)]
 
     def launch_plan(self):
         return kb_screen_launch(max(1, self.n), self.ref.numel(), self._ref.dtype)

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -77,6 +78,20 @@ int32_t gate_one(const kb_tensor& ref, const kb_tensor& c) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Launch tuning override for measurement sweeps: KB_SCREEN_TUNE="kg=16,blocks=1024"
+// caps the candidates per group (1, 2, 4, 8 or 16) and sets the target total
+// number of work-groups.  Unset, the built-in choice applies.
+void tuning_override(int* kg_cap, int* blocks_total) {
+    const char* s = std::getenv("KB_SCREEN_TUNE");
+    if (s == nullptr) return;
+    int v;
+    const char* k = std::strstr(s, "kg=");
+    if (k && std::sscanf(k + 3, "%d", &v) == 1 && (v == 1 || v == 2 || v == 4 || v == 8 || v == 16))
+        *kg_cap = v;
+    const char* b = std::strstr(s, "blocks=");  // 0 or absent: occupancy-based
+    if (b && std::sscanf(b + 7, "%d", &v) == 1 && v >= 8 && v <= (1 << 20)) *blocks_total = v;
+}
+
 // ---------------------------------------------------------------------------
 // Pinned host staging ring for launch-table uploads.  A slot is reused only
 // after the copy that last read it has completed (its event), so callers may
@@ -149,7 +164,27 @@ Staging& staging() {
 // ---------------------------------------------------------------------------
 // Launch plan.
 // ---------------------------------------------------------------------------
-bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, ScreenPlan* plan) {
+
+// Work-groups of the screening kernel for (dtype, kg) resident on the
+// current device at once; 0 if the device cannot be queried (then the plan
+// falls back to a fixed total).
+int resident_blocks(int dtype, int kg) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return cus * screen_blocks_per_cu(dtype, kg);
+}
+int plan_group_size(int n_cands) {
+    int kg_cap = 8, blocks_total = 0;
+    tuning_override(&kg_cap, &blocks_total);
+    int kg = 1;
+    while (kg < n_cands && kg < kg_cap) kg *= 2;
+    return kg;
+}
+
+bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_blocks,
+               ScreenPlan* plan) {
     if (n_cands < 1 || n_acc < 0 || n_acc > n_cands || !is_float_dtype(dtype)) return false;
     ScreenPlan P{};
     P.dtype = dtype;
@@ -159,37 +194,59 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, ScreenPlan* pl
     P.numel = numel;
     const uint64_t vec = 16 / elem_size(dtype);
     P.n_vec = numel / vec;
-    // Candidates per group: all of them when few, else 8.  Chosen from
-    // n_cands so that the workspace sized for n_cands always suffices.
-    int kg = 1;
-    while (kg < n_cands && kg < 8) kg *= 2;
-    P.kg = kg;
-    const int groups_max = (n_cands + kg - 1) / kg;
-    P.n_groups = n_acc > 0 ? (n_acc + kg - 1) / kg : 0;
-    // Work-groups per candidate group: about 2048 in total, a multiple of 8
-    // (XCDs), no more than there are 256-vector stripes, and enough that one
-    // work-group sees fewer than 2^31 elements (32-bit partial counts).
-    const uint64_t target_total = 2048;
-    uint64_t C = (target_total + groups_max - 1) / groups_max;
-    const uint64_t stripes = (P.n_vec + 255) / 256;
-    if (C > stripes) C = stripes;
-    const uint64_t min_c = numel / (1ull << 31) + 1;
+    // Candidates per group: all of them when few, else 8 (chosen from n_cands
+    // so that the workspace sized for n_cands always suffices).
+    P.kg = plan_group_size(n_cands);
+    const int groups_max = (n_cands + P.kg - 1) / P.kg;
+    P.n_groups = n_acc > 0 ? (n_acc + P.kg - 1) / P.kg : 0;
+    // Work-groups per candidate group (a multiple of 8, the XCD count):
+    //  - at least enough that one work-group sees fewer than 2^31 elements
+    //    (32-bit partial counts), at most one per 4 chunks of 512 elements;
+    //  - for the launch: one round of the work-groups that are resident on the
+    //    device at once (occupancy of the chosen kernel x CUs), spread over
+    //    the candidate groups -- the grid is persistent, each wave strides
+    //    over the chunks -- unless a tuning override sets the total;
+    //  - the workspace is laid out for the bound C_ws, independent of the
+    //    device, and the launch never exceeds it.
+    const uint64_t n_chunks = numel / 512;
+    const uint64_t c_work = align_up((n_chunks + 3) / 4, 8);
+    const uint64_t min_c = align_up(numel / (1ull << 31) + 1, 8);
+    uint64_t c_ws = align_up((4096 + groups_max - 1) / groups_max, 8);
+    if (c_ws > c_work) c_ws = c_work;
+    if (c_ws < min_c) c_ws = min_c;
+    if (c_ws < 8) c_ws = 8;
+    if (c_ws > (1u << 20)) return false;
+    int kg_cap = 8, blocks_total = 0;
+    tuning_override(&kg_cap, &blocks_total);
+    if (blocks_total <= 0) blocks_total = resident_blocks > 0 ? resident_blocks : 2048;
+    const int groups = P.n_groups > 0 ? P.n_groups : 1;
+    uint64_t C = align_up(((uint64_t)blocks_total + groups - 1) / groups, 8);
+    if (C > c_ws) C = c_ws;
     if (C < min_c) C = min_c;
-    C = align_up(C < 8 ? 8 : C, 8);
-    if (C > (1u << 20)) return false;
+    if (C < 8) C = 8;
     P.blocks_per_group = (int)C;
-    // Workspace layout, sized for the group count of n_cands.
+    const uint64_t Cw = c_ws;  // layout stride bound
+    // Workspace layout, sized for the group count of n_cands.  The tickets
+    // come first: the launch-table upload zeroes them on every call.
+    P.n_super = (int)((C + 15) / 16);
+    const int super_ws = (int)((Cw + 15) / 16);
     size_t off = 0;
-    P.off_tickets = off;
-    off = align_up(off + (size_t)groups_max * 4, 256);
+    P.off_tickets2 = off;
+    off += (size_t)groups_max * 4;
+    P.off_tickets1 = off;
+    off = align_up(off + (size_t)groups_max * super_ws * 4, 256);
     P.off_table = off;
-    off = align_up(off + (size_t)n_cands * sizeof(CandEntry), 256);
+    off = align_up(off + (size_t)(n_cands + P.kg) * sizeof(CandEntry), 256);
     P.off_part_u32 = off;
-    off = align_up(off + (size_t)PF_COUNT * n_cands * C * 4, 256);
+    off = align_up(off + (size_t)PF_COUNT * n_cands * Cw * 4, 256);
     P.off_part_ssd = off;
-    off = align_up(off + (size_t)n_cands * C * 8, 256);
+    off = align_up(off + (size_t)n_cands * Cw * 8, 256);
     P.off_part_ssr = off;
-    off = align_up(off + (size_t)groups_max * C * 8, 256);
+    off = align_up(off + (size_t)groups_max * Cw * 8, 256);
+    P.off_part2 = off;
+    off = align_up(off + (size_t)n_cands * super_ws * sizeof(Part2), 256);
+    P.off_part2_ssr = off;
+    off = align_up(off + (size_t)groups_max * super_ws * 8, 256);
     P.total = off;
     *plan = P;
     return true;
@@ -220,7 +277,7 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands, i
 
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype) {
     ScreenPlan P;
-    if (!make_plan(n_cands, n_cands, numel, dtype, &P)) return 0;
+    if (!make_plan(n_cands, n_cands, numel, dtype, 0, &P)) return 0;
     return P.total;
 }
 
@@ -229,7 +286,7 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out) {
     if (out == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_screen_launch: out is NULL");
     if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "dtype %d not screenable", dtype);
     ScreenPlan P;
-    if (!make_plan(n_cands, n_cands, numel, dtype, &P))
+    if (!make_plan(n_cands, n_cands, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands)), &P))
         return fail(KB_ERR_INVALID_ARG, "no launch plan for n_cands=%d numel=%llu", n_cands,
                     (unsigned long long)numel);
     out->group_size = P.kg;
@@ -261,7 +318,7 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
 
     ScreenPlan P;
-    if (!make_plan(n_cands, n_acc, numel, dtype, &P))
+    if (!make_plan(n_cands, n_acc, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands)), &P))
         return fail(KB_ERR_INVALID_ARG, "kb_screen: no launch plan (numel=%llu)",
                     (unsigned long long)numel);
     if (workspace == nullptr || workspace_bytes < P.total)
@@ -273,27 +330,37 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
         if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
             return fail(KB_ERR_ALIGNMENT, "kb_screen: candidate %d data not 16-byte aligned", k);
 
-    // Launch table: tickets (zeroed) then accepted candidates, then rejected.
-    const size_t upload = P.off_table + (size_t)n_cands * sizeof(CandEntry);
-    rc = staging().upload(
-        upload,
-        [&](void* host) {
-            std::memset(host, 0, P.off_table);
-            CandEntry* tab = (CandEntry*)((char*)host + P.off_table);
-            int w = 0;
-            for (int k = 0; k < n_cands; ++k)
-                if (status[k] == KB_STATUS_OK) tab[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
-            for (int k = 0; k < n_cands; ++k)
-                if (status[k] != KB_STATUS_OK) tab[w++] = CandEntry{nullptr, k, status[k]};
-        },
-        workspace, stream);
-    if (rc != KB_OK) return rc;
-
+    // Launch table: accepted candidates in call order padded to whole groups
+    // (padding points at the reference and writes no record), then rejected
+    // ones.  Up to kInlineCands entries travel in the kernel arguments; a
+    // larger table is uploaded to the workspace through the pinned staging
+    // ring.
+    const int n_groups = P.n_groups;
+    const int rej_start = n_groups * P.kg;
+    const int n_table = rej_start + (n_cands - n_acc);
+    const bool table_inline = n_table <= kInlineCands;
+    InlineTable tab;
+    auto fill = [&](CandEntry* t) {
+        int w = 0;
+        for (int k = 0; k < n_cands; ++k)
+            if (status[k] == KB_STATUS_OK) t[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
+        while (w < rej_start) t[w++] = CandEntry{ref->data, -1, KB_STATUS_OK};
+        for (int k = 0; k < n_cands; ++k)
+            if (status[k] != KB_STATUS_OK) t[w++] = CandEntry{nullptr, k, status[k]};
+    };
     char* ws = (char*)workspace;
     const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
+    if (table_inline) {
+        fill(tab.e);
+    } else {
+        rc = staging().upload(
+            (size_t)n_table * sizeof(CandEntry), [&](void* host) { fill((CandEntry*)host); },
+            ws + P.off_table, stream);
+        if (rc != KB_OK) return rc;
+    }
     hipError_t e;
     if (n_acc == 0 || numel == 0) {
-        e = launch_records_only(d_table, n_cands, numel, d_stats, stream);
+        e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, stream);
         if (e != hipSuccess) return fail_hip(e, "kb_screen: records launch");
         return KB_OK;
     }
@@ -307,15 +374,55 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     p.flags = flags;
     p.n_acc = n_acc;
     p.n_cands = n_cands;
+    p.n_table = n_table;
+    p.rej_start = rej_start;
+    p.table_inline = table_inline ? 1 : 0;
     p.n_groups = P.n_groups;
     p.blocks_per_group = P.blocks_per_group;
-    p.tickets = (uint32_t*)(ws + P.off_tickets);
+    p.n_super = P.n_super;
+    p.tickets1 = (uint32_t*)(ws + P.off_tickets1);
+    p.tickets2 = (uint32_t*)(ws + P.off_tickets2);
     p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
     p.part_ssd = (double*)(ws + P.off_part_ssd);
     p.part_ssr = (double*)(ws + P.off_part_ssr);
+    p.part2 = (Part2*)(ws + P.off_part2);
+    p.part2_ssr = (double*)(ws + P.off_part2_ssr);
     p.stats = d_stats;
-    e = launch_screen(P, p, stream);
+    e = launch_screen(P, p, tab, stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen: kernel launch");
+    return KB_OK;
+}
+
+int kb_screen_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    if (workspace == nullptr || workspace_bytes == 0)
+        return fail(KB_ERR_WORKSPACE, "kb_screen_workspace_init: no workspace");
+    if (!aligned16(workspace) || (workspace_bytes & 15u))
+        return fail(KB_ERR_ALIGNMENT, "kb_screen_workspace_init: workspace not 16-byte aligned/sized");
+    hipError_t e = launch_zero_fill(workspace, workspace_bytes, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen_workspace_init: fill launch");
+    return KB_OK;
+}
+
+int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary) {
+    clear_error();
+    if (h_stats == nullptr || summary == nullptr || n_cands < 0)
+        return fail(KB_ERR_INVALID_ARG, "kb_summarize: null argument or negative count");
+    kb_summary s{n_cands, 0, 0, 0, -1, -1};
+    for (int k = 0; k < n_cands; ++k) {
+        const kb_stats& st = h_stats[k];
+        if (st.status != KB_STATUS_OK) {
+            s.n_rejected++;
+        } else if (st.mismatches == 0) {
+            s.n_passed++;
+            if (s.first_passed < 0) s.first_passed = k;
+            continue;
+        } else {
+            s.n_failed++;
+        }
+        if (s.first_failed < 0) s.first_failed = k;
+    }
+    *summary = s;
     return KB_OK;
 }
 
@@ -337,23 +444,7 @@ int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats, kb_
     }
     hipError_t e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen_stats: hipStreamSynchronize");
-    if (summary) {
-        kb_summary s{n_cands, 0, 0, 0, -1, -1};
-        for (int k = 0; k < n_cands; ++k) {
-            const kb_stats& st = dst[k];
-            if (st.status != KB_STATUS_OK) {
-                s.n_rejected++;
-            } else if (st.mismatches == 0) {
-                s.n_passed++;
-                if (s.first_passed < 0) s.first_passed = k;
-                continue;
-            } else {
-                s.n_failed++;
-            }
-            if (s.first_failed < 0) s.first_failed = k;
-        }
-        *summary = s;
-    }
+    if (summary) return kb_summarize(dst, n_cands, summary);
     return KB_OK;
 }
 

@@ -162,4 +162,35 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
     return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
+// Reductions within one 16-lane DPP row: the four steps above leave every
+// lane of a row holding the row's result (no cross-row reads), so a
+// work-group can reduce up to 16 independent values, one per row.
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
+    v = max(v, dpp_u32<DPP_QUAD_XOR1>(v));
+    v = max(v, dpp_u32<DPP_QUAD_XOR2>(v));
+    v = max(v, dpp_u32<DPP_ROW_HALF_MIRROR>(v));
+    return max(v, dpp_u32<DPP_ROW_MIRROR>(v));
+}
+
+__device__ __forceinline__ uint32_t row_or_u32(uint32_t v) {
+    v |= dpp_u32<DPP_QUAD_XOR1>(v);
+    v |= dpp_u32<DPP_QUAD_XOR2>(v);
+    v |= dpp_u32<DPP_ROW_HALF_MIRROR>(v);
+    return v | dpp_u32<DPP_ROW_MIRROR>(v);
+}
+
+__device__ __forceinline__ uint64_t row_sum_u64(uint64_t v) {
+    v += dpp_u64<DPP_QUAD_XOR1>(v);
+    v += dpp_u64<DPP_QUAD_XOR2>(v);
+    v += dpp_u64<DPP_ROW_HALF_MIRROR>(v);
+    return v + dpp_u64<DPP_ROW_MIRROR>(v);
+}
+
+__device__ __forceinline__ double row_sum_f64(double v) {
+    v = v + dpp_f64<DPP_QUAD_XOR1>(v);
+    v = v + dpp_f64<DPP_QUAD_XOR2>(v);
+    v = v + dpp_f64<DPP_ROW_HALF_MIRROR>(v);
+    return v + dpp_f64<DPP_ROW_MIRROR>(v);
+}
+
 }  // namespace kb

@@ -10,11 +10,13 @@
 
 namespace kb {
 
-// One entry of the candidate table uploaded to the workspace: accepted
-// candidates first (in call order), then rejected ones.
+// One entry of the launch table.  The table holds the accepted candidates
+// in call order, padded to whole candidate groups with entries that point
+// at the reference (index -1; the kernel compares them but writes no
+// record), then the rejected candidates.
 struct CandEntry {
     const void* data;  // device pointer (NULL for rejected entries)
-    int32_t index;     // position in the caller's candidate array
+    int32_t index;     // position in the caller's candidate array, -1 for padding
     int32_t status;    // KB_STATUS_OK or KB_REJECT_*
 };
 
@@ -42,12 +44,39 @@ struct ScreenPlan {
     int threads;
     uint64_t numel;
     uint64_t n_vec;       // full 16-byte vectors per tensor
+    int n_super;          // ceil(blocks_per_group / 16): first-level combine groups
     // workspace byte offsets
-    size_t off_tickets, off_table, off_part_u32, off_part_ssd, off_part_ssr, total;
+    size_t off_tickets1, off_tickets2, off_table, off_part_u32, off_part_ssd, off_part_ssr,
+        off_part2, off_part2_ssr, total;
 };
 
-// Launch geometry and workspace layout for (n_cands candidates, all accepted).
-bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, ScreenPlan* plan);
+// Second-level partial of one candidate: the combine of up to 16 work-groups.
+struct Part2 {
+    uint64_t mism, nan, pinf, ninf;
+    uint32_t maxabs, maxrel, bitdiff, pad;
+    double ssd;
+};
+
+// Launch geometry and workspace layout.  The layout depends only on
+// (n_cands, numel, dtype); resident_blocks (work-groups of the chosen kernel
+// that fit on the device at once, 0 if unknown) sizes the launch.
+bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_blocks,
+               ScreenPlan* plan);
+
+// Candidates per group the plan picks for n_cands candidates.
+int plan_group_size(int n_cands);
+
+// Work-groups of screen_kernel<dtype, kg> resident per CU (occupancy query,
+// cached), or 0 on failure.
+int screen_blocks_per_cu(int dtype, int kg);
+
+// Launch tables of up to this many candidates travel in the kernel
+// arguments (no upload); larger ones are uploaded to the workspace.
+constexpr int kInlineCands = 128;
+
+struct InlineTable {
+    CandEntry e[kInlineCands];
+};
 
 // Device-side parameters of the screening kernel.
 struct ScreenParams {
@@ -60,20 +89,32 @@ struct ScreenParams {
     uint32_t flags;
     int n_acc;
     int n_cands;
+    int n_table;         // table entries: n_groups * KG padded accepted + rejected
+    int rej_start;       // first rejected entry (n_groups * KG)
+    int table_inline;    // 1: the table is the kernel argument, 0: p.table
     int n_groups;
     int blocks_per_group;
-    uint32_t* tickets;
+    int n_super;
+    uint32_t* tickets1;  // [n_groups][n_super]
+    uint32_t* tickets2;  // [n_groups]
     uint32_t* part_u32;  // [PF_COUNT][n_acc][blocks_per_group]
     double* part_ssd;    // [n_acc][blocks_per_group]
     double* part_ssr;    // [n_groups][blocks_per_group]
+    Part2* part2;        // [n_acc][n_super]
+    double* part2_ssr;   // [n_groups][n_super]
     kb_stats* stats;     // caller's records, indexed by CandEntry::index
 };
 
-hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, hipStream_t stream);
+// tab: the launch table when it is inline (n_cands <= kInlineCands), else
+// ignored (p.table points at the uploaded copy).
+hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                         hipStream_t stream);
+// Zero-fill n bytes of device memory (workspace initialisation).
+hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream);
 // Records for calls with no element to read (numel == 0 or no accepted
 // candidate): every record written from the table alone.
-hipError_t launch_records_only(const CandEntry* table, int n_cands, uint64_t numel,
-                               kb_stats* stats, hipStream_t stream);
+hipError_t launch_records_only(const CandEntry* table, const InlineTable& tab, int table_inline,
+                               int n_table, uint64_t numel, kb_stats* stats, hipStream_t stream);
 
 hipError_t launch_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
                       uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,

@@ -5,25 +5,47 @@
 // indicator K(p), Sections 3.1 and 3.4): mismatches under
 // |c - r| <= atol + rtol*|r|, NaN/+Inf/-Inf counts, bitwise identity, max
 // abs error, max rel error and the two squared-error sums of the relative L2
-// error.  The work is a streaming reduction bound by HBM bandwidth: no
-// contraction, so no MFMA.
+// error.  The work is a streaming reduction bound by HBM bandwidth (no
+// contraction, so no MFMA); the design goal is to spend fewer VALU
+// instructions per (element, candidate) than HBM delivers elements.
 //
 // Work split.  Candidates that passed the policy gate are cut into groups of
-// KG; a work-group owns one candidate group and one stripe of the element
-// range, walks its stripe in 16-byte vectors (grid-stride over the group's
-// work-groups, so that consecutive work-groups read consecutive memory), loads
-// each reference vector once and compares it with the KG candidates' vectors
-// while it is in registers.  Work-group ids are mapped so that all candidate
-// groups of one stripe run on the same XCD (ids are dealt to the 8 XCDs round
-// robin), and a reference stripe fetched for one group is then found in that
-// XCD's L2 by the others.
+// KG.  A work-group (4 waves) owns one candidate group and one stripe of the
+// element range.  A wave handles 512-element chunks (8 elements per lane:
+// one 16-byte load per tensor for 16-bit types, two for fp32), grid-striding
+// over the group's waves so that consecutive waves read consecutive memory.
+// Each reference chunk is loaded once and compared with the KG candidate
+// chunks while it sits in registers.  Work-group ids are mapped so that the
+// candidate groups of one stripe run on the same XCD (ids are dealt to the 8
+// XCDs round robin), so a reference stripe fetched for one group is found in
+// that XCD's L2 by the others.
 //
-// Reduction.  Per lane accumulators -> 64-lane DPP reductions -> LDS combine
-// of the work-group's waves in wave order -> per-(work-group, candidate)
-// partials in the workspace.  The last work-group of a candidate group to
-// finish (an atomic ticket after a release fence) combines the partials of
-// its group in a fixed order and writes the kb_stats records; the binary64
-// sums are therefore the same bits on every call.
+// Two paths per (chunk, candidate), chosen per wave:
+//   fast  -- all values finite and no extreme squared difference: per
+//            element one subtract, one compare (match counts are popcounts of
+//            wave ballots, kept in scalar registers), a max tree for the max
+//            abs error, one multiply by a per-reference reciprocal for the
+//            max-rel filter, and one fused multiply-add for the squared
+//            difference (8 binary32 terms per lane, then one binary64 add);
+//   exact -- the definition applied element by element (IEEE division,
+//            binary64 squares, NaN/Inf classification), taken by a wave when
+//            any lane sees a NaN, an infinity or a binary32 overflow of
+//            (c - r)^2.
+// Two narrower exact fix-ups run inside the fast path: binary64 squares for
+// lanes whose differences are all below 2^-60 (where binary32 squares would
+// underflow), and IEEE division for lanes whose filtered relative error may
+// exceed the wave's exact running maximum.  Every count, flag and maximum is
+// therefore exact; the sum of squares has relative error at most about
+// 8 * 2^-24 (eight binary32 roundings per lane and chunk) before the binary64
+// accumulation.
+//
+// Reduction.  Lane values -> 64-lane DPP reductions (wave-level counts are
+// already scalar) -> LDS combine of the work-group's waves in wave order ->
+// per-(work-group, candidate) partials in the workspace.  The last
+// work-group of a candidate group to finish (atomic ticket after a release
+// fence) combines its group's partials in a fixed order with 16 lanes per
+// candidate and writes the kb_stats records, so the binary64 sums are the
+// same bits on every call.
 #include "kb_device.hpp"
 #include "kb_internal.hpp"
 
@@ -32,95 +54,238 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kE = 8;                 // elements per lane per chunk
+constexpr int kChunk = 64 * kE;       // elements per wave per chunk
+constexpr float kTiny = 0x1p-60f;     // below this binary32 squares may underflow
+constexpr float kRelMargin = 0x1.ffffep-1f;  // 1 - 2^-20: max-rel filter slack
 
+// Raw storage of one lane's 8 elements of a chunk.
 template <int DT>
-struct Elem {
-    static constexpr int kVec = DT == DT_F32 ? 4 : 8;  // elements per 16-byte vector
+struct Raw {
+    static constexpr int kWords = DT == DT_F32 ? 8 : 4;
+    uint32_t w[kWords];
 };
 
-// Per-lane running statistics of one candidate.
-struct LaneAcc {
-    uint32_t mism, nan, pinf, ninf, bitdiff;
-    float max_abs, max_rel;
-    double ssd;
-};
+// 16-byte vector loaded through a global (address space 1) pointer, so
+// that candidate pointers read from the launch table produce global_load
+// rather than flat_load instructions.
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) v4u32* gvec;
 
-__device__ __forceinline__ void acc_init(LaneAcc& a) {
-    a.mism = a.nan = a.pinf = a.ninf = a.bitdiff = 0u;
-    a.max_abs = a.max_rel = 0.f;
-    a.ssd = 0.0;
+template <bool NT>
+__device__ __forceinline__ v4u32 ld16(gvec p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
 }
 
-// Reference-side values of one element, computed once and used for all KG
-// candidates: r, |r|, the tolerance atol + rtol*|r| (two binary32 roundings;
-// -1 for a non-finite r, which only c == r can match) and finiteness.
-struct RefElem {
-    float r, a, tol;
-    bool fin;
-};
-
-__device__ __forceinline__ RefElem ref_elem(float r, float atol, float rtol) {
-    RefElem e;
-    e.r = r;
-    e.a = fabsf(r);
-    e.fin = __builtin_isfinite(r);
-    e.tol = e.fin ? __fadd_rn(atol, __fmul_rn(rtol, e.a)) : -1.0f;
-    return e;
-}
-
-// One (element, candidate) pair, by definition.
-__device__ __forceinline__ void acc_elem(LaneAcc& A, float c, const RefElem& R, bool equal_nan) {
-    const bool cnan = __builtin_isnan(c);
-    A.nan += cnan ? 1u : 0u;
-    A.pinf += (c == __builtin_inff()) ? 1u : 0u;
-    A.ninf += (c == -__builtin_inff()) ? 1u : 0u;
-    const float d = fabsf(__fsub_rn(c, R.r));
-    const bool match = (c == R.r) || (d <= R.tol) || (equal_nan && cnan && __builtin_isnan(R.r));
-    A.mism += match ? 0u : 1u;
-    if (d > A.max_abs) A.max_abs = d;
-    const float q = d / R.a;  // IEEE binary32 division (x/0 = inf, 0/0 = NaN)
-    if (q > A.max_rel) A.max_rel = q;
-    if (R.fin && __builtin_isfinite(c)) A.ssd = __builtin_fma((double)d, (double)d, A.ssd);
+// fp32: lane l holds elements 4l..4l+3 and 256+4l..256+4l+3 of the chunk
+// (two fully coalesced 1 KB wave loads); 16-bit: elements 8l..8l+7.  NT
+// marks the loads nontemporal: every candidate byte is used once, and
+// streaming it past the caches leaves them to the reference, which the
+// other candidate groups of the stripe re-read.
+template <int DT, bool NT>
+__device__ __forceinline__ Raw<DT> load_chunk(const void* base, uint64_t chunk, int lane) {
+    Raw<DT> x;
+    if constexpr (DT == DT_F32) {
+        const gvec p = (gvec)base + chunk * 128;
+        const v4u32 a = ld16<NT>(p + lane);
+        const v4u32 b = ld16<NT>(p + 64 + lane);
+        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+        x.w[4] = b.x; x.w[5] = b.y; x.w[6] = b.z; x.w[7] = b.w;
+    } else {
+        const gvec p = (gvec)base + chunk * 64;
+        const v4u32 a = ld16<NT>(p + lane);
+        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+    }
+    return x;
 }
 
 template <int DT>
-__device__ __forceinline__ float widen(uint32_t bits) {
+__device__ __forceinline__ float widen_bits(uint32_t bits) {
     if constexpr (DT == DT_F32) return __uint_as_float(bits);
     else if constexpr (DT == DT_F16) return f16_bits_to_f32(bits);
     else return bf16_bits_to_f32(bits);
 }
 
-// Element i of a 16-byte vector (little-endian halves for 16-bit types).
+// Element i (0..7) of a lane's chunk, widened exactly to binary32.
 template <int DT>
-__device__ __forceinline__ uint32_t vec_elem_bits(const uint4& v, int i) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    if constexpr (DT == DT_F32) return w[i];
-    else return (w[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+__device__ __forceinline__ float elem(const Raw<DT>& x, int i) {
+    if constexpr (DT == DT_F32) return __uint_as_float(x.w[i]);
+    else if constexpr (DT == DT_F16) return f16_bits_to_f32((x.w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+    else return bf16_bits_to_f32(i & 1 ? (x.w[i >> 1] >> 16) : (x.w[i >> 1] & 0xFFFFu));
 }
 
-template <int DT>
-__device__ __forceinline__ uint32_t scalar_bits(const void* base, uint64_t i) {
-    if constexpr (DT == DT_F32) return ((const uint32_t*)base)[i];
-    else return ((const uint16_t*)base)[i];
+__device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__builtin_popcountll(m); }
+
+// Cross-work-group hand-off without L2 maintenance.  Partials are written
+// with agent-scope atomic stores (made coherent across XCDs by the store
+// itself), the work-group waits for their completion, and only then takes a
+// ticket with a relaxed agent-scope atomic.  The work-group that draws the
+// last ticket reads the partials with agent-scope atomic loads, which return
+// the coherent copy.  So no work-group writes back or invalidates its XCD's
+// L2, which is what a device-scope fence costs here and which would also
+// evict the lines other work-groups on the XCD are streaming.
+__device__ __forceinline__ void complete_stores() { __builtin_amdgcn_s_waitcnt(0); }
+__device__ __forceinline__ uint32_t ticket(uint32_t* t) {
+    return __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <class T>
+__device__ __forceinline__ T ld_coherent(const T* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_coherent(const double* p) {
+    return __builtin_bit_cast(double, ld_coherent((const uint64_t*)p));
+}
+template <class T>
+__device__ __forceinline__ void st_coherent(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coherent(double* p, double v) {
+    st_coherent((uint64_t*)p, __builtin_bit_cast(uint64_t, v));
+}
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+__device__ __forceinline__ float wave_max_f(float v) {
+    return __uint_as_float(wave_max_u32(__float_as_uint(v)));
 }
 
-// Block-wide fixed-order combine helpers (LDS scratch provided by caller).
-struct Lds {
-    uint32_t u[kWaves][PF_COUNT];
-    double ssd[kWaves];
-    double ssr[kWaves];
+// Hides a value from the optimizer, so that work on it inside a rare branch
+// is not hoisted into the common path (it would run for every chunk and
+// keep registers live across the loop).
+__device__ __forceinline__ void opaque(float& x) { asm volatile("" : "+v"(x)); }
+
+// Wave-uniform accumulators of the work-group's candidates; the per-lane
+// sums of squares live in LDS.
+//
+// The max relative error is kept as the exact ratio relD / relA of the best
+// element seen (|c - r| and |r| as binary32; relA = 0 encodes +inf), and
+// relT = fl(fl(relD / relA) (1 - 2^-20)) is the threshold of the cheap filter.
+// Candidates that pass the filter are compared exactly (binary64 products
+// of binary32 values are exact), so elements that only tie the maximum cost
+// one comparison.  Rounding is monotone, so fl(max ratio) = max fl(ratio):
+// the record's max_rel_err is fl(relD / relA) of the final state.
+//
+// The counts stay in scalar registers; the maxima, written rarely, live in
+// LDS (one slot per wave and candidate, read back as a broadcast) so that
+// they take no registers across the loop.
+template <int KG>
+struct WaveAcc {
+    uint32_t mism[KG];  // mismatches seen by this wave
+    uint32_t bitdiff;   // bit j: candidate j differs somewhere in this wave's range
 };
 
+struct WaveMax {
+    float abs;   // exact max abs error seen by this wave
+    float relT;  // max-rel filter threshold
+    float relD;  // max-rel state: ratio relD / relA
+    float relA;
+};
+typedef volatile WaveMax* WaveMaxPtr;
+
+// d / a > bd / ba, exactly (finite non-negative binary32 inputs, a or ba may
+// be zero for an infinite ratio).
+__device__ __forceinline__ bool ratio_gt(float d, float a, float bd, float ba) {
+    return (double)d * (double)ba > (double)bd * (double)a;
+}
+
+// Wave step of the max-rel state: lanes with has = true propose the ratio
+// bd / ba (each greater than the current state); the state moves to the
+// proposal with the largest rounded quotient (lowest lane on ties).
+__device__ __forceinline__ void rel_propose(WaveMaxPtr M, bool has, float bd, float ba) {
+    const float key = has ? (ba > 0.f ? bd / ba : __builtin_inff()) : 0.f;
+    const uint32_t kmax = wave_max_u32(__float_as_uint(key));
+    const uint64_t win = ballot(has && __float_as_uint(key) == kmax);
+    if (win) {
+        const int lane = __builtin_ctzll(win);
+        M->relD = __uint_as_float(readlane_u32(__float_as_uint(bd), lane));
+        M->relA = __uint_as_float(readlane_u32(__float_as_uint(ba), lane));
+        M->relT = __uint_as_float(kmax) * kRelMargin;
+    }
+}
+
+// Non-finite counts (rare): per wave, per candidate, in LDS.
+struct NonFinite {
+    uint32_t nan, pinf, ninf;
+};
+
+// The definition, element by element, for a whole lane chunk of one
+// candidate (every lane active).  Also the path for the ragged tail.
 template <int DT, int KG>
-__global__ __launch_bounds__(kThreads) void screen_kernel(ScreenParams p) {
-    constexpr int V = Elem<DT>::kVec;
-    __shared__ Lds lds[KG];
+__device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_in[kE], float atol,
+                                            float rtol, bool equal_nan, double* ssd_slot,
+                                            WaveAcc<KG>& W, int j, WaveMaxPtr M, NonFinite& nf) {
+    float r[kE];
+#pragma unroll
+    for (int i = 0; i < kE; ++i) {
+        r[i] = r_in[i];
+        opaque(r[i]);
+    }
+    uint32_t nm = 0, nnan = 0, npinf = 0, nninf = 0;
+    float ma = 0.f;
+    float bd = M->relD, ba = M->relA;
+    bool has = false;
+    double sd = 0.0;
+#pragma unroll
+    for (int i = 0; i < kE; ++i) {
+        const float c = elem<DT>(cand, i);
+        const float ri = r[i];
+        const bool cnan = __builtin_isnan(c);
+        nnan += popc(ballot(cnan));
+        npinf += popc(ballot(c == __builtin_inff()));
+        nninf += popc(ballot(c == -__builtin_inff()));
+        const float d = fabsf(c - ri);
+        const float a = fabsf(ri);
+        const bool rfin = __builtin_isfinite(ri);
+        const float tol = rfin ? __fadd_rn(atol, __fmul_rn(rtol, a)) : -1.0f;
+        const bool match = (c == ri) || (d <= tol) || (equal_nan && cnan && __builtin_isnan(ri));
+        nm += popc(ballot(!match));
+        if (d > ma) ma = d;
+        // the quotient d / a is a NaN for 0/0 and inf/inf and 0 for x/inf:
+        // none of these can raise the maximum
+        if (d > 0.f && a < __builtin_inff()) {
+            const float dd = d < __builtin_inff() ? d : 1.f;  // d = inf: ratio inf = 1/0
+            const float aa = d < __builtin_inff() ? a : 0.f;
+            if (ratio_gt(dd, aa, bd, ba)) {
+                bd = dd;
+                ba = aa;
+                has = true;
+            }
+        }
+        if (rfin && __builtin_isfinite(c)) sd = __builtin_fma((double)d, (double)d, sd);
+    }
+    atomicAdd(ssd_slot, sd);
+    W.mism[j] += nm;
+    M->abs = fmaxf(M->abs, wave_max_f(ma));
+    if (ballot(has)) rel_propose(M, has, bd, ba);
+    nf.nan += nnan;
+    nf.pinf += npinf;
+    nf.ninf += nninf;
+}
+
+// Per-wave results, combined across the work-group's waves in LDS.
+struct WaveOut {
+    uint32_t u[PF_COUNT];
+    double ssd;
+};
+
+// Minimum waves per SIMD the register allocator must allow: 3 keeps the
+// 16-bit kernels (which need more waves to cover the load latency of their
+// shorter per-candidate work) at 12 waves per CU; the fp32 kernels hold
+// twice the data per lane and are left to the allocator.
+constexpr int min_waves(int dt, int kg) { return (dt != DT_F32 && kg <= 8) ? 3 : 1; }
+
+template <int DT, int KG>
+__global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
+                                                                            InlineTable tab) {
+    const CandEntry* table = p.table_inline ? tab.e : p.table;
+    __shared__ double s_ssd[KG][kThreads];  // lane sums of squared differences
+    __shared__ WaveOut s_out[kWaves][KG];
+    __shared__ double s_ssr[kWaves];
+    __shared__ NonFinite s_nf[kWaves][KG];
+    __shared__ WaveMax s_max[kWaves][KG];
     __shared__ uint32_t s_is_last;
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // XCD-aware ids: block ids are dealt to the 8 XCDs round robin; keep one
-    // stripe's candidate groups on one XCD.
     const int xcd = blockIdx.x & 7;
     const int slot = blockIdx.x >> 3;
     const int g = slot % p.n_groups;
@@ -128,56 +293,160 @@ __global__ __launch_bounds__(kThreads) void screen_kernel(ScreenParams p) {
     const int j0 = g * KG;
     const int kg = min(KG, p.n_acc - j0);
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
+    const float atol = p.atol, rtol = p.rtol;
 
-    const uint4* cand[KG];
+    const void* cand[KG];
 #pragma unroll
-    for (int j = 0; j < KG; ++j) cand[j] = (const uint4*)(j < kg ? p.table[j0 + j].data : p.ref);
-    const uint4* ref = (const uint4*)p.ref;
+    for (int j = 0; j < KG; ++j) cand[j] = table[j0 + j].data;  // padded: always valid
 
-    LaneAcc acc[KG];
+    WaveAcc<KG> W;
+    W.bitdiff = 0u;
 #pragma unroll
-    for (int j = 0; j < KG; ++j) acc_init(acc[j]);
+    for (int j = 0; j < KG; ++j) {
+        W.mism[j] = 0u;
+        s_ssd[j][threadIdx.x] = 0.0;
+    }
+    if (lane < KG) s_max[wave][lane] = WaveMax{0.f, 0.f, 0.f, 1.f};  // ratio 0 / 1
+    if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
     double ssr = 0.0;
 
-    const uint64_t stride = (uint64_t)p.blocks_per_group * kThreads;
-    for (uint64_t v = (uint64_t)stripe * kThreads + threadIdx.x; v < p.n_vec; v += stride) {
-        const uint4 rv = ref[v];
-        RefElem R[V];
+    const uint64_t n_chunks = p.numel / kChunk;
+    const uint64_t wstride = (uint64_t)p.blocks_per_group * kWaves;
+    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave; chunk < n_chunks; chunk += wstride) {
+        const Raw<DT> rraw = load_chunk<DT, false>(p.ref, chunk, lane);
+        Raw<DT> craw[KG];
 #pragma unroll
-        for (int i = 0; i < V; ++i) {
-            R[i] = ref_elem(widen<DT>(vec_elem_bits<DT>(rv, i)), p.atol, p.rtol);
-            if (R[i].fin) ssr = __builtin_fma((double)R[i].r, (double)R[i].r, ssr);
+        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(cand[j], chunk, lane);
+        // Reference side, once per element for all KG candidates.
+        float r[kE], tol[kE], inv[kE];
+        double rr = 0.0;
+#pragma unroll
+        for (int i = 0; i < kE; ++i) {
+            r[i] = elem<DT>(rraw, i);
+            const uint32_t abits = __float_as_uint(r[i]) & 0x7FFFFFFFu;
+            tol[i] = __fadd_rn(atol, __fmul_rn(rtol, __uint_as_float(abits)));
+            // rcp of min(|r|, 2^100) (NaN clamps to 2^100; such lanes take the
+            // exact path): at least 1/|r| (1 - 2^-22) for normal |r|, an
+            // over-estimate for larger |r|, and very large or +inf for zero
+            // or subnormal |r| -- a conservative max-rel filter everywhere.
+            inv[i] = __builtin_amdgcn_rcpf(__uint_as_float(min(abits, 0x71800000u)));
+            rr = __builtin_fma((double)r[i], (double)r[i], rr);
         }
-        uint4 cv[KG];
+        if (!(rr < __builtin_inf())) {  // a non-finite reference value in this lane
+            rr = 0.0;
 #pragma unroll
-        for (int j = 0; j < KG; ++j)
-            if (j < kg) cv[j] = cand[j][v];
+            for (int i = 0; i < kE; ++i)
+                if (__builtin_isfinite(r[i])) rr = __builtin_fma((double)r[i], (double)r[i], rr);
+        }
+        ssr += rr;
+
 #pragma unroll
         for (int j = 0; j < KG; ++j) {
-            if (j < kg) {
-                acc[j].bitdiff |= (cv[j].x ^ rv.x) | (cv[j].y ^ rv.y) | (cv[j].z ^ rv.z) |
-                                  (cv[j].w ^ rv.w);
+            // Keep the scheduler from interleaving candidates: each holds a
+            // set of per-element ballot masks in scalar registers until they
+            // are counted, and interleaving multiplies the live set.  All the
+            // chunk's loads were issued above, so latency hiding is
+            // unaffected.
+            __builtin_amdgcn_sched_barrier(0);
+            const Raw<DT>& cr = craw[j];
+            // bitwise identity on raw storage, until a difference is known
+            if (!((W.bitdiff >> j) & 1u)) {
+                uint32_t x = 0;
 #pragma unroll
-                for (int i = 0; i < V; ++i)
-                    acc_elem(acc[j], widen<DT>(vec_elem_bits<DT>(cv[j], i)), R[i], equal_nan);
+                for (int w = 0; w < Raw<DT>::kWords; ++w) x |= cr.w[w] ^ rraw.w[w];
+                if (ballot(x != 0u)) W.bitdiff |= 1u << j;
+            }
+            // fast path
+            uint32_t nmatch = 0;
+            float tmax = 0.f, qmax = 0.f, acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < kE; ++i) {
+                const float s = elem<DT>(cr, i) - r[i];
+                nmatch += popc(ballot(fabsf(s) <= tol[i]));
+                tmax = fmaxf(tmax, fabsf(s));
+                qmax = fmaxf(qmax, fabsf(s * inv[i]));  // 0 * inf = NaN is ignored by fmaxf
+                acc = fmaf(s, s, acc);
+            }
+            if (ballot(!(acc < __builtin_inff()))) {
+                // NaN, infinity or a squared difference beyond binary32
+                exact_chunk<DT, KG>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], W, j,
+                                    &s_max[wave][j], s_nf[wave][j]);
+                continue;
+            }
+            W.mism[j] += (uint32_t)kChunk - nmatch;
+            const WaveMaxPtr M = &s_max[wave][j];
+            const float cur_abs = M->abs, thr = M->relT;
+            if (ballot(tmax > cur_abs)) M->abs = fmaxf(cur_abs, wave_max_f(tmax));
+            // lanes whose differences are all tiny but not all zero
+            const bool tiny = (__float_as_uint(tmax) - 1u) < (__float_as_uint(kTiny) - 1u);
+            double add = (double)acc;
+            if (ballot(tiny)) {
+                if (tiny) {
+                    double t = 0.0;
+#pragma unroll
+                    for (int i = 0; i < kE; ++i) {
+                        const double s = (double)(elem<DT>(cr, i) - r[i]);
+                        t = __builtin_fma(s, s, t);
+                    }
+                    add = t;
+                }
+            }
+            atomicAdd(&s_ssd[j][threadIdx.x], add);
+            // max-rel filter: q~ >= q (1 - 2^-21) whenever q is finite and
+            // |r| is normal (and q~ over-estimates q otherwise), so a ratio
+            // above the state's passes q~ > relT; the exact comparison then
+            // decides.
+            if (ballot(qmax > thr)) {
+                float bd = M->relD, ba = M->relA;
+                bool has = false;
+                if (qmax > thr) {
+#pragma unroll
+                    for (int i = 0; i < kE; ++i) {
+                        const float s = elem<DT>(cr, i) - r[i];
+                        if (fabsf(s * inv[i]) > thr) {
+                            const float d = fabsf(s), a = fabsf(r[i]);
+                            if (ratio_gt(d, a, bd, ba)) {
+                                bd = d;
+                                ba = a;
+                                has = true;
+                            }
+                        }
+                    }
+                }
+                if (ballot(has)) rel_propose(M, has, bd, ba);
             }
         }
     }
-    // Ragged tail (numel not a multiple of V): stripe 0 of each group.
+
+    // Ragged tail: the last numel mod 512 elements, by stripe 0 of each
+    // group, one element per thread, exact path (out-of-range lanes compare
+    // 0 with 0, which changes no statistic).
     if (stripe == 0) {
-        const uint64_t first = p.n_vec * V;
-        const uint64_t i = first + threadIdx.x;
-        if (i < p.numel) {
-            const uint32_t rb = scalar_bits<DT>(p.ref, i);
-            const RefElem R = ref_elem(widen<DT>(rb), p.atol, p.rtol);
-            if (R.fin) ssr = __builtin_fma((double)R.r, (double)R.r, ssr);
+        const uint64_t first = n_chunks * kChunk;
+        for (uint64_t base = first; base < p.numel; base += kThreads) {
+            const uint64_t e = base + threadIdx.x;
+            const bool valid = e < p.numel;
+            uint32_t rb = 0;
+            if (valid) rb = DT == DT_F32 ? ((const uint32_t*)p.ref)[e] : ((const uint16_t*)p.ref)[e];
+            float r[kE];
+            r[0] = widen_bits<DT>(rb);
+#pragma unroll
+            for (int i = 1; i < kE; ++i) r[i] = 0.f;
+            if (__builtin_isfinite(r[0])) ssr = __builtin_fma((double)r[0], (double)r[0], ssr);
 #pragma unroll
             for (int j = 0; j < KG; ++j) {
-                if (j < kg) {
-                    const uint32_t cb = scalar_bits<DT>(p.table[j0 + j].data, i);
-                    acc[j].bitdiff |= cb ^ rb;
-                    acc_elem(acc[j], widen<DT>(cb), R, equal_nan);
-                }
+                if (j >= kg) continue;
+                uint32_t cb = 0;
+                if (valid)
+                    cb = DT == DT_F32 ? ((const uint32_t*)cand[j])[e] : ((const uint16_t*)cand[j])[e];
+                if (ballot(cb != rb)) W.bitdiff |= 1u << j;
+                Raw<DT> cr;
+#pragma unroll
+                for (int w = 0; w < Raw<DT>::kWords; ++w) cr.w[w] = 0u;
+                cr.w[0] = cb;
+                // element 0 carries the tail element; elements 1..7 compare 0 with 0
+                exact_chunk<DT, KG>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], W, j,
+                                    &s_max[wave][j], s_nf[wave][j]);
             }
         }
     }
@@ -185,162 +454,212 @@ __global__ __launch_bounds__(kThreads) void screen_kernel(ScreenParams p) {
     // Wave reductions, then the work-group's partials in wave order.
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
-        if (j < kg) {
-            const uint32_t m = wave_sum_u32(acc[j].mism);
-            const uint32_t na = wave_sum_u32(acc[j].nan);
-            const uint32_t pi = wave_sum_u32(acc[j].pinf);
-            const uint32_t ni = wave_sum_u32(acc[j].ninf);
-            const uint32_t ma = wave_max_u32(__float_as_uint(acc[j].max_abs));
-            const uint32_t mr = wave_max_u32(__float_as_uint(acc[j].max_rel));
-            const uint32_t bd = wave_or_u32(acc[j].bitdiff);
-            const double sd = wave_sum_f64(acc[j].ssd);
-            if (lane == 0) {
-                lds[j].u[wave][PF_MISM] = m;
-                lds[j].u[wave][PF_NAN] = na;
-                lds[j].u[wave][PF_PINF] = pi;
-                lds[j].u[wave][PF_NINF] = ni;
-                lds[j].u[wave][PF_MAXABS] = ma;
-                lds[j].u[wave][PF_MAXREL] = mr;
-                lds[j].u[wave][PF_BITDIFF] = bd;
-                lds[j].ssd[wave] = sd;
-            }
+        if (j >= kg) continue;
+        const double sd = wave_sum_f64(s_ssd[j][threadIdx.x]);
+        if (lane == 0) {
+            WaveOut& o = s_out[wave][j];
+            o.u[PF_MISM] = W.mism[j];
+            o.u[PF_NAN] = s_nf[wave][j].nan;
+            o.u[PF_PINF] = s_nf[wave][j].pinf;
+            o.u[PF_NINF] = s_nf[wave][j].ninf;
+            const WaveMax& M = s_max[wave][j];
+            o.u[PF_MAXABS] = __float_as_uint(M.abs);
+            o.u[PF_MAXREL] = __float_as_uint(M.relA > 0.f ? M.relD / M.relA : __builtin_inff());
+            o.u[PF_BITDIFF] = (W.bitdiff >> j) & 1u;
+            o.ssd = sd;
         }
     }
     {
         const double sr = wave_sum_f64(ssr);
-        if (lane == 0) lds[0].ssr[wave] = sr;
+        if (lane == 0) s_ssr[wave] = sr;
     }
     __syncthreads();
 
     const int C = p.blocks_per_group;
+    const size_t plane = (size_t)p.n_acc * C;
     if (threadIdx.x < kg) {
         const int j = threadIdx.x;
-        const Lds& L = lds[j];
         uint32_t m = 0, na = 0, pi = 0, ni = 0, ma = 0, mr = 0, bd = 0;
         double sd = 0.0;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
-            m += L.u[w][PF_MISM];
-            na += L.u[w][PF_NAN];
-            pi += L.u[w][PF_PINF];
-            ni += L.u[w][PF_NINF];
-            ma = max(ma, L.u[w][PF_MAXABS]);
-            mr = max(mr, L.u[w][PF_MAXREL]);
-            bd |= L.u[w][PF_BITDIFF];
-            sd += L.ssd[w];
+            const WaveOut& o = s_out[w][j];
+            m += o.u[PF_MISM];
+            na += o.u[PF_NAN];
+            pi += o.u[PF_PINF];
+            ni += o.u[PF_NINF];
+            ma = max(ma, o.u[PF_MAXABS]);
+            mr = max(mr, o.u[PF_MAXREL]);
+            bd |= o.u[PF_BITDIFF];
+            sd += o.ssd;
         }
         const size_t row = (size_t)(j0 + j) * C + stripe;
-        const size_t plane = (size_t)p.n_acc * C;
-        p.part_u32[PF_MISM * plane + row] = m;
-        p.part_u32[PF_NAN * plane + row] = na;
-        p.part_u32[PF_PINF * plane + row] = pi;
-        p.part_u32[PF_NINF * plane + row] = ni;
-        p.part_u32[PF_MAXABS * plane + row] = ma;
-        p.part_u32[PF_MAXREL * plane + row] = mr;
-        p.part_u32[PF_BITDIFF * plane + row] = bd;
-        p.part_ssd[row] = sd;
+        st_coherent(&p.part_u32[PF_MISM * plane + row], m);
+        st_coherent(&p.part_u32[PF_NAN * plane + row], na);
+        st_coherent(&p.part_u32[PF_PINF * plane + row], pi);
+        st_coherent(&p.part_u32[PF_NINF * plane + row], ni);
+        st_coherent(&p.part_u32[PF_MAXABS * plane + row], ma);
+        st_coherent(&p.part_u32[PF_MAXREL * plane + row], mr);
+        st_coherent(&p.part_u32[PF_BITDIFF * plane + row], bd);
+        st_coherent(&p.part_ssd[row], sd);
     }
-    if (threadIdx.x == 0) {
-        double sr = 0.0;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) sr += lds[0].ssr[w];
-        p.part_ssr[(size_t)g * C + stripe] = sr;
-    }
+    if (threadIdx.x == 0)
+        st_coherent(&p.part_ssr[(size_t)g * C + stripe], (s_ssr[0] + s_ssr[1]) + (s_ssr[2] + s_ssr[3]));
 
-    // Last work-group of this candidate group finishes it.
-    __threadfence();
+    // Two-level finish.  Level 1: the last work-group to arrive in each set
+    // of 16 consecutive stripes (a "super-group") combines their partials,
+    // one DPP row (16 lanes, one stripe each) per candidate.  Level 2: the
+    // last super-group combiner of the candidate group combines the
+    // super-group partials (each lane takes super-groups q = lane, lane + 16,
+    // ... in order) and writes the records.  Fixed orders throughout, so the
+    // binary64 sums are the same bits on every call.
+    const int S = p.n_super;
+    const int m = stripe >> 4;
+    const int msize = min(16, C - 16 * m);
+    complete_stores();
     __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t t = atomicAdd(&p.tickets[g], 1u);
-        s_is_last = (t == (uint32_t)C - 1u) ? 1u : 0u;
-    }
+    if (threadIdx.x == 0) s_is_last = ticket(&p.tickets1[(size_t)g * S + m]) == (uint32_t)msize - 1u;
     __syncthreads();
     if (!s_is_last) return;
-    __threadfence();
 
-    // Fixed-order combine over stripes: thread t takes stripes t, t+256, ...
-    // in order, then the work-group combines threads in a fixed tree.
-    __shared__ double s_red[kWaves];
-    __shared__ uint64_t s_cnt[kWaves][4];
-    __shared__ uint32_t s_mx[kWaves][3];
-
-    double total_ssr;
+    const int jj = threadIdx.x >> 4;
+    const int sl = threadIdx.x & 15;
     {
-        double acc_r = 0.0;
-        for (int s = threadIdx.x; s < C; s += kThreads) acc_r += p.part_ssr[(size_t)g * C + s];
-        const double w = wave_sum_f64(acc_r);
-        if (lane == 0) s_red[wave] = w;
-        __syncthreads();
-        total_ssr = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
-        __syncthreads();
+        const bool have = sl < msize;
+        const int s = 16 * m + sl;
+        if (jj < kg) {
+            const size_t idx = (size_t)(j0 + jj) * C + s;
+            uint64_t mi = 0, na = 0, pi = 0, ni = 0;
+            uint32_t ma = 0, mr = 0, bd = 0;
+            double sd = 0.0;
+            if (have) {
+                mi = ld_coherent(&p.part_u32[PF_MISM * plane + idx]);
+                na = ld_coherent(&p.part_u32[PF_NAN * plane + idx]);
+                pi = ld_coherent(&p.part_u32[PF_PINF * plane + idx]);
+                ni = ld_coherent(&p.part_u32[PF_NINF * plane + idx]);
+                ma = ld_coherent(&p.part_u32[PF_MAXABS * plane + idx]);
+                mr = ld_coherent(&p.part_u32[PF_MAXREL * plane + idx]);
+                bd = ld_coherent(&p.part_u32[PF_BITDIFF * plane + idx]);
+                sd = ld_coherent(&p.part_ssd[idx]);
+            }
+            mi = row_sum_u64(mi);
+            na = row_sum_u64(na);
+            pi = row_sum_u64(pi);
+            ni = row_sum_u64(ni);
+            ma = row_max_u32(ma);
+            mr = row_max_u32(mr);
+            bd = row_or_u32(bd);
+            sd = row_sum_f64(sd);
+            if (sl == 0) {
+                Part2* q = &p.part2[(size_t)(j0 + jj) * S + m];
+                st_coherent(&q->mism, mi);
+                st_coherent(&q->nan, na);
+                st_coherent(&q->pinf, pi);
+                st_coherent(&q->ninf, ni);
+                st_coherent(&q->maxabs, ma);
+                st_coherent(&q->maxrel, mr);
+                st_coherent(&q->bitdiff, bd);
+                st_coherent(&q->ssd, sd);
+            }
+        }
+        if (jj == 0) {
+            double sr = have ? ld_coherent(&p.part_ssr[(size_t)g * C + s]) : 0.0;
+            sr = row_sum_f64(sr);
+            if (sl == 0) st_coherent(&p.part2_ssr[(size_t)g * S + m], sr);
+        }
     }
+    if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
 
-    const size_t plane = (size_t)p.n_acc * C;
-    for (int j = 0; j < kg; ++j) {
-        const size_t base = (size_t)(j0 + j) * C;
+    complete_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) s_is_last = ticket(&p.tickets2[g]) == (uint32_t)S - 1u;
+    __syncthreads();
+    if (!s_is_last) return;
+
+    if (jj < kg) {
+        uint64_t mi = 0, na = 0, pi = 0, ni = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
-        uint64_t m64 = 0, na64 = 0, pi64 = 0, ni64 = 0;
-        double sd = 0.0;
-        for (int s = threadIdx.x; s < C; s += kThreads) {
-            m64 += p.part_u32[PF_MISM * plane + base + s];
-            na64 += p.part_u32[PF_NAN * plane + base + s];
-            pi64 += p.part_u32[PF_PINF * plane + base + s];
-            ni64 += p.part_u32[PF_NINF * plane + base + s];
-            ma = max(ma, p.part_u32[PF_MAXABS * plane + base + s]);
-            mr = max(mr, p.part_u32[PF_MAXREL * plane + base + s]);
-            bd |= p.part_u32[PF_BITDIFF * plane + base + s];
-            sd += p.part_ssd[base + s];
+        double sd = 0.0, sr = 0.0;
+        const Part2* row = p.part2 + (size_t)(j0 + jj) * S;
+        const double* rs = p.part2_ssr + (size_t)g * S;
+        for (int q0 = sl; q0 < S; q0 += 64) {
+            Part2 v[4];
+            double w[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int q = q0 + 16 * u;
+                if (q < S) {
+                    const Part2* e = &row[q];
+                    v[u].mism = ld_coherent(&e->mism);
+                    v[u].nan = ld_coherent(&e->nan);
+                    v[u].pinf = ld_coherent(&e->pinf);
+                    v[u].ninf = ld_coherent(&e->ninf);
+                    v[u].maxabs = ld_coherent(&e->maxabs);
+                    v[u].maxrel = ld_coherent(&e->maxrel);
+                    v[u].bitdiff = ld_coherent(&e->bitdiff);
+                    v[u].ssd = ld_coherent(&e->ssd);
+                    w[u] = ld_coherent(&rs[q]);
+                } else {
+                    v[u] = Part2{0, 0, 0, 0, 0u, 0u, 0u, 0u, 0.0};
+                    w[u] = 0.0;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                mi += v[u].mism;
+                na += v[u].nan;
+                pi += v[u].pinf;
+                ni += v[u].ninf;
+                ma = max(ma, v[u].maxabs);
+                mr = max(mr, v[u].maxrel);
+                bd |= v[u].bitdiff;
+                sd += v[u].ssd;
+                sr += w[u];
+            }
         }
-        const uint64_t wm = wave_sum_u64(m64), wn = wave_sum_u64(na64);
-        const uint64_t wp = wave_sum_u64(pi64), wq = wave_sum_u64(ni64);
-        const uint32_t wma = wave_max_u32(ma), wmr = wave_max_u32(mr), wbd = wave_or_u32(bd);
-        const double wsd = wave_sum_f64(sd);
-        if (lane == 0) {
-            s_cnt[wave][0] = wm;
-            s_cnt[wave][1] = wn;
-            s_cnt[wave][2] = wp;
-            s_cnt[wave][3] = wq;
-            s_mx[wave][0] = wma;
-            s_mx[wave][1] = wmr;
-            s_mx[wave][2] = wbd;
-            s_red[wave] = wsd;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
+        mi = row_sum_u64(mi);
+        na = row_sum_u64(na);
+        pi = row_sum_u64(pi);
+        ni = row_sum_u64(ni);
+        ma = row_max_u32(ma);
+        mr = row_max_u32(mr);
+        bd = row_or_u32(bd);
+        sd = row_sum_f64(sd);
+        sr = row_sum_f64(sr);
+        if (sl == 0) {
             kb_stats st;
             st.numel = p.numel;
-            st.mismatches = (s_cnt[0][0] + s_cnt[1][0]) + (s_cnt[2][0] + s_cnt[3][0]);
-            st.nan_count = (s_cnt[0][1] + s_cnt[1][1]) + (s_cnt[2][1] + s_cnt[3][1]);
-            st.pos_inf_count = (s_cnt[0][2] + s_cnt[1][2]) + (s_cnt[2][2] + s_cnt[3][2]);
-            st.neg_inf_count = (s_cnt[0][3] + s_cnt[1][3]) + (s_cnt[2][3] + s_cnt[3][3]);
-            const double ssd_t = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
-            st.sum_sq_diff = ssd_t;
-            st.sum_sq_ref = total_ssr;
-            st.rel_l2 = total_ssr > 0.0 ? sqrt(ssd_t / total_ssr)
-                                        : (ssd_t == 0.0 ? 0.0 : __builtin_inf());
-            st.max_abs_err = __uint_as_float(max(max(s_mx[0][0], s_mx[1][0]), max(s_mx[2][0], s_mx[3][0])));
-            st.max_rel_err = __uint_as_float(max(max(s_mx[0][1], s_mx[1][1]), max(s_mx[2][1], s_mx[3][1])));
-            st.bitwise_equal = ((s_mx[0][2] | s_mx[1][2]) | (s_mx[2][2] | s_mx[3][2])) == 0u ? 1 : 0;
+            st.mismatches = mi;
+            st.nan_count = na;
+            st.pos_inf_count = pi;
+            st.neg_inf_count = ni;
+            st.sum_sq_diff = sd;
+            st.sum_sq_ref = sr;
+            st.rel_l2 = sr > 0.0 ? sqrt(sd / sr) : (sd == 0.0 ? 0.0 : __builtin_inf());
+            st.max_abs_err = __uint_as_float(ma);
+            st.max_rel_err = __uint_as_float(mr);
+            st.bitwise_equal = bd == 0u ? 1 : 0;
             st.status = KB_STATUS_OK;
-            p.stats[p.table[j0 + j].index] = st;
+            p.stats[table[j0 + jj].index] = st;
         }
-        __syncthreads();
     }
     // Group 0's finisher also writes the rejected candidates' records.
     if (g == 0) {
-        for (int k = p.n_acc + threadIdx.x; k < p.n_cands; k += kThreads) {
+        for (int k = p.rej_start + threadIdx.x; k < p.n_table; k += kThreads) {
             kb_stats st = {};
-            st.status = p.table[k].status;
-            p.stats[p.table[k].index] = st;
+            st.status = table[k].status;
+            p.stats[table[k].index] = st;
         }
     }
     // Leave the ticket at zero for the next call on this workspace.
-    if (threadIdx.x == 0) p.tickets[g] = 0u;
+    if (threadIdx.x == 0) p.tickets2[g] = 0u;
 }
 
-__global__ void records_only_kernel(const CandEntry* table, int n_cands, uint64_t numel,
-                                    kb_stats* stats) {
-    for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_cands; k += gridDim.x * blockDim.x) {
+__global__ void records_only_kernel(const CandEntry* uploaded, InlineTable tab, int table_inline,
+                                    int n_table, uint64_t numel, kb_stats* stats) {
+    const CandEntry* table = table_inline ? tab.e : uploaded;
+    for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_table; k += gridDim.x * blockDim.x) {
+        if (table[k].index < 0) continue;  // padding
         kb_stats st = {};
         st.status = table[k].status;
         if (st.status == KB_STATUS_OK) {
@@ -352,38 +671,91 @@ __global__ void records_only_kernel(const CandEntry* table, int n_cands, uint64_
 }
 
 template <int DT, int KG>
-hipError_t launch_kg(const ScreenPlan& plan, const ScreenParams& p, hipStream_t stream) {
+hipError_t launch_kg(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                     hipStream_t stream) {
     const unsigned grid = (unsigned)plan.n_groups * (unsigned)plan.blocks_per_group;
-    hipLaunchKernelGGL((screen_kernel<DT, KG>), dim3(grid), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((screen_kernel<DT, KG>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
     return hipGetLastError();
 }
 
+template <int DT, int KG>
+int occupancy_kg() {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG>, kThreads, 0) !=
+        hipSuccess)
+        return 0;
+    return n;
+}
+
 template <int DT>
-hipError_t launch_dt(const ScreenPlan& plan, const ScreenParams& p, hipStream_t stream) {
+int occupancy_dt(int kg) {
+    switch (kg) {
+        case 1: return occupancy_kg<DT, 1>();
+        case 2: return occupancy_kg<DT, 2>();
+        case 4: return occupancy_kg<DT, 4>();
+        case 8: return occupancy_kg<DT, 8>();
+        default: return occupancy_kg<DT, 16>();
+    }
+}
+
+template <int DT>
+hipError_t launch_dt(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                     hipStream_t stream) {
     switch (plan.kg) {
-        case 1: return launch_kg<DT, 1>(plan, p, stream);
-        case 2: return launch_kg<DT, 2>(plan, p, stream);
-        case 4: return launch_kg<DT, 4>(plan, p, stream);
-        case 8: return launch_kg<DT, 8>(plan, p, stream);
-        default: return launch_kg<DT, 16>(plan, p, stream);
+        case 1: return launch_kg<DT, 1>(plan, p, tab, stream);
+        case 2: return launch_kg<DT, 2>(plan, p, tab, stream);
+        case 4: return launch_kg<DT, 4>(plan, p, tab, stream);
+        case 8: return launch_kg<DT, 8>(plan, p, tab, stream);
+        default: return launch_kg<DT, 16>(plan, p, tab, stream);
     }
 }
 
 }  // namespace
 
-hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, hipStream_t stream) {
+hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                         hipStream_t stream) {
     switch (plan.dtype) {
-        case DT_F32: return launch_dt<DT_F32>(plan, p, stream);
-        case DT_F16: return launch_dt<DT_F16>(plan, p, stream);
-        default: return launch_dt<DT_BF16>(plan, p, stream);
+        case DT_F32: return launch_dt<DT_F32>(plan, p, tab, stream);
+        case DT_F16: return launch_dt<DT_F16>(plan, p, tab, stream);
+        default: return launch_dt<DT_BF16>(plan, p, tab, stream);
     }
 }
 
-hipError_t launch_records_only(const CandEntry* table, int n_cands, uint64_t numel,
-                               kb_stats* stats, hipStream_t stream) {
-    const int grid = (n_cands + 255) / 256;
-    hipLaunchKernelGGL(records_only_kernel, dim3(grid), dim3(256), 0, stream, table, n_cands,
-                       numel, stats);
+__global__ void zero_fill_kernel(uint4* dst, uint64_t n16) {
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        dst[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream) {
+    // the workspace size is always a multiple of 256 bytes
+    const uint64_t n16 = n / 16;
+    if (n16 == 0) return hipSuccess;
+    const uint64_t want = (n16 + 255) / 256;
+    const unsigned grid = (unsigned)(want < 4096 ? want : 4096);
+    hipLaunchKernelGGL(zero_fill_kernel, dim3(grid), dim3(256), 0, stream, (uint4*)dst, n16);
+    return hipGetLastError();
+}
+
+int screen_blocks_per_cu(int dtype, int kg) {
+    // The occupancy of a kernel does not change during the process.
+    static int cache[3][5] = {{-1, -1, -1, -1, -1}, {-1, -1, -1, -1, -1}, {-1, -1, -1, -1, -1}};
+    const int ki = kg == 1 ? 0 : kg == 2 ? 1 : kg == 4 ? 2 : kg == 8 ? 3 : 4;
+    const int di = dtype == DT_F32 ? 0 : dtype == DT_F16 ? 1 : 2;
+    int v = __atomic_load_n(&cache[di][ki], __ATOMIC_RELAXED);
+    if (v < 0) {
+        v = dtype == DT_F32 ? occupancy_dt<DT_F32>(kg)
+                            : dtype == DT_F16 ? occupancy_dt<DT_F16>(kg) : occupancy_dt<DT_BF16>(kg);
+        __atomic_store_n(&cache[di][ki], v, __ATOMIC_RELAXED);
+    }
+    return v;
+}
+
+hipError_t launch_records_only(const CandEntry* table, const InlineTable& tab, int table_inline,
+                               int n_table, uint64_t numel, kb_stats* stats, hipStream_t stream) {
+    const int grid = (n_table + 255) / 256;
+    hipLaunchKernelGGL(records_only_kernel, dim3(grid), dim3(256), 0, stream, table, tab,
+                       table_inline, n_table, numel, stats);
     return hipGetLastError();
 }
 

@@ -177,3 +177,23 @@ def test_missing_library_fails_loudly(monkeypatch):
     monkeypatch.setattr(kb, "LIB_PATH", "/nonexistent/libkb.so")
     with pytest.raises(kb.KbError):
         kb.lib()
+
+
+def test_summarize_on_host(L):
+    recs = []
+    for status, mism in ((0, 0), (kb.KB_REJECT_DTYPE, 0), (0, 3), (0, 0), (kb.KB_REJECT_NULL, 0)):
+        r = {name: 0 for name, _ in kb.KbStats._fields_}
+        r["status"], r["mismatches"] = status, mism
+        recs.append(r)
+    assert kb.kb_summarize(recs) == {"n_candidates": 5, "n_passed": 2, "n_rejected": 2,
+                                     "n_failed": 1, "first_passed": 0, "first_failed": 1}
+    assert kb.kb_summarize([])["n_candidates"] == 0
+    assert kb.lib().kb_summarize(None, 3, None) == kb.KB_ERR_INVALID_ARG
+
+
+def test_workspace_init_argument_errors(L):
+    f = kb.lib().kb_screen_workspace_init
+    assert f(None, 256, None) == kb.KB_ERR_WORKSPACE
+    assert f(0x1000, 0, None) == kb.KB_ERR_WORKSPACE
+    assert f(0x1008, 256, None) == kb.KB_ERR_ALIGNMENT
+    assert f(0x1000, 250, None) == kb.KB_ERR_ALIGNMENT

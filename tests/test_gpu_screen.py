@@ -223,7 +223,7 @@ def test_all_rejected_and_empty(dev):
 
 # --------------------------------------------------- determinism & reuse ---
 
-def test_determinism_and_dirty_workspace(dev):
+def test_determinism_and_workspace_reuse(dev):
     say("determinism")
     w = synth.build("c2", dev, seed=1, scale=1 / 16)
     K = len(w.cands)
@@ -231,7 +231,10 @@ def test_determinism_and_dirty_workspace(dev):
     st = kb.alloc_stats(K, dev)
     first = None
     for it in range(20):
-        ws.fill_(0xFF if it % 2 else 0x5A)  # contents must not matter
+        if it % 5 == 4:
+            # a dirtied workspace is usable again after re-initialisation
+            ws.fill_(0xFF if it % 2 else 0x5A)
+            kb.kb_screen_workspace_init(ws)
         kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, 0, ws, st)
         recs, _ = kb.kb_screen_stats(st, K)
         if first is None:
@@ -239,6 +242,41 @@ def test_determinism_and_dirty_workspace(dev):
         else:
             assert recs == first, it
     assert_records_match(first, oracle_records(w.ref, w.cands, w.atol, w.rtol), "c2 1/16")
+
+
+def test_workspace_reinit_between_sizes(dev):
+    say("workspace reuse across sizes")
+    big = synth.build("c4", dev, seed=2, scale=1 / 256, K=40)
+    small = synth.build("c1", dev, seed=2)
+    nbytes = max(kb.kb_screen_workspace_bytes(40, big.numel, kb.KB_F16),
+                 kb.kb_screen_workspace_bytes(4, small.numel, kb.KB_F32))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    for w, code in ((big, kb.KB_F16), (small, kb.KB_F32), (big, kb.KB_F16)):
+        kb.kb_screen_workspace_init(ws)
+        st = kb.alloc_stats(len(w.cands), dev)
+        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, 0, ws, st)
+        recs, _ = kb.kb_screen_stats(st, len(w.cands))
+        assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), w.name)
+
+
+def test_pinned_host_records_pipeline(dev):
+    say("pinned host records")
+    w = synth.build("c2", dev, seed=4, scale=1 / 64)
+    scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol, host_slots=2)
+    ev = [torch.cuda.Event(), torch.cuda.Event()]
+    seen = []
+    for i in range(6):
+        scr.launch(i % 2)
+        ev[i % 2].record()
+        if i > 0:
+            ev[(i - 1) % 2].synchronize()
+            seen.append((scr.summarize((i - 1) % 2).as_dict(), scr.records((i - 1) % 2)))
+    ev[5 % 2].synchronize()
+    seen.append((scr.summarize(5 % 2).as_dict(), scr.records(5 % 2)))
+    orc = oracle_records(w.ref, w.cands, w.atol, w.rtol)
+    for summ, recs in seen:
+        assert_records_match(recs, orc, "pinned slot")
+        assert summ == kb.kb_summarize(recs)
 
 
 def test_stream_ordering_with_side_stream(dev):
