@@ -57,7 +57,6 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kE = 8;                 // elements per lane per chunk
 constexpr int kChunk = 64 * kE;       // elements per wave per chunk
 constexpr float kTiny = 0x1p-60f;     // below this binary32 squares may underflow
-constexpr float kRelMargin = 0x1.ffffep-1f;  // 1 - 2^-20: max-rel filter slack
 
 // Raw storage of one lane's 8 elements of a chunk.
 template <int DT>
@@ -66,9 +65,16 @@ struct Raw {
     uint32_t w[kWords];
 };
 
-// 16-byte vector loaded through a global (address space 1) pointer, so
-// that candidate pointers read from the launch table produce global_load
-// rather than flat_load instructions.
+// Bytes of one tensor per 512-element chunk.
+template <int DT>
+constexpr uint64_t chunk_bytes() {
+    return DT == DT_F32 ? 4 * kChunk : 2 * kChunk;
+}
+
+// Global (address space 1) pointers.  Tensor bases are wave-uniform and
+// kept in scalar registers; a load adds the lane's 32-bit byte offset, so
+// the address costs no vector instruction (global_load with a scalar base).
+typedef const __attribute__((address_space(1))) char* gbytes;
 typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) v4u32* gvec;
 
@@ -82,22 +88,26 @@ __device__ __forceinline__ v4u32 ld16(gvec p) {
 // (two fully coalesced 1 KB wave loads); 16-bit: elements 8l..8l+7.  NT
 // marks the loads nontemporal: every candidate byte is used once, and
 // streaming it past the caches leaves them to the reference, which the
-// other candidate groups of the stripe re-read.
+// other candidate groups of the stripe re-read.  base is the chunk's first
+// byte (wave-uniform), off = 16 * lane.
 template <int DT, bool NT>
-__device__ __forceinline__ Raw<DT> load_chunk(const void* base, uint64_t chunk, int lane) {
+__device__ __forceinline__ Raw<DT> load_chunk(gbytes base, uint32_t off) {
     Raw<DT> x;
+    const v4u32 a = ld16<NT>((gvec)(base + off));
+    x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
     if constexpr (DT == DT_F32) {
-        const gvec p = (gvec)base + chunk * 128;
-        const v4u32 a = ld16<NT>(p + lane);
-        const v4u32 b = ld16<NT>(p + 64 + lane);
-        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+        const v4u32 b = ld16<NT>((gvec)(base + off + 1024u));
         x.w[4] = b.x; x.w[5] = b.y; x.w[6] = b.z; x.w[7] = b.w;
-    } else {
-        const gvec p = (gvec)base + chunk * 64;
-        const v4u32 a = ld16<NT>(p + lane);
-        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
     }
     return x;
+}
+
+// A pointer made explicitly wave-uniform (held in scalar registers).
+__device__ __forceinline__ gbytes uniform_ptr(const void* p) {
+    const uint64_t v = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (gbytes)(((uint64_t)hi << 32) | lo);
 }
 
 template <int DT>
@@ -116,6 +126,21 @@ __device__ __forceinline__ float elem(const Raw<DT>& x, int i) {
 }
 
 __device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__builtin_popcountll(m); }
+
+// Number of lanes with |s| <= tol (a wave-uniform count).  The compare and
+// the population count are one unit, so the 64-bit lane mask lives only in
+// VCC: counting eight elements per candidate this way keeps no masks alive
+// in scalar registers (which, with several candidates in flight, would
+// spill to vector lanes and cost more than the compares themselves).  No
+// wait states are needed between a VALU write of VCC and a SALU read.
+__device__ __forceinline__ uint32_t count_within(float s, float tol) {
+    uint32_t n;
+    asm("v_cmp_le_f32_e64 vcc, |%1|, %2\n\ts_bcnt1_i32_b64 %0, vcc"
+        : "=s"(n)
+        : "v"(s), "v"(tol)
+        : "vcc");
+    return n;
+}
 
 // Cross-work-group hand-off without L2 maintenance.  Partials are written
 // with agent-scope atomic stores (made coherent across XCDs by the store
@@ -153,53 +178,29 @@ __device__ __forceinline__ float wave_max_f(float v) {
 // keep registers live across the loop).
 __device__ __forceinline__ void opaque(float& x) { asm volatile("" : "+v"(x)); }
 
-// Wave-uniform accumulators of the work-group's candidates; the per-lane
-// sums of squares live in LDS.
-//
-// The max relative error is kept as the exact ratio relD / relA of the best
-// element seen (|c - r| and |r| as binary32; relA = 0 encodes +inf), and
-// relT = fl(fl(relD / relA) (1 - 2^-20)) is the threshold of the cheap filter.
-// Candidates that pass the filter are compared exactly (binary64 products
-// of binary32 values are exact), so elements that only tie the maximum cost
-// one comparison.  Rounding is monotone, so fl(max ratio) = max fl(ratio):
-// the record's max_rel_err is fl(relD / relA) of the final state.
-//
-// The counts stay in scalar registers; the maxima, written rarely, live in
-// LDS (one slot per wave and candidate, read back as a broadcast) so that
-// they take no registers across the loop.
-template <int KG>
-struct WaveAcc {
-    uint32_t mism[KG];  // mismatches seen by this wave
-    uint32_t bitdiff;   // bit j: candidate j differs somewhere in this wave's range
-};
-
-struct WaveMax {
-    float abs;   // exact max abs error seen by this wave
-    float relT;  // max-rel filter threshold
-    float relD;  // max-rel state: ratio relD / relA
-    float relA;
-};
-typedef volatile WaveMax* WaveMaxPtr;
-
-// d / a > bd / ba, exactly (finite non-negative binary32 inputs, a or ba may
-// be zero for an infinite ratio).
-__device__ __forceinline__ bool ratio_gt(float d, float a, float bd, float ba) {
-    return (double)d * (double)ba > (double)bd * (double)a;
-}
-
-// Wave step of the max-rel state: lanes with has = true propose the ratio
-// bd / ba (each greater than the current state); the state moves to the
-// proposal with the largest rounded quotient (lowest lane on ties).
-__device__ __forceinline__ void rel_propose(WaveMaxPtr M, bool has, float bd, float ba) {
-    const float key = has ? (ba > 0.f ? bd / ba : __builtin_inff()) : 0.f;
-    const uint32_t kmax = wave_max_u32(__float_as_uint(key));
-    const uint64_t win = ballot(has && __float_as_uint(key) == kmax);
-    if (win) {
-        const int lane = __builtin_ctzll(win);
-        M->relD = __uint_as_float(readlane_u32(__float_as_uint(bd), lane));
-        M->relA = __uint_as_float(readlane_u32(__float_as_uint(ba), lane));
-        M->relT = __uint_as_float(kmax) * kRelMargin;
+// Max relative error.  The record holds max over elements of fl(d / |r|)
+// (IEEE division, NaN quotients ignored); rounding is monotone, so this is
+// also fl of the largest exact ratio.  A wave keeps O, the exact maximum of
+// the quotients it has seen (wave-uniform, per candidate).  An element can
+// raise it only if d / a > O, i.e. d - O a > 0, and fma(-O, a, d) has the
+// sign of d - O a (one rounding; an exact zero stays zero), so
+//   y = fma(-O, |r|, |c - r|) > 0
+// is a filter that never misses (elements that tie O give y = 0 and are
+// skipped).  A wave whose filter passes computes the IEEE quotients of the
+// passing elements.  The one blind spot is underflow: y rounds to zero
+// when 0 < d - O a < 2^-150, which can hide an exceeding element only if
+// O a < 2^-125; lanes holding a nonzero |r| with O |r| < 2^-124 therefore
+// take the exact test too.
+__device__ __forceinline__ float rel_candidates(const float s[kE], const float r[kE], float O) {
+    float qm = 0.f;
+#pragma unroll
+    for (int i = 0; i < kE; ++i) {
+        const float d = fabsf(s[i]), a = fabsf(r[i]);
+        // exact sign of d - O a: the binary64 product of two binary32 values
+        // is exact, and one rounding keeps the sign
+        if (__builtin_fma(-(double)O, (double)a, (double)d) > 0.0) qm = fmaxf(qm, d / a);
     }
+    return qm;
 }
 
 // Non-finite counts (rare): per wave, per candidate, in LDS.
@@ -209,10 +210,13 @@ struct NonFinite {
 
 // The definition, element by element, for a whole lane chunk of one
 // candidate (every lane active).  Also the path for the ragged tail.
-template <int DT, int KG>
+// Updates the wave's mismatch count, the lane's max abs error, the wave's
+// max-rel O and non-finite counts, and adds the lane's binary64 squared
+// differences to its LDS slot.
+template <int DT>
 __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_in[kE], float atol,
                                             float rtol, bool equal_nan, double* ssd_slot,
-                                            WaveAcc<KG>& W, int j, WaveMaxPtr M, NonFinite& nf) {
+                                            uint32_t& mism, float& amax, float& O, NonFinite& nf) {
     float r[kE];
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -220,9 +224,7 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
         opaque(r[i]);
     }
     uint32_t nm = 0, nnan = 0, npinf = 0, nninf = 0;
-    float ma = 0.f;
-    float bd = M->relD, ba = M->relA;
-    bool has = false;
+    float ma = 0.f, qm = 0.f;
     double sd = 0.0;
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -238,24 +240,14 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
         const float tol = rfin ? __fadd_rn(atol, __fmul_rn(rtol, a)) : -1.0f;
         const bool match = (c == ri) || (d <= tol) || (equal_nan && cnan && __builtin_isnan(ri));
         nm += popc(ballot(!match));
-        if (d > ma) ma = d;
-        // the quotient d / a is a NaN for 0/0 and inf/inf and 0 for x/inf:
-        // none of these can raise the maximum
-        if (d > 0.f && a < __builtin_inff()) {
-            const float dd = d < __builtin_inff() ? d : 1.f;  // d = inf: ratio inf = 1/0
-            const float aa = d < __builtin_inff() ? a : 0.f;
-            if (ratio_gt(dd, aa, bd, ba)) {
-                bd = dd;
-                ba = aa;
-                has = true;
-            }
-        }
+        ma = fmaxf(ma, d);       // NaN differences are ignored
+        qm = fmaxf(qm, d / a);   // so are 0/0 and inf/inf
         if (rfin && __builtin_isfinite(c)) sd = __builtin_fma((double)d, (double)d, sd);
     }
     atomicAdd(ssd_slot, sd);
-    W.mism[j] += nm;
-    M->abs = fmaxf(M->abs, wave_max_f(ma));
-    if (ballot(has)) rel_propose(M, has, bd, ba);
+    mism += nm;
+    amax = fmaxf(amax, ma);
+    O = fmaxf(O, wave_max_f(qm));
     nf.nan += nnan;
     nf.pinf += npinf;
     nf.ninf += nninf;
@@ -267,25 +259,20 @@ struct WaveOut {
     double ssd;
 };
 
-// Minimum waves per SIMD the register allocator must allow: 3 keeps the
-// 16-bit kernels (which need more waves to cover the load latency of their
-// shorter per-candidate work) at 12 waves per CU; the fp32 kernels hold
-// twice the data per lane and are left to the allocator.
-constexpr int min_waves(int dt, int kg) { return (dt != DT_F32 && kg <= 8) ? 3 : 1; }
+// Minimum waves per SIMD the register allocator must allow.
+constexpr int min_waves(int dt, int kg) { return kg <= 8 ? 4 : 2; }
 
 template <int DT, int KG>
 __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
                                                                             InlineTable tab) {
-    const CandEntry* table = p.table_inline ? tab.e : p.table;
     __shared__ double s_ssd[KG][kThreads];  // lane sums of squared differences
     __shared__ WaveOut s_out[kWaves][KG];
     __shared__ double s_ssr[kWaves];
     __shared__ NonFinite s_nf[kWaves][KG];
-    __shared__ WaveMax s_max[kWaves][KG];
     __shared__ uint32_t s_is_last;
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int xcd = blockIdx.x & 7;
     const int slot = blockIdx.x >> 3;
     const int g = slot % p.n_groups;
@@ -295,132 +282,132 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
     const float atol = p.atol, rtol = p.rtol;
 
-    const void* cand[KG];
+    // The accepted part of the table is padded to whole groups with the
+    // reference, so all KG slots hold a readable tensor.
+    gbytes cand[KG];
 #pragma unroll
-    for (int j = 0; j < KG; ++j) cand[j] = table[j0 + j].data;  // padded: always valid
+    for (int j = 0; j < KG; ++j)
+        cand[j] = uniform_ptr(p.table_inline ? tab.e[j0 + j].data : p.table[j0 + j].data);
+    const gbytes ref = uniform_ptr(p.ref);
 
-    WaveAcc<KG> W;
-    W.bitdiff = 0u;
+    uint32_t mism[KG];  // wave-uniform mismatch counts
+    float amax[KG];     // lane max abs error
+    float orel[KG];     // wave-uniform max rel error
+    uint32_t bitdiff = 0u;  // bit j: candidate j differs somewhere in this wave's range
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
-        W.mism[j] = 0u;
+        mism[j] = 0u;
+        amax[j] = 0.f;
+        orel[j] = 0.f;
         s_ssd[j][threadIdx.x] = 0.0;
     }
-    if (lane < KG) s_max[wave][lane] = WaveMax{0.f, 0.f, 0.f, 1.f};  // ratio 0 / 1
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
     double ssr = 0.0;
 
+    const uint32_t off = 16u * (uint32_t)lane;
     const uint64_t n_chunks = p.numel / kChunk;
     const uint64_t wstride = (uint64_t)p.blocks_per_group * kWaves;
     for (uint64_t chunk = (uint64_t)stripe * kWaves + wave; chunk < n_chunks; chunk += wstride) {
-        const Raw<DT> rraw = load_chunk<DT, false>(p.ref, chunk, lane);
+        const uint64_t cb = chunk * chunk_bytes<DT>();
+        // Re-materialise the lane offset inside the loop so that instruction
+        // selection sees (scalar base + zero-extended 32-bit offset) and
+        // emits scalar-base loads instead of 64-bit vector address adds.
+        uint32_t o = off;
+        asm volatile("" : "+v"(o));
+        const Raw<DT> rraw = load_chunk<DT, false>(ref + cb, o);
         Raw<DT> craw[KG];
 #pragma unroll
-        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(cand[j], chunk, lane);
+        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(cand[j] + cb, o);
+
         // Reference side, once per element for all KG candidates.
-        float r[kE], tol[kE], inv[kE];
-        double rr = 0.0;
+        float r[kE], tol[kE];
+        float rr = 0.f;
+        uint32_t um = 0xFFFFFFFFu;
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
             r[i] = elem<DT>(rraw, i);
-            const uint32_t abits = __float_as_uint(r[i]) & 0x7FFFFFFFu;
-            tol[i] = __fadd_rn(atol, __fmul_rn(rtol, __uint_as_float(abits)));
-            // rcp of min(|r|, 2^100) (NaN clamps to 2^100; such lanes take the
-            // exact path): at least 1/|r| (1 - 2^-22) for normal |r|, an
-            // over-estimate for larger |r|, and very large or +inf for zero
-            // or subnormal |r| -- a conservative max-rel filter everywhere.
-            inv[i] = __builtin_amdgcn_rcpf(__uint_as_float(min(abits, 0x71800000u)));
-            rr = __builtin_fma((double)r[i], (double)r[i], rr);
+            tol[i] = __fadd_rn(atol, __fmul_rn(rtol, fabsf(r[i])));
+            rr = fmaf(r[i], r[i], rr);
+            // 2|r| - 2 in the bit domain: zeros map to the top, so the
+            // minimum picks the smallest nonzero |r|
+            um = min(um, (__float_as_uint(r[i]) << 1) - 2u);
         }
-        if (!(rr < __builtin_inf())) {  // a non-finite reference value in this lane
-            rr = 0.0;
+        const float amin_nz = um >= 0xFFFFFFFEu ? __builtin_inff() : __uint_as_float((um + 2u) >> 1);
+        // Reference squares: eight binary32 terms, exact in binary64 where
+        // the binary32 sum could lose precision (tiny or non-finite).
+        double rrd = (double)rr;
+        const bool rbad = !(rr >= 0x1p-100f && rr < __builtin_inff());
+        if (ballot(rbad)) {
+            if (rbad) {
+                double t = 0.0;
 #pragma unroll
-            for (int i = 0; i < kE; ++i)
-                if (__builtin_isfinite(r[i])) rr = __builtin_fma((double)r[i], (double)r[i], rr);
+                for (int i = 0; i < kE; ++i)
+                    if (__builtin_isfinite(r[i])) t = __builtin_fma((double)r[i], (double)r[i], t);
+                rrd = t;
+            }
         }
-        ssr += rr;
+        ssr += rrd;
 
 #pragma unroll
         for (int j = 0; j < KG; ++j) {
-            // Keep the scheduler from interleaving candidates: each holds a
-            // set of per-element ballot masks in scalar registers until they
-            // are counted, and interleaving multiplies the live set.  All the
-            // chunk's loads were issued above, so latency hiding is
-            // unaffected.
+            // Keep the scheduler from interleaving candidates: interleaving
+            // multiplies the live registers, and all the chunk's loads were
+            // issued above, so latency hiding is unaffected.
             __builtin_amdgcn_sched_barrier(0);
             const Raw<DT>& cr = craw[j];
             // bitwise identity on raw storage, until a difference is known
-            if (!((W.bitdiff >> j) & 1u)) {
+            if (!((bitdiff >> j) & 1u)) {
                 uint32_t x = 0;
 #pragma unroll
                 for (int w = 0; w < Raw<DT>::kWords; ++w) x |= cr.w[w] ^ rraw.w[w];
-                if (ballot(x != 0u)) W.bitdiff |= 1u << j;
+                if (ballot(x != 0u)) bitdiff |= 1u << j;
             }
             // fast path
+            const float O = orel[j];
+            float s[kE];
             uint32_t nmatch = 0;
-            float tmax = 0.f, qmax = 0.f, acc = 0.f;
+            float tmax = 0.f, acc = 0.f, ymax = -__builtin_inff();
 #pragma unroll
             for (int i = 0; i < kE; ++i) {
-                const float s = elem<DT>(cr, i) - r[i];
-                nmatch += popc(ballot(fabsf(s) <= tol[i]));
-                tmax = fmaxf(tmax, fabsf(s));
-                qmax = fmaxf(qmax, fabsf(s * inv[i]));  // 0 * inf = NaN is ignored by fmaxf
-                acc = fmaf(s, s, acc);
+                s[i] = elem<DT>(cr, i) - r[i];
+                nmatch += count_within(s[i], tol[i]);
+                tmax = fmaxf(tmax, fabsf(s[i]));
+                acc = fmaf(s[i], s[i], acc);
+                ymax = fmaxf(ymax, fmaf(-O, fabsf(r[i]), fabsf(s[i])));
             }
             if (ballot(!(acc < __builtin_inff()))) {
                 // NaN, infinity or a squared difference beyond binary32
-                exact_chunk<DT, KG>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], W, j,
-                                    &s_max[wave][j], s_nf[wave][j]);
+                exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
+                                amax[j], orel[j], s_nf[wave][j]);
                 continue;
             }
-            W.mism[j] += (uint32_t)kChunk - nmatch;
-            const WaveMaxPtr M = &s_max[wave][j];
-            const float cur_abs = M->abs, thr = M->relT;
-            if (ballot(tmax > cur_abs)) M->abs = fmaxf(cur_abs, wave_max_f(tmax));
-            // lanes whose differences are all tiny but not all zero
+            mism[j] += (uint32_t)kChunk - nmatch;
+            amax[j] = fmaxf(amax[j], tmax);
+            // lanes whose differences are all tiny but not all zero: binary32
+            // squares would underflow, so square in binary64
             const bool tiny = (__float_as_uint(tmax) - 1u) < (__float_as_uint(kTiny) - 1u);
             double add = (double)acc;
             if (ballot(tiny)) {
                 if (tiny) {
                     double t = 0.0;
 #pragma unroll
-                    for (int i = 0; i < kE; ++i) {
-                        const double s = (double)(elem<DT>(cr, i) - r[i]);
-                        t = __builtin_fma(s, s, t);
-                    }
+                    for (int i = 0; i < kE; ++i) t = __builtin_fma((double)s[i], (double)s[i], t);
                     add = t;
                 }
             }
             atomicAdd(&s_ssd[j][threadIdx.x], add);
-            // max-rel filter: q~ >= q (1 - 2^-21) whenever q is finite and
-            // |r| is normal (and q~ over-estimates q otherwise), so a ratio
-            // above the state's passes q~ > relT; the exact comparison then
-            // decides.
-            if (ballot(qmax > thr)) {
-                float bd = M->relD, ba = M->relA;
-                bool has = false;
-                if (qmax > thr) {
-#pragma unroll
-                    for (int i = 0; i < kE; ++i) {
-                        const float s = elem<DT>(cr, i) - r[i];
-                        if (fabsf(s * inv[i]) > thr) {
-                            const float d = fabsf(s), a = fabsf(r[i]);
-                            if (ratio_gt(d, a, bd, ba)) {
-                                bd = d;
-                                ba = a;
-                                has = true;
-                            }
-                        }
-                    }
-                }
-                if (ballot(has)) rel_propose(M, has, bd, ba);
+            const bool rel = ymax > 0.f || (O > 0.f && O * amin_nz < 0x1p-124f);
+            if (ballot(rel)) {
+                float qm = 0.f;
+                if (rel) qm = rel_candidates(s, r, O);
+                orel[j] = fmaxf(O, wave_max_f(qm));
             }
         }
     }
 
     // Ragged tail: the last numel mod 512 elements, by stripe 0 of each
-    // group, one element per thread, exact path (out-of-range lanes compare
-    // 0 with 0, which changes no statistic).
+    // group, one element per thread, exact path (out-of-range lanes and
+    // elements 1..7 compare 0 with 0, which changes no statistic).
     if (stripe == 0) {
         const uint64_t first = n_chunks * kChunk;
         for (uint64_t base = first; base < p.numel; base += kThreads) {
@@ -438,15 +425,15 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
                 if (j >= kg) continue;
                 uint32_t cb = 0;
                 if (valid)
-                    cb = DT == DT_F32 ? ((const uint32_t*)cand[j])[e] : ((const uint16_t*)cand[j])[e];
-                if (ballot(cb != rb)) W.bitdiff |= 1u << j;
+                    cb = DT == DT_F32 ? ((const __attribute__((address_space(1))) uint32_t*)cand[j])[e]
+                                      : ((const __attribute__((address_space(1))) uint16_t*)cand[j])[e];
+                if (ballot(cb != rb)) bitdiff |= 1u << j;
                 Raw<DT> cr;
 #pragma unroll
                 for (int w = 0; w < Raw<DT>::kWords; ++w) cr.w[w] = 0u;
                 cr.w[0] = cb;
-                // element 0 carries the tail element; elements 1..7 compare 0 with 0
-                exact_chunk<DT, KG>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], W, j,
-                                    &s_max[wave][j], s_nf[wave][j]);
+                exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
+                                amax[j], orel[j], s_nf[wave][j]);
             }
         }
     }
@@ -456,16 +443,16 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     for (int j = 0; j < KG; ++j) {
         if (j >= kg) continue;
         const double sd = wave_sum_f64(s_ssd[j][threadIdx.x]);
+        const float am = wave_max_f(amax[j]);
         if (lane == 0) {
             WaveOut& o = s_out[wave][j];
-            o.u[PF_MISM] = W.mism[j];
+            o.u[PF_MISM] = mism[j];
             o.u[PF_NAN] = s_nf[wave][j].nan;
             o.u[PF_PINF] = s_nf[wave][j].pinf;
             o.u[PF_NINF] = s_nf[wave][j].ninf;
-            const WaveMax& M = s_max[wave][j];
-            o.u[PF_MAXABS] = __float_as_uint(M.abs);
-            o.u[PF_MAXREL] = __float_as_uint(M.relA > 0.f ? M.relD / M.relA : __builtin_inff());
-            o.u[PF_BITDIFF] = (W.bitdiff >> j) & 1u;
+            o.u[PF_MAXABS] = __float_as_uint(am);
+            o.u[PF_MAXREL] = __float_as_uint(orel[j]);
+            o.u[PF_BITDIFF] = (bitdiff >> j) & 1u;
             o.ssd = sd;
         }
     }
@@ -576,6 +563,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     __syncthreads();
     if (!s_is_last) return;
 
+    const CandEntry* table = p.table_inline ? tab.e : p.table;
     if (jj < kg) {
         uint64_t mi = 0, na = 0, pi = 0, ni = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
