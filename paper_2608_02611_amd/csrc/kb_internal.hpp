@@ -64,7 +64,7 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
                ScreenPlan* plan);
 
 // Candidates per group the plan picks for n_cands candidates.
-int plan_group_size(int n_cands);
+int plan_group_size(int n_cands, int dtype);
 
 // Work-groups of screen_kernel<dtype, kg> resident per CU (occupancy query,
 // cached), or 0 on failure.

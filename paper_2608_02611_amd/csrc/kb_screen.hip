@@ -103,12 +103,13 @@ __device__ __forceinline__ Raw<DT> load_chunk(gbytes base, uint32_t off) {
 }
 
 // A pointer made explicitly wave-uniform (held in scalar registers).
-__device__ __forceinline__ gbytes uniform_ptr(const void* p) {
-    const uint64_t v = (uint64_t)p;
+__device__ __forceinline__ gbytes uniform_ptr(uint64_t v) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
     return (gbytes)(((uint64_t)hi << 32) | lo);
 }
+__device__ __forceinline__ gbytes uniform_ptr(const void* p) { return uniform_ptr((uint64_t)p); }
+__device__ __forceinline__ gbytes uniform_ptr(gbytes p) { return uniform_ptr((uint64_t)p); }
 
 template <int DT>
 __device__ __forceinline__ float widen_bits(uint32_t bits) {
@@ -190,15 +191,32 @@ __device__ __forceinline__ void opaque(float& x) { asm volatile("" : "+v"(x)); }
 // passing elements.  The one blind spot is underflow: y rounds to zero
 // when 0 < d - O a < 2^-150, which can hide an exceeding element only if
 // O a < 2^-125; lanes holding a nonzero |r| with O |r| < 2^-124 therefore
-// take the exact test too.
-__device__ __forceinline__ float rel_candidates(const float s[kE], const float r[kE], float O) {
+// take the exact test too -- unless O is an integer: then O a, like d, lies
+// on the 2^-149 grid of binary32, so a nonzero d - O a is at least 2^-149
+// and cannot underflow (the common case O = 1 of flushed subnormals).
+//
+// The waves of a work-group share what they learn: a wave that raises its
+// O also raises the work-group's copy in LDS, which every wave reads with
+// each chunk and takes into its own O.  A shared value is a quotient some
+// wave of the work-group recorded, so the maximum over the waves is
+// unchanged, and skipping elements with d / a <= O loses nothing; a stale
+// value only filters less.  (Sharing across the grid through global atomics
+// was measured to cost far more than it saves: every work-group contends
+// for the same few words.)
+//
+// The quotients of one lane's elements that pass the filter (0 if none).
+// GUARD: the lane may be in the underflow case, so the sign of d - O a is
+// taken in binary64 (the product of two binary32 values is exact there and
+// one rounding keeps the sign); otherwise the binary32 residual is exact.
+template <bool GUARD>
+__device__ __forceinline__ float rel_quotients(const float s[kE], const float r[kE], float O) {
     float qm = 0.f;
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
         const float d = fabsf(s[i]), a = fabsf(r[i]);
-        // exact sign of d - O a: the binary64 product of two binary32 values
-        // is exact, and one rounding keeps the sign
-        if (__builtin_fma(-(double)O, (double)a, (double)d) > 0.0) qm = fmaxf(qm, d / a);
+        const bool pass = GUARD ? __builtin_fma(-(double)O, (double)a, (double)d) > 0.0
+                                : fmaf(-O, a, d) > 0.f;
+        if (pass) qm = fmaxf(qm, d / a);
     }
     return qm;
 }
@@ -216,7 +234,7 @@ struct NonFinite {
 template <int DT>
 __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_in[kE], float atol,
                                             float rtol, bool equal_nan, double* ssd_slot,
-                                            uint32_t& mism, float& amax, float& O, NonFinite& nf) {
+                                            uint32_t& mism, uint32_t& amax, float& O, NonFinite& nf) {
     float r[kE];
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -246,11 +264,26 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
     }
     atomicAdd(ssd_slot, sd);
     mism += nm;
-    amax = fmaxf(amax, ma);
+    amax = max(amax, __float_as_uint(ma));
     O = fmaxf(O, wave_max_f(qm));
     nf.nan += nnan;
     nf.pinf += npinf;
     nf.ninf += nninf;
+}
+
+// Raises the work-group's max-rel value of one candidate (rare; O >= 0, so
+// the binary32 bits order like the values).
+__device__ __forceinline__ void publish_rel(uint32_t* s_rel, float O, int lane) {
+    if (lane == 0) atomicMax(s_rel, __float_as_uint(O));
+}
+
+// 2|x| - 2 on the bits of x: zeros map to the top of the unsigned range, so
+// an unsigned minimum over it picks the smallest nonzero magnitude.  (An
+// opaque instruction, so the compiler keeps it on the widened bits.)
+__device__ __forceinline__ uint32_t nz_key(float x) {
+    uint32_t u;
+    asm("v_lshl_add_u32 %0, %1, 1, -2" : "=v"(u) : "v"(__float_as_uint(x)));
+    return u;
 }
 
 // Per-wave results, combined across the work-group's waves in LDS.
@@ -259,8 +292,9 @@ struct WaveOut {
     double ssd;
 };
 
-// Minimum waves per SIMD the register allocator must allow.
-constexpr int min_waves(int dt, int kg) { return kg <= 8 ? 4 : 2; }
+// Minimum waves per SIMD the register allocator must allow: 4 (at most 128
+// VGPRs) where the kernel fits without spilling, else 2.
+constexpr int min_waves(int dt, int kg) { return kg <= 4 || (kg == 8 && dt != DT_F32) ? 4 : 2; }
 
 template <int DT, int KG>
 __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
@@ -269,6 +303,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     __shared__ WaveOut s_out[kWaves][KG];
     __shared__ double s_ssr[kWaves];
     __shared__ NonFinite s_nf[kWaves][KG];
+    __shared__ uint32_t s_rel[KG];  // work-group max-rel values (binary32 bits)
     __shared__ uint32_t s_is_last;
 
     const int lane = threadIdx.x & 63;
@@ -291,18 +326,20 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     const gbytes ref = uniform_ptr(p.ref);
 
     uint32_t mism[KG];  // wave-uniform mismatch counts
-    float amax[KG];     // lane max abs error
+    uint32_t amax[KG];  // lane max abs error (binary32 bits, non-negative)
     float orel[KG];     // wave-uniform max rel error
     uint32_t bitdiff = 0u;  // bit j: candidate j differs somewhere in this wave's range
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
         mism[j] = 0u;
-        amax[j] = 0.f;
+        amax[j] = 0u;
         orel[j] = 0.f;
         s_ssd[j][threadIdx.x] = 0.0;
     }
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
+    if (threadIdx.x < KG) s_rel[threadIdx.x] = 0u;
     double ssr = 0.0;
+    __syncthreads();
 
     const uint32_t off = 16u * (uint32_t)lane;
     const uint64_t n_chunks = p.numel / kChunk;
@@ -314,10 +351,14 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         // emits scalar-base loads instead of 64-bit vector address adds.
         uint32_t o = off;
         asm volatile("" : "+v"(o));
-        const Raw<DT> rraw = load_chunk<DT, false>(ref + cb, o);
+        const Raw<DT> rraw = load_chunk<DT, false>(uniform_ptr(ref + cb), o);
         Raw<DT> craw[KG];
 #pragma unroll
-        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(cand[j] + cb, o);
+        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(uniform_ptr(cand[j] + cb), o);
+        // the work-group's shared max-rel values
+#pragma unroll
+        for (int j = 0; j < KG; ++j)
+            orel[j] = fmaxf(orel[j], __uint_as_float(__builtin_amdgcn_readfirstlane(s_rel[j])));
 
         // Reference side, once per element for all KG candidates.
         float r[kE], tol[kE];
@@ -328,15 +369,14 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             r[i] = elem<DT>(rraw, i);
             tol[i] = __fadd_rn(atol, __fmul_rn(rtol, fabsf(r[i])));
             rr = fmaf(r[i], r[i], rr);
-            // 2|r| - 2 in the bit domain: zeros map to the top, so the
-            // minimum picks the smallest nonzero |r|
-            um = min(um, (__float_as_uint(r[i]) << 1) - 2u);
+            um = min(um, nz_key(r[i]));
         }
         const float amin_nz = um >= 0xFFFFFFFEu ? __builtin_inff() : __uint_as_float((um + 2u) >> 1);
         // Reference squares: eight binary32 terms, exact in binary64 where
         // the binary32 sum could lose precision (tiny or non-finite).
         double rrd = (double)rr;
-        const bool rbad = !(rr >= 0x1p-100f && rr < __builtin_inff());
+        // not in [2^-100, inf), NaN included, as one unsigned compare
+        const bool rbad = __float_as_uint(rr) - 0x0D800000u >= 0x7F800000u - 0x0D800000u;
         if (ballot(rbad)) {
             if (rbad) {
                 double t = 0.0;
@@ -377,12 +417,14 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             }
             if (ballot(!(acc < __builtin_inff()))) {
                 // NaN, infinity or a squared difference beyond binary32
+                const float before = orel[j];
                 exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
                                 amax[j], orel[j], s_nf[wave][j]);
+                if (orel[j] > before) publish_rel(&s_rel[j], orel[j], lane);
                 continue;
             }
             mism[j] += (uint32_t)kChunk - nmatch;
-            amax[j] = fmaxf(amax[j], tmax);
+            amax[j] = max(amax[j], __float_as_uint(tmax));
             // lanes whose differences are all tiny but not all zero: binary32
             // squares would underflow, so square in binary64
             const bool tiny = (__float_as_uint(tmax) - 1u) < (__float_as_uint(kTiny) - 1u);
@@ -396,11 +438,23 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
                 }
             }
             atomicAdd(&s_ssd[j][threadIdx.x], add);
-            const bool rel = ymax > 0.f || (O > 0.f && O * amin_nz < 0x1p-124f);
+            // the underflow guard as a residual too: 2^-124 - O amin > 0
+            // (never while O = 0, where y = d exactly, or for integer O)
+            const bool guard = O > 0.f && floorf(O) != O;
+            const float hz = fmaf(-O, amin_nz, guard ? 0x1p-124f : -__builtin_inff());
+            const bool rel = fmaxf(ymax, hz) > 0.f;
             if (ballot(rel)) {
                 float qm = 0.f;
-                if (rel) qm = rel_candidates(s, r, O);
-                orel[j] = fmaxf(O, wave_max_f(qm));
+                if (ballot(hz > 0.f)) {
+                    if (rel) qm = rel_quotients<true>(s, r, O);
+                } else {
+                    if (rel) qm = rel_quotients<false>(s, r, O);
+                }
+                const float q = wave_max_f(qm);
+                if (q > orel[j]) {
+                    orel[j] = q;
+                    publish_rel(&s_rel[j], q, lane);
+                }
             }
         }
     }
@@ -443,14 +497,14 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     for (int j = 0; j < KG; ++j) {
         if (j >= kg) continue;
         const double sd = wave_sum_f64(s_ssd[j][threadIdx.x]);
-        const float am = wave_max_f(amax[j]);
+        const uint32_t am = wave_max_u32(amax[j]);
         if (lane == 0) {
             WaveOut& o = s_out[wave][j];
             o.u[PF_MISM] = mism[j];
             o.u[PF_NAN] = s_nf[wave][j].nan;
             o.u[PF_PINF] = s_nf[wave][j].pinf;
             o.u[PF_NINF] = s_nf[wave][j].ninf;
-            o.u[PF_MAXABS] = __float_as_uint(am);
+            o.u[PF_MAXABS] = am;
             o.u[PF_MAXREL] = __float_as_uint(orel[j]);
             o.u[PF_BITDIFF] = (bitdiff >> j) & 1u;
             o.ssd = sd;
@@ -490,8 +544,12 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         st_coherent(&p.part_u32[PF_BITDIFF * plane + row], bd);
         st_coherent(&p.part_ssd[row], sd);
     }
-    if (threadIdx.x == 0)
-        st_coherent(&p.part_ssr[(size_t)g * C + stripe], (s_ssr[0] + s_ssr[1]) + (s_ssr[2] + s_ssr[3]));
+    if (threadIdx.x == 0) {
+        double sr = 0.0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) sr += s_ssr[w];
+        st_coherent(&p.part_ssr[(size_t)g * C + stripe], sr);
+    }
 
     // Two-level finish.  Level 1: the last work-group to arrive in each set
     // of 16 consecutive stripes (a "super-group") combines their partials,
