@@ -17,7 +17,16 @@ on the launch stream around each launch inside the timed region; the
 algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
 read of every candidate and the reference once), the CPU oracle timed on a
 bounded sample of the same workload, and the generator's throughput.
+
+roofline.traffic is the kernel's HBM traffic per launch from hardware
+counters (FETCH_SIZE and WRITE_SIZE, each scaled by the reading of the same
+counter for a plain device copy of known size, collected by two rocprofv3
+--pmc runs of `bench.py --copy-calibration`).  The collected numbers are
+kept in profiles/screen_traffic_<workload>.txt together with a digest of the
+kernel sources they were taken from; when the sources have changed since,
+traffic is null.
 """
+import hashlib
 import argparse
 import json
 import math
@@ -29,6 +38,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+METRIC = "candidate GB/s screened (K\u00d7N\u00d7dtype bytes/s) and % of MI355X HBM peak"
+KERNEL_SOURCES = ["paper_2608_02611_amd/csrc/kb_screen.hip", "paper_2608_02611_amd/csrc/kb_device.hpp",
+                  "paper_2608_02611_amd/csrc/kb_internal.hpp"]
 WORKLOADS = {
     "c1": "K=4 candidates, N=65,536 fp32, atol=rtol=1e-5",
     "c2": "K=16 candidates, 4096x4096 bf16 (GEMM-output shape), atol=rtol=1e-2",
@@ -40,6 +52,46 @@ WORKLOADS = {
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_digest():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic(config):
+    """HBM bytes per launch from the committed counter summary, or None when
+    there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "screen_traffic_%s.txt" % config)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith(" "):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_digest") != kernel_digest():
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(dev, nbytes=1 << 30, reps=3):
+    """A plain device copy of known size (nbytes read, nbytes written per
+    launch), run so that a counter pass can scale its readings."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def cpu_baseline(w, seconds):
@@ -99,6 +151,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gen", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the screening path is built and measured on a single "
@@ -162,7 +216,7 @@ def main():
     log("summary", summ)
 
     out = {
-        "metric": "candidate GB/s screened (K x N x dtype bytes/s) and % of MI355X HBM peak",
+        "metric": METRIC,
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -182,9 +236,12 @@ def main():
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "kernel_ms": round(kern_ms, 5),
-                     "algorithmic_bytes_per_launch": algorithmic},
+                     "traffic": counted_traffic(args.config), "kernel_ms": round(kern_ms, 5),
+                     "algorithmic_bytes_per_launch": algorithmic, "kernel_digest": kernel_digest()},
     }
+    if args.copy_calibration:
+        log("copy calibration")
+        copy_calibration(dev)
     if not args.no_gen:
         log("generator throughput")
         out["gen"] = gen_throughput(dev, kb, n, w.ref.dtype)
