@@ -204,7 +204,8 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     P.n_groups = n_acc > 0 ? (n_acc + P.kg - 1) / P.kg : 0;
     // Work-groups per candidate group (a multiple of 8, the XCD count):
     //  - at least enough that one work-group sees fewer than 2^31 elements
-    //    (32-bit partial counts), at most one per 4 chunks of 512 elements;
+    //    (32-bit partial counts), at most one per 8 chunks of 512 elements
+    //    (so small tensors get at most 16 stripes and a one-level finish);
     //  - for the launch: one round of the work-groups that are resident on the
     //    device at once (occupancy of the chosen kernel x CUs), spread over
     //    the candidate groups -- the grid is persistent, each wave strides
@@ -212,7 +213,7 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     //  - the workspace is laid out for the bound C_ws, independent of the
     //    device, and the launch never exceeds it.
     const uint64_t n_chunks = numel / 512;
-    const uint64_t c_work = align_up((n_chunks + 3) / 4, 8);
+    const uint64_t c_work = align_up((n_chunks + 7) / 8, 8);
     const uint64_t min_c = align_up(numel / (1ull << 31) + 1, 8);
     uint64_t c_ws = align_up((4096 + groups_max - 1) / groups_max, 8);
     if (c_ws > c_work) c_ws = c_work;

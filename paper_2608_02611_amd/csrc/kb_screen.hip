@@ -277,6 +277,12 @@ __device__ __forceinline__ void publish_rel(uint32_t* s_rel, float O, int lane) 
     if (lane == 0) atomicMax(s_rel, __float_as_uint(O));
 }
 
+// fp16 needs no guard at all: a nonzero binary32 difference of two fp16
+// values is at least 2^-24 and |r| is below 2^16, so O > 0 means O >= 2^-40,
+// and a nonzero |r| is at least 2^-24, so O |r| >= 2^-64 > 2^-124.
+template <int DT>
+constexpr bool kGuard = DT != DT_F16;
+
 // 2|x| - 2 on the bits of x: zeros map to the top of the unsigned range, so
 // an unsigned minimum over it picks the smallest nonzero magnitude.  (An
 // opaque instruction, so the compiler keeps it on the widened bits.)
@@ -284,6 +290,35 @@ __device__ __forceinline__ uint32_t nz_key(float x) {
     uint32_t u;
     asm("v_lshl_add_u32 %0, %1, 1, -2" : "=v"(u) : "v"(__float_as_uint(x)));
     return u;
+}
+
+// The record of one accepted candidate from its combined statistics.
+__device__ __forceinline__ void write_record(kb_stats* dst, uint64_t numel, uint64_t mi, uint64_t na,
+                                             uint64_t pi, uint64_t ni, uint32_t ma, uint32_t mr,
+                                             uint32_t bd, double sd, double sr) {
+    kb_stats st;
+    st.numel = numel;
+    st.mismatches = mi;
+    st.nan_count = na;
+    st.pos_inf_count = pi;
+    st.neg_inf_count = ni;
+    st.sum_sq_diff = sd;
+    st.sum_sq_ref = sr;
+    st.rel_l2 = sr > 0.0 ? sqrt(sd / sr) : (sd == 0.0 ? 0.0 : __builtin_inf());
+    st.max_abs_err = __uint_as_float(ma);
+    st.max_rel_err = __uint_as_float(mr);
+    st.bitwise_equal = bd == 0u ? 1 : 0;
+    st.status = KB_STATUS_OK;
+    *dst = st;
+}
+
+// Records of the rejected candidates (written by group 0's finisher).
+__device__ __forceinline__ void write_rejected(const ScreenParams& p, const CandEntry* table) {
+    for (int k = p.rej_start + (int)threadIdx.x; k < p.n_table; k += kThreads) {
+        kb_stats st = {};
+        st.status = table[k].status;
+        p.stats[table[k].index] = st;
+    }
 }
 
 // Per-wave results, combined across the work-group's waves in LDS.
@@ -305,6 +340,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     __shared__ NonFinite s_nf[kWaves][KG];
     __shared__ uint32_t s_rel[KG];  // work-group max-rel values (binary32 bits)
     __shared__ uint32_t s_is_last;
+    __shared__ double s_sr1;        // single-level finish: the group's sum of r^2
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -327,13 +363,13 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
 
     uint32_t mism[KG];  // wave-uniform mismatch counts
     uint32_t amax[KG];  // lane max abs error (binary32 bits, non-negative)
-    float orel[KG];     // wave-uniform max rel error
+    uint32_t orel[KG];  // wave-uniform max rel error O (binary32 bits, non-negative)
     uint32_t bitdiff = 0u;  // bit j: candidate j differs somewhere in this wave's range
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
         mism[j] = 0u;
         amax[j] = 0u;
-        orel[j] = 0.f;
+        orel[j] = 0u;
         s_ssd[j][threadIdx.x] = 0.0;
     }
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
@@ -358,18 +394,18 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         // the work-group's shared max-rel values
 #pragma unroll
         for (int j = 0; j < KG; ++j)
-            orel[j] = fmaxf(orel[j], __uint_as_float(__builtin_amdgcn_readfirstlane(s_rel[j])));
+            orel[j] = max(orel[j], __builtin_amdgcn_readfirstlane(s_rel[j]));
 
         // Reference side, once per element for all KG candidates.
         float r[kE], tol[kE];
         float rr = 0.f;
-        uint32_t um = 0xFFFFFFFFu;
+        uint32_t um = 0xFFFFFFFFu;  // smallest nonzero |r| (guard only)
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
             r[i] = elem<DT>(rraw, i);
             tol[i] = __fadd_rn(atol, __fmul_rn(rtol, fabsf(r[i])));
             rr = fmaf(r[i], r[i], rr);
-            um = min(um, nz_key(r[i]));
+            if constexpr (kGuard<DT>) um = min(um, nz_key(r[i]));
         }
         const float amin_nz = um >= 0xFFFFFFFEu ? __builtin_inff() : __uint_as_float((um + 2u) >> 1);
         // Reference squares: eight binary32 terms, exact in binary64 where
@@ -403,24 +439,30 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
                 if (ballot(x != 0u)) bitdiff |= 1u << j;
             }
             // fast path
-            const float O = orel[j];
-            float s[kE];
+            const float O = __uint_as_float(orel[j]);
+            float s[kE], y[kE];
             uint32_t nmatch = 0;
-            float tmax = 0.f, acc = 0.f, ymax = -__builtin_inff();
+            float tmax = 0.f, acc = 0.f;
 #pragma unroll
             for (int i = 0; i < kE; ++i) {
                 s[i] = elem<DT>(cr, i) - r[i];
                 nmatch += count_within(s[i], tol[i]);
                 tmax = fmaxf(tmax, fabsf(s[i]));
                 acc = fmaf(s[i], s[i], acc);
-                ymax = fmaxf(ymax, fmaf(-O, fabsf(r[i]), fabsf(s[i])));
+                y[i] = fmaf(-O, fabsf(r[i]), fabsf(s[i]));
             }
+            float ymax = y[0];
+#pragma unroll
+            for (int i = 1; i < kE; ++i) ymax = fmaxf(ymax, y[i]);
             if (ballot(!(acc < __builtin_inff()))) {
                 // NaN, infinity or a squared difference beyond binary32
-                const float before = orel[j];
+                float o = O;
                 exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
-                                amax[j], orel[j], s_nf[wave][j]);
-                if (orel[j] > before) publish_rel(&s_rel[j], orel[j], lane);
+                                amax[j], o, s_nf[wave][j]);
+                if (o > O) {
+                    orel[j] = __float_as_uint(o);
+                    publish_rel(&s_rel[j], o, lane);
+                }
                 continue;
             }
             mism[j] += (uint32_t)kChunk - nmatch;
@@ -440,19 +482,20 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             atomicAdd(&s_ssd[j][threadIdx.x], add);
             // the underflow guard as a residual too: 2^-124 - O amin > 0
             // (never while O = 0, where y = d exactly, or for integer O)
-            const bool guard = O > 0.f && floorf(O) != O;
-            const float hz = fmaf(-O, amin_nz, guard ? 0x1p-124f : -__builtin_inff());
+            float hz = -__builtin_inff();
+            if constexpr (kGuard<DT>)
+                hz = fmaf(-O, amin_nz, (O > 0.f && floorf(O) != O) ? 0x1p-124f : -__builtin_inff());
             const bool rel = fmaxf(ymax, hz) > 0.f;
             if (ballot(rel)) {
                 float qm = 0.f;
-                if (ballot(hz > 0.f)) {
+                if (kGuard<DT> && ballot(hz > 0.f)) {
                     if (rel) qm = rel_quotients<true>(s, r, O);
                 } else {
                     if (rel) qm = rel_quotients<false>(s, r, O);
                 }
                 const float q = wave_max_f(qm);
-                if (q > orel[j]) {
-                    orel[j] = q;
+                if (q > O) {
+                    orel[j] = __float_as_uint(q);
                     publish_rel(&s_rel[j], q, lane);
                 }
             }
@@ -486,8 +529,10 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
 #pragma unroll
                 for (int w = 0; w < Raw<DT>::kWords; ++w) cr.w[w] = 0u;
                 cr.w[0] = cb;
+                float o = __uint_as_float(orel[j]);
                 exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
-                                amax[j], orel[j], s_nf[wave][j]);
+                                amax[j], o, s_nf[wave][j]);
+                orel[j] = __float_as_uint(o);
             }
         }
     }
@@ -505,7 +550,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             o.u[PF_PINF] = s_nf[wave][j].pinf;
             o.u[PF_NINF] = s_nf[wave][j].ninf;
             o.u[PF_MAXABS] = am;
-            o.u[PF_MAXREL] = __float_as_uint(orel[j]);
+            o.u[PF_MAXREL] = orel[j];
             o.u[PF_BITDIFF] = (bitdiff >> j) & 1u;
             o.ssd = sd;
         }
@@ -556,8 +601,10 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     // one DPP row (16 lanes, one stripe each) per candidate.  Level 2: the
     // last super-group combiner of the candidate group combines the
     // super-group partials (each lane takes super-groups q = lane, lane + 16,
-    // ... in order) and writes the records.  Fixed orders throughout, so the
-    // binary64 sums are the same bits on every call.
+    // ... in order) and writes the records.  A group of at most 16 stripes
+    // has one super-group, whose combiner writes the records directly.
+    // Fixed orders throughout, so the binary64 sums are the same bits on
+    // every call.
     const int S = p.n_super;
     const int m = stripe >> 4;
     const int msize = min(16, C - 16 * m);
@@ -569,14 +616,15 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
 
     const int jj = threadIdx.x >> 4;
     const int sl = threadIdx.x & 15;
+    const CandEntry* table = p.table_inline ? tab.e : p.table;
     {
         const bool have = sl < msize;
         const int s = 16 * m + sl;
+        uint64_t mi = 0, na = 0, pi = 0, ni = 0;
+        uint32_t ma = 0, mr = 0, bd = 0;
+        double sd = 0.0;
         if (jj < kg) {
             const size_t idx = (size_t)(j0 + jj) * C + s;
-            uint64_t mi = 0, na = 0, pi = 0, ni = 0;
-            uint32_t ma = 0, mr = 0, bd = 0;
-            double sd = 0.0;
             if (have) {
                 mi = ld_coherent(&p.part_u32[PF_MISM * plane + idx]);
                 na = ld_coherent(&p.part_u32[PF_NAN * plane + idx]);
@@ -595,7 +643,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             mr = row_max_u32(mr);
             bd = row_or_u32(bd);
             sd = row_sum_f64(sd);
-            if (sl == 0) {
+            if (sl == 0 && S > 1) {
                 Part2* q = &p.part2[(size_t)(j0 + jj) * S + m];
                 st_coherent(&q->mism, mi);
                 st_coherent(&q->nan, na);
@@ -610,7 +658,21 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         if (jj == 0) {
             double sr = have ? ld_coherent(&p.part_ssr[(size_t)g * C + s]) : 0.0;
             sr = row_sum_f64(sr);
-            if (sl == 0) st_coherent(&p.part2_ssr[(size_t)g * S + m], sr);
+            if (sl == 0) {
+                if (S > 1) st_coherent(&p.part2_ssr[(size_t)g * S + m], sr);
+                else s_sr1 = sr;
+            }
+        }
+        if (S == 1) {
+            // Single-level finish: the group has at most 16 stripes, and this
+            // work-group has combined all of them.
+            __syncthreads();
+            if (jj < kg && sl == 0)
+                write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd, sd,
+                             s_sr1);
+            if (g == 0) write_rejected(p, table);
+            if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
+            return;
         }
     }
     if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
@@ -621,7 +683,6 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     __syncthreads();
     if (!s_is_last) return;
 
-    const CandEntry* table = p.table_inline ? tab.e : p.table;
     if (jj < kg) {
         uint64_t mi = 0, na = 0, pi = 0, ni = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
@@ -672,31 +733,11 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         bd = row_or_u32(bd);
         sd = row_sum_f64(sd);
         sr = row_sum_f64(sr);
-        if (sl == 0) {
-            kb_stats st;
-            st.numel = p.numel;
-            st.mismatches = mi;
-            st.nan_count = na;
-            st.pos_inf_count = pi;
-            st.neg_inf_count = ni;
-            st.sum_sq_diff = sd;
-            st.sum_sq_ref = sr;
-            st.rel_l2 = sr > 0.0 ? sqrt(sd / sr) : (sd == 0.0 ? 0.0 : __builtin_inf());
-            st.max_abs_err = __uint_as_float(ma);
-            st.max_rel_err = __uint_as_float(mr);
-            st.bitwise_equal = bd == 0u ? 1 : 0;
-            st.status = KB_STATUS_OK;
-            p.stats[table[j0 + jj].index] = st;
-        }
+        if (sl == 0)
+            write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd, sd, sr);
     }
     // Group 0's finisher also writes the rejected candidates' records.
-    if (g == 0) {
-        for (int k = p.rej_start + threadIdx.x; k < p.n_table; k += kThreads) {
-            kb_stats st = {};
-            st.status = table[k].status;
-            p.stats[table[k].index] = st;
-        }
-    }
+    if (g == 0) write_rejected(p, table);
     // Leave the ticket at zero for the next call on this workspace.
     if (threadIdx.x == 0) p.tickets2[g] = 0u;
 }
