@@ -94,6 +94,33 @@ def copy_calibration(dev, nbytes=1 << 30, reps=3):
     del src, dst
 
 
+def stream_context(dev, nbytes=1 << 30):
+    """What plain library kernels reach on this machine (context for the
+    roofline, not a bound of the screening kernel): a device-to-device copy
+    (nbytes read + nbytes written) and torch's sum over nbytes of fp32
+    (nbytes read)."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    x = src.view(torch.float32)
+    res = {}
+    for name, fn, moved in (("copy", lambda: dst.copy_(src), 2 * nbytes),
+                            ("sum_f32", lambda: x.sum(), nbytes)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(10):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / 10
+        res[name] = {"bytes": moved, "ms": round(ms, 4), "GB_per_s": round(moved / ms / 1e6, 1)}
+    del src, dst, x
+    return res
+
+
 def cpu_baseline(w, seconds):
     """The oracle, single-threaded, on the first S elements of every candidate,
     S chosen from a probe so that the sample takes about `seconds`."""
@@ -151,6 +178,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gen", action="store_true")
+    ap.add_argument("--no-stream-context", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
@@ -242,6 +270,9 @@ def main():
     if args.copy_calibration:
         log("copy calibration")
         copy_calibration(dev)
+    if not args.no_stream_context:
+        log("stream context")
+        out["stream_context"] = stream_context(dev)
     if not args.no_gen:
         log("generator throughput")
         out["gen"] = gen_throughput(dev, kb, n, w.ref.dtype)

@@ -85,6 +85,9 @@ def lib():
         L.kbo_screen.restype = ctypes.c_int
         L.kbo_match.argtypes = [f32, f32, f32, f32, u32]
         L.kbo_match.restype = ctypes.c_int
+        L.kbo_locate.argtypes = [ctypes.c_int, vp, vp, u64, f32, f32, u32, f32, f32,
+                                 ctypes.POINTER(ctypes.c_int64 * 3)]
+        L.kbo_locate.restype = ctypes.c_int
         for name in ("kbo_f32_to_f16_n", "kbo_f32_to_bf16_n", "kbo_f16_to_f32_n",
                      "kbo_bf16_to_f32_n"):
             getattr(L, name).argtypes = [vp, vp, u64]
@@ -194,6 +197,22 @@ def screen(ref, cand, dtype, atol, rtol, flags=0, chunk=None, threads=1):
     else:
         parts = [screen_partial(ref, cand, code, atol, rtol, flags, lo, hi) for lo, hi in bounds]
     return finalize(merge(parts))
+
+
+def locate(ref, cand, dtype, atol, rtol, max_abs, max_rel, flags=0):
+    """(first_mismatch, max_abs_index, max_rel_index) of one candidate, -1
+    where none; max_abs / max_rel are the candidate's maxima."""
+    code = _code(dtype)
+    ref = _storage(ref, code)
+    cand = _storage(cand, code)
+    if cand.size != ref.size:
+        raise ValueError("size mismatch")
+    out = (ctypes.c_int64 * 3)()
+    rc = lib().kbo_locate(code, ref.ctypes.data, cand.ctypes.data, ref.size, atol, rtol, flags,
+                          max_abs, max_rel, ctypes.byref(out))
+    if rc:
+        raise ValueError("bad dtype")
+    return tuple(out)
 
 
 def match(c, r, atol, rtol, flags=0):

@@ -340,6 +340,27 @@ int kbo_screen(int dtype, const void* ref, const void* cand, uint64_t n, float a
     return 0;
 }
 
+int kbo_locate(int dtype, const void* ref, const void* cand, uint64_t n, float atol, float rtol,
+               uint32_t flags, float max_abs, float max_rel, kbo_locate_t* out) {
+    if (dtype != KBO_F32 && dtype != KBO_F16 && dtype != KBO_BF16) return -1;
+    fpenv_guard env = fpenv_enter();
+    out->first_mismatch = out->max_abs_index = out->max_rel_index = -1;
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t cb, rb;
+        float c, r;
+        load_elem(dtype, cand, i, &cb, &c);
+        load_elem(dtype, ref, i, &rb, &r);
+        float d = fabsf(c - r);
+        float q = d / fabsf(r);
+        if (out->first_mismatch < 0 && !kbo_match(c, r, atol, rtol, flags))
+            out->first_mismatch = (int64_t)i;
+        if (out->max_abs_index < 0 && max_abs > 0.0f && d == max_abs) out->max_abs_index = (int64_t)i;
+        if (out->max_rel_index < 0 && max_rel > 0.0f && q == max_rel) out->max_rel_index = (int64_t)i;
+    }
+    fpenv_leave(env);
+    return 0;
+}
+
 /* ---------------------------------------------------------------------------
  * Bulk forms (loops over the single-element definitions above).
  * ------------------------------------------------------------------------- */

@@ -107,6 +107,20 @@ int kbo_screen(int dtype, const void* ref, const void* cand, uint64_t n, float a
 /* The single-element match predicate. */
 int kbo_match(float c, float r, float atol, float rtol, uint32_t flags);
 
+/* Positions in one candidate, for the diagnostics fed back about a failed
+ * candidate: the smallest element index i
+ *   first_mismatch: with kbo_match(c_i, r_i) false;
+ *   max_abs_index:  with |fl(c_i - r_i)| == max_abs (only if max_abs > 0);
+ *   max_rel_index:  with fl(|fl(c_i - r_i)| / |r_i|) == max_rel (only if
+ *                   max_rel > 0);
+ * each -1 when no element qualifies.  max_abs and max_rel are the
+ * candidate's maxima (kbo_stats). */
+typedef struct {
+    int64_t first_mismatch, max_abs_index, max_rel_index;
+} kbo_locate_t;
+int kbo_locate(int dtype, const void* ref, const void* cand, uint64_t n, float atol, float rtol,
+               uint32_t flags, float max_abs, float max_rel, kbo_locate_t* out);
+
 /* Elementwise bulk forms of the maps above, for exhaustive sweeps. */
 void kbo_f32_to_f16_n(const float* in, uint16_t* out, uint64_t n);
 void kbo_f32_to_bf16_n(const float* in, uint16_t* out, uint64_t n);
