@@ -153,6 +153,21 @@ typedef struct kb_summary {
     int32_t first_failed; /* lowest index rejected or failed, -1 if none */
 } kb_summary;
 
+/* Positions in one candidate (kb_screen_locate): element indices in the
+ * flattened tensor, -1 where no element qualifies.
+ *   first_mismatch  smallest i that does not match;
+ *   max_abs_index   smallest i with |fl(c_i - r_i)| == max_abs_err
+ *                   (-1 when max_abs_err is 0);
+ *   max_rel_index   smallest i with fl(|fl(c_i - r_i)| / |r_i|) == max_rel_err
+ *                   (-1 when max_rel_err is 0);
+ *   reserved        -1. */
+typedef struct kb_locate {
+    int64_t first_mismatch;
+    int64_t max_abs_index;
+    int64_t max_rel_index;
+    int64_t reserved;
+} kb_locate;
+
 /* Launch configuration of a kb_screen call (reported, for measurement). */
 typedef struct kb_launch {
     int32_t group_size;       /* candidates per work-group (KG) */
@@ -230,6 +245,25 @@ int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary);
  * Errors: KB_ERR_INVALID_ARG, KB_ERR_HIP. */
 int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats,
                     kb_summary* summary, hipStream_t stream);
+
+/* Positions of the first mismatch and of the maxima of each candidate: the
+ * element-level detail that the feedback about a failed candidate carries
+ * (Section 3.4: the check's log is passed on to the next generation step).
+ * A second, optional pass over the same buffers, stream-ordered after the
+ * kb_screen call whose records it uses.
+ *   ref, cands, n_cands, atol, rtol, flags   as given to kb_screen;
+ *   stats    the n_cands records kb_screen wrote for them (device memory or
+ *            mapped pinned host memory; read by the kernel);
+ *   d_loc    n_cands kb_locate written by the kernels (device memory or
+ *            mapped pinned host memory), 16-byte aligned.
+ * Rejected candidates get -1 everywhere.  A wave stops scanning for a
+ * position once it has found one (later elements have larger indices), so a
+ * candidate with an early mismatch costs little.  No workspace is needed.
+ * Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_DTYPE,
+ * KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+                     float rtol, uint32_t flags, const kb_stats* stats, kb_locate* d_loc,
+                     hipStream_t stream);
 
 /* ------------------------------------------------------------- generator -- */
 

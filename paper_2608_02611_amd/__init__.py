@@ -74,12 +74,21 @@ class KbLaunch(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class KbLocate(ctypes.Structure):
+    _fields_ = [("first_mismatch", ctypes.c_int64), ("max_abs_index", ctypes.c_int64),
+                ("max_rel_index", ctypes.c_int64), ("reserved", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
 assert ctypes.sizeof(KbStats) == 80
+assert ctypes.sizeof(KbLocate) == 32
 assert ctypes.sizeof(KbTensor) == 144
 
 EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
            "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
-           "kb_last_error", "kb_version")
+           "kb_screen_locate", "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -110,6 +119,9 @@ def lib():
         L.kb_screen_stats.argtypes = [vp, i32, ctypes.POINTER(KbStats), ctypes.POINTER(KbSummary),
                                       vp]
         L.kb_screen_stats.restype = i32
+        L.kb_screen_locate.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32,
+                                       f32, u32, vp, vp, vp]
+        L.kb_screen_locate.restype = i32
         L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
         L.kb_gen_inputs.restype = i32
         L.kb_last_error.argtypes = []
@@ -247,6 +259,31 @@ def kb_screen_stats(d_stats, n_cands, stream=None):
     _check(lib().kb_screen_stats(ctypes.c_void_p(d_stats.data_ptr()), n_cands, host,
                                  ctypes.byref(summ), _stream_handle(stream)))
     return [host[k].as_dict() for k in range(n_cands)], summ.as_dict()
+
+
+def kb_screen_locate(ref, cands, atol, rtol, d_stats, flags=0, stream=None):
+    """Positions of the first mismatch and of the maxima for each candidate
+    (list of dicts, -1 where none).  d_stats holds the records kb_screen
+    wrote for the same arguments on the same stream; synchronizes the
+    stream to read the result."""
+    torch = _torch()
+    r = describe(ref)
+    arr = (KbTensor * max(1, len(cands)))(*[describe(c) for c in cands])
+    out = torch.empty(max(1, len(cands)) * ctypes.sizeof(KbLocate), dtype=torch.uint8,
+                      device=ref.device)
+    _check(lib().kb_screen_locate(ctypes.byref(r), arr, len(cands), float(atol), float(rtol),
+                                  int(flags), ctypes.c_void_p(d_stats.data_ptr()),
+                                  ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)))
+    host = out.cpu()
+    locs = (KbLocate * max(1, len(cands))).from_buffer_copy(host.numpy().tobytes())
+    return [locs[k].as_dict() for k in range(len(cands))]
+
+
+def locate(ref, cands, atol, rtol, flags=0, stream=None):
+    """Screen, then locate: (records, positions)."""
+    d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)
+    recs, _ = kb_screen_stats(d_stats, len(cands), stream=stream)
+    return recs, kb_screen_locate(ref, cands, atol, rtol, d_stats, flags, stream=stream)
 
 
 def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):

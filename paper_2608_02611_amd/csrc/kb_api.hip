@@ -452,6 +452,61 @@ int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats, kb_
     return KB_OK;
 }
 
+int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+                     float rtol, uint32_t flags, const kb_stats* stats, kb_locate* d_loc,
+                     hipStream_t stream) {
+    clear_error();
+    if (ref == nullptr || cands == nullptr || stats == nullptr || d_loc == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: null ref, cands, stats or d_loc");
+    if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: n_cands = %d < 1", n_cands);
+    if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: atol and rtol must be finite and >= 0");
+    if (flags & ~(uint32_t)KB_EQUAL_NAN)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: unknown flags 0x%x", flags);
+    std::vector<int32_t> status((size_t)n_cands);
+    int rc = kb_policy_check(ref, cands, n_cands, status.data());
+    if (rc != KB_OK) return rc;
+    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "reference is not contiguous");
+    if (!aligned16(ref->data) || !aligned16(d_loc))
+        return fail(KB_ERR_ALIGNMENT, "kb_screen_locate: reference or d_loc not 16-byte aligned");
+    for (int k = 0; k < n_cands; ++k)
+        if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
+            return fail(KB_ERR_ALIGNMENT, "kb_screen_locate: candidate %d not 16-byte aligned", k);
+    const uint64_t numel = tensor_numel(*ref);
+    // every position starts as "none" (all ones, -1 as int64)
+    hipError_t e = launch_fill_u32(d_loc, (uint64_t)n_cands * sizeof(kb_locate) / 4, 0xFFFFFFFFu, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen_locate: fill");
+    if (numel == 0) return KB_OK;
+    LocateParams p{};
+    p.ref = ref->data;
+    p.numel = numel;
+    p.atol = atol;
+    p.rtol = rtol;
+    p.flags = flags;
+    p.stats = stats;
+    p.out = d_loc;
+    // Work-groups per candidate: about 2048 in flight per launch, a multiple
+    // of 8, at most one per 8 chunks (and at least one).
+    const uint64_t n_chunks = numel / 512;
+    LocTable tab;
+    int k = 0;
+    while (k < n_cands) {
+        int n = 0;
+        for (; k < n_cands && n < kLocateBatch; ++k)
+            if (status[k] == KB_STATUS_OK) tab.e[n++] = LocEntry{cands[k].data, k, 0};
+        if (n == 0) break;
+        uint64_t stripes = (2048 + n - 1) / n;
+        stripes = (stripes + 7) / 8 * 8;
+        const uint64_t cap = n_chunks / 8 > 8 ? n_chunks / 8 / 8 * 8 : 8;
+        if (stripes > cap) stripes = cap;
+        p.n = n;
+        p.stripes = (int)stripes;
+        e = launch_locate(ref->dtype, p, tab, stream);
+        if (e != hipSuccess) return fail_hip(e, "kb_screen_locate: kernel launch");
+    }
+    return KB_OK;
+}
+
 int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1, uint64_t seed,
                   uint32_t stream_id, uint32_t sub, uint64_t offset, hipStream_t stream) {
     clear_error();

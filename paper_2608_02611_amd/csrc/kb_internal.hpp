@@ -116,6 +116,32 @@ hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream);
 hipError_t launch_records_only(const CandEntry* table, const InlineTable& tab, int table_inline,
                                int n_table, uint64_t numel, kb_stats* stats, hipStream_t stream);
 
+// Position search (kb_screen_locate): up to kLocateBatch candidates per
+// launch, their table in the kernel arguments.
+constexpr int kLocateBatch = 128;
+struct LocEntry {
+    const void* data;
+    int32_t index;  // position in the caller's candidate array
+    int32_t pad;
+};
+struct LocTable {
+    LocEntry e[kLocateBatch];
+};
+struct LocateParams {
+    const void* ref;
+    uint64_t numel;
+    float atol;
+    float rtol;
+    uint32_t flags;
+    int n;        // candidates in this launch
+    int stripes;  // work-groups per candidate
+    const kb_stats* stats;
+    kb_locate* out;
+};
+hipError_t launch_locate(int dtype, const LocateParams& p, const LocTable& tab, hipStream_t stream);
+// Fill n_words 32-bit words with value.
+hipError_t launch_fill_u32(void* dst, uint64_t n_words, uint32_t value, hipStream_t stream);
+
 hipError_t launch_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
                       uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
                       hipStream_t stream);

@@ -1,0 +1,199 @@
+// kb_locate.hip -- positions of the first mismatch and of the maxima.
+//
+// The detail a failed candidate's feedback carries (the agent passes the log
+// of the failing check to the next generation step, Section 3.4 and the
+// prompt template of the appendix): per candidate, the smallest element
+// index that does not match, whose |c - r| equals the candidate's max abs
+// error, and whose d / |r| equals its max rel error.  The maxima come from
+// the records kb_screen wrote, so this is a second, optional pass over the
+// candidates one asks about.
+//
+// A wave scans its chunks in increasing index order and stops looking for a
+// position as soon as one of its lanes has found it: every later chunk of
+// the wave holds larger indices.  On a failing candidate the first mismatch
+// is usually in a wave's first chunk, so most of the pass is skipped.  The
+// per-lane first hits are reduced to a wave minimum (DPP) and merged into the
+// output with a 64-bit atomic minimum; "none" is all-ones, which reads as -1.
+#include "kb_device.hpp"
+#include "kb_internal.hpp"
+
+namespace kb {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kE = 8;
+constexpr int kChunk = 64 * kE;
+constexpr uint64_t kNone = ~0ull;
+
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) v4u32* gvec;
+
+template <int DT>
+__device__ __forceinline__ float widen_bits(uint32_t bits) {
+    if constexpr (DT == DT_F32) return __uint_as_float(bits);
+    else if constexpr (DT == DT_F16) return f16_bits_to_f32(bits);
+    else return bf16_bits_to_f32(bits);
+}
+
+// Storage bits of element i of a lane's chunk and its index within the chunk
+// (fp32: elements 4l..4l+3 and 256+4l..256+4l+3; 16-bit: 8l..8l+7; both in
+// increasing index order in i).
+template <int DT>
+struct LaneChunk {
+    uint32_t w[DT == DT_F32 ? 8 : 4];
+    __device__ __forceinline__ uint32_t bits(int i) const {
+        if constexpr (DT == DT_F32) return w[i];
+        else return (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+    }
+    static __device__ __forceinline__ uint32_t offset(int lane, int i) {
+        if constexpr (DT == DT_F32) return i < 4 ? 4 * lane + i : 256 + 4 * lane + (i - 4);
+        else return 8 * lane + i;
+    }
+};
+
+template <int DT>
+__device__ __forceinline__ LaneChunk<DT> load_lane(const void* base, uint64_t chunk, int lane) {
+    LaneChunk<DT> x;
+    if constexpr (DT == DT_F32) {
+        const gvec p = (gvec)base + chunk * 128;
+        const v4u32 a = __builtin_nontemporal_load(p + lane);
+        const v4u32 b = __builtin_nontemporal_load(p + 64 + lane);
+        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+        x.w[4] = b.x; x.w[5] = b.y; x.w[6] = b.z; x.w[7] = b.w;
+    } else {
+        const gvec p = (gvec)base + chunk * 64;
+        const v4u32 a = __builtin_nontemporal_load(p + lane);
+        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+    v = min(v, dpp_u64<DPP_QUAD_XOR1>(v));
+    v = min(v, dpp_u64<DPP_QUAD_XOR2>(v));
+    v = min(v, dpp_u64<DPP_ROW_HALF_MIRROR>(v));
+    v = min(v, dpp_u64<DPP_ROW_MIRROR>(v));
+    return min(min(readlane_u64(v, 0), readlane_u64(v, 16)), min(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// The three predicates of one element (the definitions of the screening
+// statistics, element by element).
+struct Hit {
+    bool mism, abs, rel;
+};
+__device__ __forceinline__ Hit classify(float c, float r, float atol, float rtol, bool equal_nan,
+                                        float max_abs, float max_rel, bool want_abs, bool want_rel) {
+    const float d = fabsf(c - r);
+    const float a = fabsf(r);
+    const float tol = __builtin_isfinite(r) ? __fadd_rn(atol, __fmul_rn(rtol, a)) : -1.0f;
+    const bool match = (c == r) || (d <= tol) || (equal_nan && __builtin_isnan(c) && __builtin_isnan(r));
+    Hit h;
+    h.mism = !match;
+    h.abs = want_abs && d == max_abs;
+    h.rel = false;
+    if (want_rel) {
+        // fl(d / a) == max_rel needs d / a >= max_rel (1 - 2^-24), hence
+        // d - T a > 0 for T = fl(max_rel (1 - 2^-20)): a cheap filter in
+        // front of the IEEE division (the fma keeps the sign; an underflow to
+        // zero passes).  For max_rel = +inf: a zero reference, an infinite
+        // difference or a quotient beyond 2^100; for a tiny max_rel, whose
+        // product T might round back up to it, no filter.
+        bool cand;
+        if (__builtin_isinf(max_rel)) cand = a == 0.f || d == __builtin_inff() || d >= a * 0x1p100f;
+        else if (max_rel < 0x1p-100f) cand = true;
+        else cand = fmaf(-(max_rel * 0x1.ffffep-1f), a, d) >= 0.f;
+        if (cand) h.rel = (d / a) == max_rel;
+    }
+    return h;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTable tab) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int k = blockIdx.x % p.n;
+    const int stripe = blockIdx.x / p.n;
+    const void* cand = tab.e[k].data;
+    const int index = tab.e[k].index;
+    const float max_abs = p.stats[index].max_abs_err;
+    const float max_rel = p.stats[index].max_rel_err;
+    const bool want_abs = max_abs > 0.f;  // false for 0 and NaN
+    const bool want_rel = max_rel > 0.f;
+    const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
+
+    uint64_t f_mism = kNone, f_abs = kNone, f_rel = kNone;
+    bool need_mism = true, need_abs = want_abs, need_rel = want_rel;
+    const uint64_t n_chunks = p.numel / kChunk;
+    const uint64_t wstride = (uint64_t)p.stripes * kWaves;
+    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave;
+         chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += wstride) {
+        const LaneChunk<DT> rc = load_lane<DT>(p.ref, chunk, lane);
+        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, lane);
+        const uint64_t base = chunk * kChunk;
+#pragma unroll
+        for (int i = 0; i < kE; ++i) {
+            const Hit h = classify(widen_bits<DT>(cc.bits(i)), widen_bits<DT>(rc.bits(i)), p.atol, p.rtol,
+                                   equal_nan, max_abs, max_rel, need_abs, need_rel);
+            const uint64_t idx = base + LaneChunk<DT>::offset(lane, i);
+            if (need_mism && h.mism && f_mism == kNone) f_mism = idx;
+            if (h.abs && f_abs == kNone) f_abs = idx;
+            if (h.rel && f_rel == kNone) f_rel = idx;
+        }
+        // a position found anywhere in this chunk is below everything later
+        if (need_mism && ballot(f_mism != kNone)) need_mism = false;
+        if (need_abs && ballot(f_abs != kNone)) need_abs = false;
+        if (need_rel && ballot(f_rel != kNone)) need_rel = false;
+    }
+    // Ragged tail (numel mod 512 elements): stripe 0, one element per thread.
+    if (stripe == 0) {
+        for (uint64_t e = n_chunks * kChunk + threadIdx.x; e < p.numel; e += kThreads) {
+            const uint32_t rb = DT == DT_F32 ? ((const uint32_t*)p.ref)[e] : ((const uint16_t*)p.ref)[e];
+            const uint32_t cb = DT == DT_F32 ? ((const uint32_t*)cand)[e] : ((const uint16_t*)cand)[e];
+            const Hit h = classify(widen_bits<DT>(cb), widen_bits<DT>(rb), p.atol, p.rtol, equal_nan,
+                                   max_abs, max_rel, want_abs, want_rel);
+            if (h.mism && f_mism == kNone) f_mism = e;
+            if (h.abs && f_abs == kNone) f_abs = e;
+            if (h.rel && f_rel == kNone) f_rel = e;
+        }
+    }
+    f_mism = wave_min_u64(f_mism);
+    f_abs = wave_min_u64(f_abs);
+    f_rel = wave_min_u64(f_rel);
+    if (lane == 0) {
+        unsigned long long* o = (unsigned long long*)&p.out[index];
+        if (f_mism != kNone) atomicMin(&o[0], (unsigned long long)f_mism);
+        if (f_abs != kNone) atomicMin(&o[1], (unsigned long long)f_abs);
+        if (f_rel != kNone) atomicMin(&o[2], (unsigned long long)f_rel);
+    }
+}
+
+__global__ void fill_kernel(uint32_t* dst, uint64_t n, uint32_t value) {
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        dst[i] = value;
+}
+
+}  // namespace
+
+hipError_t launch_locate(int dtype, const LocateParams& p, const LocTable& tab, hipStream_t stream) {
+    const unsigned grid = (unsigned)p.n * (unsigned)p.stripes;
+    switch (dtype) {
+        case DT_F32: hipLaunchKernelGGL(locate_kernel<DT_F32>, dim3(grid), dim3(kThreads), 0, stream, p, tab); break;
+        case DT_F16: hipLaunchKernelGGL(locate_kernel<DT_F16>, dim3(grid), dim3(kThreads), 0, stream, p, tab); break;
+        default: hipLaunchKernelGGL(locate_kernel<DT_BF16>, dim3(grid), dim3(kThreads), 0, stream, p, tab); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(void* dst, uint64_t n_words, uint32_t value, hipStream_t stream) {
+    if (n_words == 0) return hipSuccess;
+    const uint64_t want = (n_words + 255) / 256;
+    const unsigned grid = (unsigned)(want < 1024 ? want : 1024);
+    hipLaunchKernelGGL(fill_kernel, dim3(grid), dim3(256), 0, stream, (uint32_t*)dst, n_words, value);
+    return hipGetLastError();
+}
+
+}  // namespace kb

@@ -197,3 +197,18 @@ def test_workspace_init_argument_errors(L):
     assert f(0x1000, 0, None) == kb.KB_ERR_WORKSPACE
     assert f(0x1008, 256, None) == kb.KB_ERR_ALIGNMENT
     assert f(0x1000, 250, None) == kb.KB_ERR_ALIGNMENT
+
+
+def test_locate_argument_errors(L):
+    ref = desc(0x10000, kb.KB_F32, (64,))
+    arr = (kb.KbTensor * 1)(desc(0x20000, kb.KB_F32, (64,)))
+    f = kb.lib().kb_screen_locate
+    assert f(None, arr, 1, 1e-5, 1e-5, 0, 0x3000, 0x4000, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 0, 1e-5, 1e-5, 0, 0x3000, 0x4000, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 1, -1.0, 1e-5, 0, 0x3000, 0x4000, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 1, 1e-5, 1e-5, 4, 0x3000, 0x4000, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 1, 1e-5, 1e-5, 0, None, 0x4000, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 1, 1e-5, 1e-5, 0, 0x3000, None, None) == kb.KB_ERR_INVALID_ARG
+    assert f(ctypes.byref(ref), arr, 1, 1e-5, 1e-5, 0, 0x3000, 0x4008, None) == kb.KB_ERR_ALIGNMENT
+    bad = desc(0x10000, kb.KB_U32, (64,))
+    assert f(ctypes.byref(bad), arr, 1, 1e-5, 1e-5, 0, 0x3000, 0x4000, None) == kb.KB_ERR_DTYPE

@@ -1,0 +1,108 @@
+"""Parity of the position search (kb_screen_locate) with the oracle (GPU).
+
+The library screens, then locates, on the device; the oracle's kbo_locate
+runs on host copies of the same bytes with the oracle's own maxima (equal to
+the library's by the screening parity).  Every position must be equal."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_02611_amd as kb
+import synth
+from tests.helpers import dtype_name, ensure_built, storage
+
+pytestmark = pytest.mark.gpu
+
+TORCH_DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+CONV = {"f32": lambda x: x.astype(np.float32), "f16": oracle.f32_to_f16_n, "bf16": oracle.f32_to_bf16_n}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    ensure_built()
+    return torch.device("cuda:0")
+
+
+def to_dev(arr, dt, dev):
+    if dt == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(dev)
+    bits = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint16).view(np.int16)).to(dev)
+    return bits.view(TORCH_DT[dt])
+
+
+def oracle_positions(ref, cands, atol, rtol, flags=0):
+    dt = dtype_name(ref)
+    r = storage(ref)
+    out = []
+    for c in cands:
+        cs = storage(c)
+        s = oracle.screen(r, cs, dt, atol, rtol, flags)
+        fm, ai, ri = oracle.locate(r, cs, dt, atol, rtol, s["max_abs_err"], s["max_rel_err"], flags)
+        out.append({"first_mismatch": fm, "max_abs_index": ai, "max_rel_index": ri})
+    return out
+
+
+def check(ref, cands, atol, rtol, flags=0, label=""):
+    recs, locs = kb.locate(ref, cands, atol, rtol, flags)
+    want = oracle_positions(ref, cands, atol, rtol, flags)
+    for k, (g, w) in enumerate(zip(locs, want)):
+        assert g == w, (label, k, g, w)
+    return locs
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("n", [1, 511, 512, 4097, 70001, 1 << 20])
+def test_planted_positions(dev, dt, n):
+    rng = np.random.default_rng(n)
+    r32 = rng.uniform(1.0, 2.0, n).astype(np.float32)
+    cands = [r32.copy() for _ in range(5)]
+    # 1: one mismatch late (in the ragged tail when there is one)
+    cands[1][n - 1] = 7.0
+    # 2: mismatches at several places, the lowest one chosen
+    for p in sorted({n // 2, n // 3, (2 * n) // 3}):
+        cands[2][p] = 5.0
+    # 3: tie of the largest difference and ratio
+    for p in sorted({n - 1, n // 5, n // 7}):
+        cands[3][p] = r32[p] + 0.5
+    # 4: NaN first, then the maximum
+    cands[4][n // 9] = np.nan
+    cands[4][n - 1 - n // 11] = r32[n - 1 - n // 11] + 0.25
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cd = [to_dev(CONV[dt](c), dt, dev) for c in cands]
+    check(ref, cd, 1e-3, 1e-3, 0, "%s n=%d" % (dt, n))
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_random_ragged(dev, dt):
+    rng = np.random.default_rng(17)
+    n = 3 * 512 * 37 + 211
+    r32 = rng.standard_normal(n).astype(np.float32)
+    r32[rng.integers(0, n, 40)] = 0.0
+    cands = []
+    for k in range(9):
+        c = (r32 + rng.standard_normal(n).astype(np.float32) * (10.0 ** (-5 + k / 2))).astype(np.float32)
+        if k % 3 == 0:
+            c[rng.integers(0, n, 3)] = np.inf
+        cands.append(c)
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cd = [to_dev(CONV[dt](c), dt, dev) for c in cands]
+    check(ref, cd, 1e-3, 1e-3, 0, dt)
+    check(ref, cd, 1e-3, 1e-3, kb.KB_EQUAL_NAN, dt + " equal_nan")
+
+
+@pytest.mark.parametrize("name,scale,K", [("c1", 1.0, 4), ("c2", 1 / 64, 16), ("c3", 1 / 8, 64),
+                                          ("c4", 1 / 256, 16), ("c5", 1 / 512, 8)])
+def test_workloads(dev, name, scale, K):
+    w = synth.build(name, dev, seed=0, scale=scale, K=K)
+    check(w.ref, w.cands, w.atol, w.rtol, 0, name)
+
+
+def test_rejected_and_identical(dev):
+    r = torch.randn(5000, device=dev)
+    cands = [r.clone(), None, r.to(torch.float16), r.clone()]
+    cands[3][4321] = float("nan")
+    recs, locs = kb.locate(r, cands, 1e-5, 1e-5)
+    assert locs[0] == {"first_mismatch": -1, "max_abs_index": -1, "max_rel_index": -1}
+    assert locs[1] == locs[0] and locs[2] == locs[0]
+    assert locs[3] == {"first_mismatch": 4321, "max_abs_index": -1, "max_rel_index": -1}
