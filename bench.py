@@ -270,6 +270,19 @@ def main():
     if args.copy_calibration:
         log("copy calibration")
         copy_calibration(dev)
+    # the optional position pass (kb_screen_locate) over all candidates,
+    # after the synchronous screen above (its records stay on the device)
+    loc_ms = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        locs = kb.kb_screen_locate(w.ref, w.cands, w.atol, w.rtol, sync.d_stats)
+        e1.record()
+        torch.cuda.synchronize()
+        loc_ms.append(e0.elapsed_time(e1))
+    out["locate"] = {"ms": round(sorted(loc_ms)[len(loc_ms) // 2], 4),
+                     "failed_candidates_first_mismatch": [l["first_mismatch"] for l in locs
+                                                          if l["first_mismatch"] >= 0][:4]}
     if not args.no_stream_context:
         log("stream context")
         out["stream_context"] = stream_context(dev)
