@@ -16,7 +16,11 @@ The JSON line also carries the roofline of the screening kernel (HIP events
 on the launch stream around each launch inside the timed region; the
 algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
 read of every candidate and the reference once), the CPU oracle timed on a
-bounded sample of the same workload, and the generator's throughput.
+bounded sample of the same workload, the generator's throughput, and two
+optional passes over the same candidates: the position search
+(kb_screen_locate) and the fail-fast screen (KB_FAIL_FAST), whose kernel
+time and share of candidate elements read are reported beside the full
+screen's.
 
 roofline.traffic is the kernel's HBM traffic per launch from hardware
 counters (FETCH_SIZE and WRITE_SIZE, each scaled by the reading of the same
@@ -283,6 +287,30 @@ def main():
     out["locate"] = {"ms": round(sorted(loc_ms)[len(loc_ms) // 2], 4),
                      "failed_candidates_first_mismatch": [l["first_mismatch"] for l in locs
                                                           if l["first_mismatch"] >= 0][:4]}
+    # the fail-fast mode (KB_FAIL_FAST) on the same candidates: the verdicts
+    # must be the ones of the full screen; reported are its kernel time and
+    # the share of candidate elements it read
+    log("fail-fast")
+    ff = kb.Screener(w.ref, w.cands, w.atol, w.rtol, flags=kb.KB_FAIL_FAST)
+    ff.launch()
+    ff.read()
+    ff_ms = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ff.launch()
+        e1.record()
+        torch.cuda.synchronize()
+        ff_ms.append(e0.elapsed_time(e1))
+    ff.read()
+    frec, full = ff.records(), sync.records()
+    assert [r["mismatches"] > 0 for r in frec] == [r["mismatches"] > 0 for r in full], \
+        "fail-fast verdicts differ from the full screen"
+    ffm = sorted(ff_ms)[len(ff_ms) // 2]
+    out["fail_fast"] = {"kernel_ms": round(ffm, 5),
+                        "vs_full_kernel": round(kern_ms / ffm, 2),
+                        "candidate_elements_read_frac": round(sum(r["numel"] for r in frec) / (K * n), 4),
+                        "n_failed": sum(r["mismatches"] > 0 for r in frec)}
     if not args.no_stream_context:
         log("stream context")
         out["stream_context"] = stream_context(dev)

@@ -86,7 +86,8 @@ enum {
 
 /* kb_screen flags. */
 enum {
-    KB_EQUAL_NAN = 1u << 0 /* a NaN candidate element matches a NaN reference element */
+    KB_EQUAL_NAN = 1u << 0, /* a NaN candidate element matches a NaN reference element */
+    KB_FAIL_FAST = 1u << 1  /* stop reading a candidate once a mismatch is seen (kb_screen) */
 };
 
 /* A tensor view.  data: device pointer to element 0 (may be NULL for a
@@ -127,7 +128,15 @@ typedef struct kb_tensor {
  * Counts, flags and maxima are exact; the two sums are binary64 sums in a
  * fixed order (deterministic from call to call, within 1e-6 relative of the
  * exact sums).  A rejected candidate has status = KB_REJECT_* and every
- * other field zero. */
+ * other field zero.
+ *
+ * With KB_FAIL_FAST a candidate that has a mismatch may be stopped early:
+ * its record then describes only the elements that were compared, numel
+ * being their count (<= the reference numel) and every other field the
+ * definition above restricted to them (sum_sq_ref included); mismatches is
+ * still >= 1, so the verdict is the same.  Which elements were compared
+ * depends on timing.  A candidate without mismatch is always read in full
+ * and its record is bit-identical to the one written without the flag. */
 typedef struct kb_stats {
     uint64_t numel;
     uint64_t mismatches;
@@ -218,7 +227,15 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
  *   cands        host array of n_cands descriptors (n_cands >= 1); each is
  *                gated by kb_policy_check and, if accepted, read once;
  *   atol, rtol   finite, >= 0 (binary32);
- *   flags        0 or KB_EQUAL_NAN;
+ *   flags        0 or a combination of KB_EQUAL_NAN and KB_FAIL_FAST.
+ *                KB_FAIL_FAST is the early-reject mode of the screening
+ *                step (Section 3.3, Observation 2: a candidate with wrong
+ *                output is to be turned away in milliseconds): every wave polls a per-candidate "failed"
+ *                word in the workspace with each chunk it reads, a wave
+ *                that finds a mismatch sets it, and a candidate known to
+ *                have failed is no longer read (see kb_stats for what its
+ *                record then holds); work-groups whose candidates have all
+ *                failed stop reading the reference too;
  *   workspace    device scratch of workspace_bytes >=
  *                kb_screen_workspace_bytes(n_cands, numel, dtype),
  *                initialised by kb_screen_workspace_init (see there); one
@@ -256,6 +273,9 @@ int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats,
  *            mapped pinned host memory; read by the kernel);
  *   d_loc    n_cands kb_locate written by the kernels (device memory or
  *            mapped pinned host memory), 16-byte aligned.
+ * KB_FAIL_FAST in flags is accepted and has no effect here; where a record
+ * was written under it for a stopped candidate, the max indices refer to the
+ * maxima that record holds.
  * Rejected candidates get -1 everywhere.  A wave stops scanning for a
  * position once it has found one (later elements have larger indices), so a
  * candidate with an early mismatch costs little.  No workspace is needed.

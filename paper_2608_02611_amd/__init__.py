@@ -24,6 +24,7 @@ KB_OK = 0
 KB_ERR_INVALID_ARG, KB_ERR_DTYPE, KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT, KB_ERR_HIP = -1, -2, -3, -4, -5
 KB_STATUS_OK, KB_REJECT_NULL, KB_REJECT_DTYPE, KB_REJECT_SHAPE, KB_REJECT_LAYOUT = 0, 1, 2, 3, 4
 KB_EQUAL_NAN = 1
+KB_FAIL_FAST = 2
 KB_MAX_DIMS = 8
 
 ERROR_NAMES = {KB_ERR_INVALID_ARG: "KB_ERR_INVALID_ARG", KB_ERR_DTYPE: "KB_ERR_DTYPE",

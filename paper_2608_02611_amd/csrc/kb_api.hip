@@ -81,7 +81,7 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Launch tuning override for measurement sweeps: KB_SCREEN_TUNE="kg=16,blocks=1024"
 // caps the candidates per group (1, 2, 4, 8 or 16) and sets the target total
 // number of work-groups.  Unset, the built-in choice applies.
-void tuning_override(int* kg_cap, int* blocks_total) {
+void tuning_override(int* kg_cap, int* blocks_total, int* ff_round = nullptr) {
     const char* s = std::getenv("KB_SCREEN_TUNE");
     if (s == nullptr) return;
     int v;
@@ -90,6 +90,8 @@ void tuning_override(int* kg_cap, int* blocks_total) {
         *kg_cap = v;
     const char* b = std::strstr(s, "blocks=");  // 0 or absent: occupancy-based
     if (b && std::sscanf(b + 7, "%d", &v) == 1 && v >= 8 && v <= (1 << 20)) *blocks_total = v;
+    const char* f = std::strstr(s, "ffround=");  // fail-fast groups per round
+    if (ff_round && f && std::sscanf(f + 8, "%d", &v) == 1 && v >= 1) *ff_round = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -168,12 +170,12 @@ Staging& staging() {
 // Work-groups of the screening kernel for (dtype, kg) resident on the
 // current device at once; 0 if the device cannot be queried (then the plan
 // falls back to a fixed total).
-int resident_blocks(int dtype, int kg) {
+int resident_blocks(int dtype, int kg, bool fail_fast = false) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
-    return cus * screen_blocks_per_cu(dtype, kg);
+    return cus * screen_blocks_per_cu(dtype, kg, fail_fast);
 }
 int plan_group_size(int n_cands, int dtype) {
     // Measured on the five screening workloads: groups of 4 for fp32 and
@@ -187,7 +189,7 @@ int plan_group_size(int n_cands, int dtype) {
 }
 
 bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_blocks,
-               ScreenPlan* plan) {
+               bool serial_groups, ScreenPlan* plan) {
     if (n_cands < 1 || n_acc < 0 || n_acc > n_cands || !is_float_dtype(dtype)) return false;
     ScreenPlan P{};
     P.dtype = dtype;
@@ -202,30 +204,48 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     P.kg = plan_group_size(n_cands, dtype);
     const int groups_max = (n_cands + P.kg - 1) / P.kg;
     P.n_groups = n_acc > 0 ? (n_acc + P.kg - 1) / P.kg : 0;
-    // Work-groups per candidate group (a multiple of 8, the XCD count):
+    // Work-groups per candidate group (stripes; a multiple of 8, the XCD count):
     //  - at least enough that one work-group sees fewer than 2^31 elements
     //    (32-bit partial counts), at most one per 8 chunks of 512 elements
     //    (so small tensors get at most 16 stripes and a one-level finish);
-    //  - for the launch: one round of the work-groups that are resident on the
+    //  - plain launch: one round of the work-groups that are resident on the
     //    device at once (occupancy of the chosen kernel x CUs), spread over
     //    the candidate groups -- the grid is persistent, each wave strides
-    //    over the chunks -- unless a tuning override sets the total;
+    //    over the chunks -- unless a tuning override sets the total; at most
+    //    about 4096 work-groups in all;
+    //  - fail-fast launch (serial_groups): the groups are screened in rounds
+    //    of ff_round groups, one round after another, and a round is one
+    //    set of resident work-groups (stripes = resident / ff_round, at most
+    //    2048).  Measured on the 16- and 64-candidate workloads, rounds of 2
+    //    groups balance best: with 1 the reference is re-read once per group,
+    //    with all groups in one round the work-groups of failed groups idle;
     //  - the workspace is laid out for the bound C_ws, independent of the
     //    device, and the launch never exceeds it.
     const uint64_t n_chunks = numel / 512;
     const uint64_t c_work = align_up((n_chunks + 7) / 8, 8);
     const uint64_t min_c = align_up(numel / (1ull << 31) + 1, 8);
-    uint64_t c_ws = align_up((4096 + groups_max - 1) / groups_max, 8);
-    if (c_ws > c_work) c_ws = c_work;
-    if (c_ws < min_c) c_ws = min_c;
-    if (c_ws < 8) c_ws = 8;
+    auto clamp_c = [&](uint64_t c) {
+        if (c > c_work) c = c_work;
+        if (c < min_c) c = min_c;
+        if (c < 8) c = 8;
+        return c;
+    };
+    const uint64_t c_plain = clamp_c(align_up((4096 + groups_max - 1) / groups_max, 8));
+    const uint64_t c_ws = clamp_c(c_plain > 2048 ? c_plain : 2048);
     if (c_ws > (1u << 20)) return false;
-    int kg_cap = 8, blocks_total = 0;
-    tuning_override(&kg_cap, &blocks_total);
+    int kg_cap = 8, blocks_total = 0, ff_round = kFailFastRound;
+    tuning_override(&kg_cap, &blocks_total, &ff_round);
     if (blocks_total <= 0) blocks_total = resident_blocks > 0 ? resident_blocks : 2048;
     const int groups = P.n_groups > 0 ? P.n_groups : 1;
-    uint64_t C = align_up(((uint64_t)blocks_total + groups - 1) / groups, 8);
-    if (C > c_ws) C = c_ws;
+    P.ff_round = ff_round < groups ? ff_round : groups;
+    uint64_t C;
+    if (serial_groups) {
+        C = align_up(((uint64_t)blocks_total + P.ff_round - 1) / P.ff_round, 8);
+        if (C > c_ws) C = c_ws;
+    } else {
+        C = align_up(((uint64_t)blocks_total + groups - 1) / groups, 8);
+        if (C > c_plain) C = c_plain;
+    }
     if (C < min_c) C = min_c;
     if (C < 8) C = 8;
     P.blocks_per_group = (int)C;
@@ -238,15 +258,20 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     P.off_tickets2 = off;
     off += (size_t)groups_max * 4;
     P.off_tickets1 = off;
-    off = align_up(off + (size_t)groups_max * super_ws * 4, 256);
+    off += (size_t)groups_max * super_ws * 4;
+    off = align_up(off, 256);
+    P.off_ff_flags = off;  // fail-fast words (128-byte lines), zero between calls like the tickets
+    off = align_up(off + (size_t)groups_max * P.kg * (size_t)(1 + super_ws) * 128, 256);
     P.off_table = off;
     off = align_up(off + (size_t)(n_cands + P.kg) * sizeof(CandEntry), 256);
     P.off_part_u32 = off;
-    off = align_up(off + (size_t)PF_COUNT * n_cands * Cw * 4, 256);
+    off = align_up(off + (size_t)kPartPlanes * n_cands * Cw * 4, 256);
     P.off_part_ssd = off;
     off = align_up(off + (size_t)n_cands * Cw * 8, 256);
     P.off_part_ssr = off;
     off = align_up(off + (size_t)groups_max * Cw * 8, 256);
+    P.off_part_ssrc = off;
+    off = align_up(off + (size_t)n_cands * Cw * 8, 256);
     P.off_part2 = off;
     off = align_up(off + (size_t)n_cands * super_ws * sizeof(Part2), 256);
     P.off_part2_ssr = off;
@@ -281,7 +306,7 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands, i
 
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype) {
     ScreenPlan P;
-    if (!make_plan(n_cands, n_cands, numel, dtype, 0, &P)) return 0;
+    if (!make_plan(n_cands, n_cands, numel, dtype, 0, false, &P)) return 0;
     return P.total;
 }
 
@@ -290,7 +315,8 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out) {
     if (out == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_screen_launch: out is NULL");
     if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "dtype %d not screenable", dtype);
     ScreenPlan P;
-    if (!make_plan(n_cands, n_cands, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands, dtype)), &P))
+    if (!make_plan(n_cands, n_cands, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands, dtype)),
+                   false, &P))
         return fail(KB_ERR_INVALID_ARG, "no launch plan for n_cands=%d numel=%llu", n_cands,
                     (unsigned long long)numel);
     out->group_size = P.kg;
@@ -310,8 +336,9 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "kb_screen: n_cands = %d < 1", n_cands);
     if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
         return fail(KB_ERR_INVALID_ARG, "kb_screen: atol and rtol must be finite and >= 0");
-    if (flags & ~(uint32_t)KB_EQUAL_NAN)
+    if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
         return fail(KB_ERR_INVALID_ARG, "kb_screen: unknown flags 0x%x", flags);
+    const bool fail_fast = (flags & KB_FAIL_FAST) != 0;
     std::vector<int32_t> status((size_t)n_cands);
     int rc = kb_policy_check(ref, cands, n_cands, status.data());
     if (rc != KB_OK) return rc;
@@ -322,7 +349,8 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
 
     ScreenPlan P;
-    if (!make_plan(n_cands, n_acc, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands, dtype)), &P))
+    if (!make_plan(n_cands, n_acc, numel, dtype,
+                   resident_blocks(dtype, plan_group_size(n_cands, dtype), fail_fast), fail_fast, &P))
         return fail(KB_ERR_INVALID_ARG, "kb_screen: no launch plan (numel=%llu)",
                     (unsigned long long)numel);
     if (workspace == nullptr || workspace_bytes < P.total)
@@ -384,15 +412,18 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     p.n_groups = P.n_groups;
     p.blocks_per_group = P.blocks_per_group;
     p.n_super = P.n_super;
+    p.ff_round = P.ff_round;
     p.tickets1 = (uint32_t*)(ws + P.off_tickets1);
     p.tickets2 = (uint32_t*)(ws + P.off_tickets2);
+    p.ff_flags = (uint32_t*)(ws + P.off_ff_flags);
     p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
     p.part_ssd = (double*)(ws + P.off_part_ssd);
     p.part_ssr = (double*)(ws + P.off_part_ssr);
+    p.part_ssrc = (double*)(ws + P.off_part_ssrc);
     p.part2 = (Part2*)(ws + P.off_part2);
     p.part2_ssr = (double*)(ws + P.off_part2_ssr);
     p.stats = d_stats;
-    e = launch_screen(P, p, tab, stream);
+    e = launch_screen(P, p, tab, fail_fast, stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen: kernel launch");
     return KB_OK;
 }
@@ -461,7 +492,7 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
     if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: n_cands = %d < 1", n_cands);
     if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
         return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: atol and rtol must be finite and >= 0");
-    if (flags & ~(uint32_t)KB_EQUAL_NAN)
+    if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
         return fail(KB_ERR_INVALID_ARG, "kb_screen_locate: unknown flags 0x%x", flags);
     std::vector<int32_t> status((size_t)n_cands);
     int rc = kb_policy_check(ref, cands, n_cands, status.data());

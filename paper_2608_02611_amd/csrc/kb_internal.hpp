@@ -32,6 +32,9 @@ enum PartField : int {
     PF_BITDIFF,
     PF_COUNT
 };
+// Fail-fast launches keep one more plane: elements compared.
+constexpr int PF_NREAD = PF_COUNT;
+constexpr int kPartPlanes = PF_COUNT + 1;
 
 // Work split and workspace layout of one kb_screen call.
 struct ScreenPlan {
@@ -40,14 +43,15 @@ struct ScreenPlan {
     int n_acc;            // candidates that passed the policy gate
     int kg;               // candidates per candidate group (kernel template)
     int n_groups;         // ceil(n_acc / kg)
-    int blocks_per_group; // multiple of 8 (XCD count)
+    int blocks_per_group; // stripes: a multiple of 8 (XCD count)
     int threads;
     uint64_t numel;
     uint64_t n_vec;       // full 16-byte vectors per tensor
     int n_super;          // ceil(blocks_per_group / 16): first-level combine groups
+    int ff_round;         // fail-fast launch: candidate groups per round
     // workspace byte offsets
-    size_t off_tickets1, off_tickets2, off_table, off_part_u32, off_part_ssd, off_part_ssr,
-        off_part2, off_part2_ssr, total;
+    size_t off_tickets1, off_tickets2, off_ff_flags, off_table, off_part_u32, off_part_ssd,
+        off_part_ssr, off_part_ssrc, off_part2, off_part2_ssr, total;
 };
 
 // Second-level partial of one candidate: the combine of up to 16 work-groups.
@@ -55,20 +59,27 @@ struct Part2 {
     uint64_t mism, nan, pinf, ninf;
     uint32_t maxabs, maxrel, bitdiff, pad;
     double ssd;
+    uint64_t nread;  // fail-fast only: elements compared
+    double ssr;      // fail-fast only: the candidate's own sum of r^2
 };
 
 // Launch geometry and workspace layout.  The layout depends only on
 // (n_cands, numel, dtype); resident_blocks (work-groups of the chosen kernel
-// that fit on the device at once, 0 if unknown) sizes the launch.
+// that fit on the device at once, 0 if unknown) sizes the launch, and
+// serial_groups selects the fail-fast geometry (the groups one after
+// another, each over the whole device).
 bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_blocks,
-               ScreenPlan* plan);
+               bool serial_groups, ScreenPlan* plan);
 
 // Candidates per group the plan picks for n_cands candidates.
 int plan_group_size(int n_cands, int dtype);
 
-// Work-groups of screen_kernel<dtype, kg> resident per CU (occupancy query,
-// cached), or 0 on failure.
-int screen_blocks_per_cu(int dtype, int kg);
+// Work-groups of the screening kernel for (dtype, kg, fail-fast) resident
+// per CU (occupancy query, cached), or 0 on failure.
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast);
+
+// Candidate groups per round of a fail-fast launch (see make_plan).
+constexpr int kFailFastRound = 2;
 
 // Launch tables of up to this many candidates travel in the kernel
 // arguments (no upload); larger ones are uploaded to the workspace.
@@ -95,20 +106,24 @@ struct ScreenParams {
     int n_groups;
     int blocks_per_group;
     int n_super;
+    int ff_round;        // fail-fast: candidate groups per round of the grid
     uint32_t* tickets1;  // [n_groups][n_super]
     uint32_t* tickets2;  // [n_groups]
-    uint32_t* part_u32;  // [PF_COUNT][n_acc][blocks_per_group]
+    uint32_t* ff_flags;  // fail-fast words: [n_groups * KG][1 + n_super] lines of 32 words
+    uint32_t* part_u32;  // [kPartPlanes][n_acc][blocks_per_group]
     double* part_ssd;    // [n_acc][blocks_per_group]
     double* part_ssr;    // [n_groups][blocks_per_group]
+    double* part_ssrc;   // fail-fast: [n_acc][blocks_per_group] per-candidate sums of r^2
     Part2* part2;        // [n_acc][n_super]
     double* part2_ssr;   // [n_groups][n_super]
     kb_stats* stats;     // caller's records, indexed by CandEntry::index
 };
 
 // tab: the launch table when it is inline (n_cands <= kInlineCands), else
-// ignored (p.table points at the uploaded copy).
+// ignored (p.table points at the uploaded copy).  fail_fast selects the
+// early-reject variant of the kernel.
 hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
-                         hipStream_t stream);
+                         bool fail_fast, hipStream_t stream);
 // Zero-fill n bytes of device memory (workspace initialisation).
 hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream);
 // Records for calls with no element to read (numel == 0 or no accepted

@@ -331,9 +331,43 @@ struct WaveOut {
 // VGPRs) where the kernel fits without spilling, else 2.
 constexpr int min_waves(int dt, int kg) { return kg <= 4 || (kg == 8 && dt != DT_F32) ? 4 : 2; }
 
-template <int DT, int KG>
-__global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
-                                                                            InlineTable tab) {
+// Fail-fast words.  Per candidate slot of the launch table, a block of
+// 1 + n_super lines of 128 bytes: line 0 holds the candidate's word (nonzero
+// once it is known to have failed), line 1 + m that of super-group m (16
+// consecutive stripes).  A work-group that finds a failure claims it in LDS
+// (one claim per work-group), then exchanges its super-group's word, and
+// only the first of the super-group sets the candidate's word; so each word
+// sees at most 16 or n_super writers.  (Stores to one word from every
+// work-group that fails at the same moment -- all of them, for a candidate
+// that is wrong everywhere -- serialize at the memory and were measured to
+// cost more than the whole pass.)  Every word lives on its own line.
+__device__ __forceinline__ uint32_t* ff_word(const ScreenParams& p, int slot, int line) {
+    return p.ff_flags + ((size_t)slot * (size_t)(1 + p.n_super) + (size_t)line) * 32u;
+}
+
+// Zero the fail-fast words of a candidate group (its finisher, once every
+// work-group of the group is past its last poll).
+__device__ __forceinline__ void clear_ff_words(const ScreenParams& p, int j0, int kgs) {
+    const int lines = 1 + p.n_super;
+    for (int i = threadIdx.x; i < kgs * lines; i += kThreads) st_coherent(ff_word(p, j0 + i / lines, i % lines), 0u);
+}
+
+// One work-group's part of the screen: candidate group g, element stripe
+// `stripe`, then the finish of the group if this work-group is its last.
+//
+// FF: the fail-fast variant.  Every wave polls its group's candidate words
+// with each chunk, and a wave that counts a mismatch publishes it (above).  A
+// candidate that failed (here or elsewhere) is no longer loaded or compared
+// by the wave, which then keeps, per candidate, the number of elements it
+// compared and its sum of r^2 over them, so that the record of a stopped
+// candidate describes exactly the elements compared.  The poll is issued
+// with the chunk's loads and read at the end of the chunk, when those loads
+// have been waited for anyway, so it adds no wait.  A candidate without
+// mismatch is never stopped, and all its sums are formed in the same order
+// as without FF (the same bits).
+template <int DT, int KG, bool FF>
+__device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineTable& tab, const int g,
+                                            const int stripe) {
     __shared__ double s_ssd[KG][kThreads];  // lane sums of squared differences
     __shared__ WaveOut s_out[kWaves][KG];
     __shared__ double s_ssr[kWaves];
@@ -341,13 +375,14 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     __shared__ uint32_t s_rel[KG];  // work-group max-rel values (binary32 bits)
     __shared__ uint32_t s_is_last;
     __shared__ double s_sr1;        // single-level finish: the group's sum of r^2
+    // fail-fast: per wave and candidate, elements compared and their sum of r^2
+    __shared__ uint32_t s_nread[FF ? kWaves : 1][FF ? KG : 1];
+    __shared__ double s_ssrc[FF ? kWaves : 1][FF ? KG : 1];
+    __shared__ double s_sr1c[FF ? KG : 1];  // single-level finish, per candidate
+    __shared__ uint32_t s_told[FF ? KG : 1];  // fail-fast: the work-group knows candidate j failed
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int xcd = blockIdx.x & 7;
-    const int slot = blockIdx.x >> 3;
-    const int g = slot % p.n_groups;
-    const int stripe = (slot / p.n_groups) * 8 + xcd;
     const int j0 = g * KG;
     const int kg = min(KG, p.n_acc - j0);
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
@@ -374,23 +409,54 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     }
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
     if (threadIdx.x < KG) s_rel[threadIdx.x] = 0u;
+    if (FF && threadIdx.x < KG) s_told[threadIdx.x] = 0u;
     double ssr = 0.0;
+    // fail-fast state (wave-uniform): candidates still compared, chunks done
+    uint32_t alive = (1u << kg) - 1u;
+    uint32_t n_done = 0u;
+    if constexpr (FF) {
+        // candidates that failed before this work-group started are not read
+        // at all (work-groups of a group whose candidates have all failed
+        // then leave at once, freeing their CU for the others)
+        const uint32_t early = (uint32_t)ballot(ld_coherent(ff_word(p, j0 + (lane & (KG - 1)), 0)) != 0u) & alive;
+        if (early != 0u && lane == 0) {
+#pragma unroll
+            for (int j = 0; j < KG; ++j) {
+                if ((early >> j) & 1u) {
+                    s_ssrc[wave][j] = 0.0;
+                    s_nread[wave][j] = 0u;
+                }
+            }
+        }
+        // (kept explicitly wave-uniform: the per-candidate tests must stay
+        // scalar branches, and the loads scalar-base loads)
+        alive = __builtin_amdgcn_readfirstlane(alive & ~early);
+    }
     __syncthreads();
 
     const uint32_t off = 16u * (uint32_t)lane;
     const uint64_t n_chunks = p.numel / kChunk;
     const uint64_t wstride = (uint64_t)p.blocks_per_group * kWaves;
-    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave; chunk < n_chunks; chunk += wstride) {
+    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave; chunk < n_chunks && (!FF || alive != 0u);
+         chunk += wstride) {
         const uint64_t cb = chunk * chunk_bytes<DT>();
         // Re-materialise the lane offset inside the loop so that instruction
         // selection sees (scalar base + zero-extended 32-bit offset) and
         // emits scalar-base loads instead of 64-bit vector address adds.
         uint32_t o = off;
         asm volatile("" : "+v"(o));
+        // the group's failed words (lane l polls candidate l mod KG)
+        uint32_t polled = 0u;
+        if constexpr (FF) polled = ld_coherent(ff_word(p, j0 + (lane & (KG - 1)), 0));
         const Raw<DT> rraw = load_chunk<DT, false>(uniform_ptr(ref + cb), o);
         Raw<DT> craw[KG];
 #pragma unroll
-        for (int j = 0; j < KG; ++j) craw[j] = load_chunk<DT, true>(uniform_ptr(cand[j] + cb), o);
+        for (int j = 0; j < KG; ++j) {
+            if constexpr (FF) {
+                if (!((alive >> j) & 1u)) continue;
+            }
+            craw[j] = load_chunk<DT, true>(uniform_ptr(cand[j] + cb), o);
+        }
         // the work-group's shared max-rel values
 #pragma unroll
         for (int j = 0; j < KG; ++j)
@@ -430,6 +496,9 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             // multiplies the live registers, and all the chunk's loads were
             // issued above, so latency hiding is unaffected.
             __builtin_amdgcn_sched_barrier(0);
+            if constexpr (FF) {
+                if (!((alive >> j) & 1u)) continue;
+            }
             const Raw<DT>& cr = craw[j];
             // bitwise identity on raw storage, until a difference is known
             if (!((bitdiff >> j) & 1u)) {
@@ -500,11 +569,52 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
                 }
             }
         }
+        if constexpr (FF) {
+            // Candidates that failed in this chunk (then set their words) or,
+            // by the poll, elsewhere: stop comparing them, keeping what this
+            // wave compared (this chunk included).
+            ++n_done;
+            uint32_t failed = 0u;
+#pragma unroll
+            for (int j = 0; j < KG; ++j)
+                if (mism[j] != 0u) failed |= 1u << j;
+            failed &= alive;
+            // known failed: by the poll, or by another wave of this work-group
+            const uint32_t told = s_told[lane & (KG - 1)];
+            const uint32_t seen = (uint32_t)ballot(polled != 0u || told != 0u) & alive;
+            // uniform as far as the compiler can tell too, so that the exit
+            // below is a scalar branch and the loop stays uniform
+            const uint32_t stop = __builtin_amdgcn_readfirstlane(failed | seen);
+            if (stop != 0u) {
+                // publish new failures (once per work-group, then once per
+                // super-group)
+                const uint32_t tell = failed & ~seen;
+                if (lane < KG && ((tell >> lane) & 1u)) {
+                    if (atomicOr(&s_told[lane], 1u) == 0u &&
+                        __hip_atomic_exchange(ff_word(p, j0 + lane, 1 + (stripe >> 4)), 1u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT) == 0u)
+                        st_coherent(ff_word(p, j0 + lane, 0), 1u);
+                }
+                const double sr = wave_sum_f64(ssr);
+                if (lane == 0) {
+#pragma unroll
+                    for (int j = 0; j < KG; ++j) {
+                        if ((stop >> j) & 1u) {
+                            s_ssrc[wave][j] = sr;
+                            s_nread[wave][j] = n_done * (uint32_t)kChunk;
+                        }
+                    }
+                }
+                alive = __builtin_amdgcn_readfirstlane(alive & ~stop);
+                if (alive == 0u) break;
+            }
+        }
     }
 
     // Ragged tail: the last numel mod 512 elements, by stripe 0 of each
     // group, one element per thread, exact path (out-of-range lanes and
     // elements 1..7 compare 0 with 0, which changes no statistic).
+    uint32_t n_tail = 0u;  // tail elements this wave compared (for every live candidate)
     if (stripe == 0) {
         const uint64_t first = n_chunks * kChunk;
         for (uint64_t base = first; base < p.numel; base += kThreads) {
@@ -512,6 +622,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             const bool valid = e < p.numel;
             uint32_t rb = 0;
             if (valid) rb = DT == DT_F32 ? ((const uint32_t*)p.ref)[e] : ((const uint16_t*)p.ref)[e];
+            if constexpr (FF) n_tail += popc(ballot(valid));
             float r[kE];
             r[0] = widen_bits<DT>(rb);
 #pragma unroll
@@ -520,6 +631,9 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
 #pragma unroll
             for (int j = 0; j < KG; ++j) {
                 if (j >= kg) continue;
+                if constexpr (FF) {
+                    if (!((alive >> j) & 1u)) continue;
+                }
                 uint32_t cb = 0;
                 if (valid)
                     cb = DT == DT_F32 ? ((const __attribute__((address_space(1))) uint32_t*)cand[j])[e]
@@ -558,6 +672,18 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     {
         const double sr = wave_sum_f64(ssr);
         if (lane == 0) s_ssr[wave] = sr;
+        if constexpr (FF) {
+            // candidates still compared at the end: everything this wave read
+            if (lane == 0) {
+#pragma unroll
+                for (int j = 0; j < KG; ++j) {
+                    if ((alive >> j) & 1u) {
+                        s_ssrc[wave][j] = sr;
+                        s_nread[wave][j] = n_done * (uint32_t)kChunk + n_tail;
+                    }
+                }
+            }
+        }
     }
     __syncthreads();
 
@@ -580,6 +706,17 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             sd += o.ssd;
         }
         const size_t row = (size_t)(j0 + j) * C + stripe;
+        if constexpr (FF) {
+            uint32_t nr = 0u;
+            double src = 0.0;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) {
+                nr += s_nread[w][j];
+                src += s_ssrc[w][j];
+            }
+            st_coherent(&p.part_u32[PF_NREAD * plane + row], nr);
+            st_coherent(&p.part_ssrc[row], src);
+        }
         st_coherent(&p.part_u32[PF_MISM * plane + row], m);
         st_coherent(&p.part_u32[PF_NAN * plane + row], na);
         st_coherent(&p.part_u32[PF_PINF * plane + row], pi);
@@ -620,11 +757,15 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     {
         const bool have = sl < msize;
         const int s = 16 * m + sl;
-        uint64_t mi = 0, na = 0, pi = 0, ni = 0;
+        uint64_t mi = 0, na = 0, pi = 0, ni = 0, nr = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
-        double sd = 0.0;
+        double sd = 0.0, src = 0.0;
         if (jj < kg) {
             const size_t idx = (size_t)(j0 + jj) * C + s;
+            if (FF && have) {
+                nr = ld_coherent(&p.part_u32[PF_NREAD * plane + idx]);
+                src = ld_coherent(&p.part_ssrc[idx]);
+            }
             if (have) {
                 mi = ld_coherent(&p.part_u32[PF_MISM * plane + idx]);
                 na = ld_coherent(&p.part_u32[PF_NAN * plane + idx]);
@@ -643,6 +784,16 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             mr = row_max_u32(mr);
             bd = row_or_u32(bd);
             sd = row_sum_f64(sd);
+            if constexpr (FF) {
+                nr = row_sum_u64(nr);
+                src = row_sum_f64(src);
+                if (sl == 0 && S > 1) {
+                    Part2* q = &p.part2[(size_t)(j0 + jj) * S + m];
+                    st_coherent(&q->nread, nr);
+                    st_coherent(&q->ssr, src);
+                }
+                if (sl == 0 && S == 1) s_sr1c[jj] = src;
+            }
             if (sl == 0 && S > 1) {
                 Part2* q = &p.part2[(size_t)(j0 + jj) * S + m];
                 st_coherent(&q->mism, mi);
@@ -667,11 +818,17 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
             // Single-level finish: the group has at most 16 stripes, and this
             // work-group has combined all of them.
             __syncthreads();
-            if (jj < kg && sl == 0)
-                write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd, sd,
-                             s_sr1);
+            if (jj < kg && sl == 0) {
+                if constexpr (FF)
+                    write_record(&p.stats[table[j0 + jj].index], nr, mi, na, pi, ni, ma, mr, bd, sd,
+                                 s_sr1c[jj]);
+                else
+                    write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd,
+                                 sd, s_sr1);
+            }
             if (g == 0) write_rejected(p, table);
             if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
+            if constexpr (FF) clear_ff_words(p, j0, KG);
             return;
         }
     }
@@ -684,9 +841,9 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
     if (!s_is_last) return;
 
     if (jj < kg) {
-        uint64_t mi = 0, na = 0, pi = 0, ni = 0;
+        uint64_t mi = 0, na = 0, pi = 0, ni = 0, nr = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
-        double sd = 0.0, sr = 0.0;
+        double sd = 0.0, sr = 0.0, src = 0.0;
         const Part2* row = p.part2 + (size_t)(j0 + jj) * S;
         const double* rs = p.part2_ssr + (size_t)g * S;
         for (int q0 = sl; q0 < S; q0 += 64) {
@@ -695,6 +852,10 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int q = q0 + 16 * u;
+                if (FF && q < S) {
+                    nr += ld_coherent(&row[q].nread);
+                    src += ld_coherent(&row[q].ssr);
+                }
                 if (q < S) {
                     const Part2* e = &row[q];
                     v[u].mism = ld_coherent(&e->mism);
@@ -707,7 +868,7 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
                     v[u].ssd = ld_coherent(&e->ssd);
                     w[u] = ld_coherent(&rs[q]);
                 } else {
-                    v[u] = Part2{0, 0, 0, 0, 0u, 0u, 0u, 0u, 0.0};
+                    v[u] = Part2{0, 0, 0, 0, 0u, 0u, 0u, 0u, 0.0, 0, 0.0};
                     w[u] = 0.0;
                 }
             }
@@ -733,13 +894,53 @@ __global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(Scr
         bd = row_or_u32(bd);
         sd = row_sum_f64(sd);
         sr = row_sum_f64(sr);
-        if (sl == 0)
-            write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd, sd, sr);
+        if constexpr (FF) {
+            nr = row_sum_u64(nr);
+            src = row_sum_f64(src);
+            if (sl == 0)
+                write_record(&p.stats[table[j0 + jj].index], nr, mi, na, pi, ni, ma, mr, bd, sd, src);
+        } else {
+            if (sl == 0)
+                write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd, sd,
+                             sr);
+        }
     }
     // Group 0's finisher also writes the rejected candidates' records.
     if (g == 0) write_rejected(p, table);
-    // Leave the ticket at zero for the next call on this workspace.
+    // Leave the ticket and the failed words at zero for the next call on
+    // this workspace (every work-group of the group has finished reading).
     if (threadIdx.x == 0) p.tickets2[g] = 0u;
+    if constexpr (FF) clear_ff_words(p, j0, KG);
+}
+
+// Work-group id -> (candidate group, stripe).  Ids are dealt round robin to
+// the 8 XCDs: id -> (XCD, slot), slot -> (group, stripe group), so that the
+// groups of one stripe run on one XCD and find the reference stripe in its
+// L2.
+// FF = false: one persistent round over all groups.
+// FF = true: the groups are taken in rounds of p.ff_round groups, each round
+// over all stripes, and the grid is sized so that a round fills the device.
+// Work-groups are dispatched in id order, so the device works through the
+// rounds one after another; the work-groups of a group whose candidates are
+// already known to have failed leave at their first poll, and the
+// dispatcher fills their place with the next ones.  (With one persistent
+// round the work-groups of failed groups would idle while those of the live
+// ones did all their work.)  Fewer groups per round re-read the reference
+// once more per round; more groups per round balance less well.
+template <int DT, int KG, bool FF>
+__global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
+                                                                            InlineTable tab) {
+    int id = blockIdx.x, g0 = 0, R = p.n_groups;
+    if constexpr (FF) {
+        const int per_round = p.ff_round * p.blocks_per_group;
+        const int r = id / per_round;
+        g0 = r * p.ff_round;
+        id -= r * per_round;
+        R = min(p.ff_round, p.n_groups - g0);
+    }
+    const int xcd = id & 7;
+    const int slot = id >> 3;
+    screen_part<DT, KG, FF>(p, tab, g0 + slot % R, (slot / R) * 8 + xcd);
 }
 
 __global__ void records_only_kernel(const CandEntry* uploaded, InlineTable tab, int table_inline,
@@ -757,55 +958,67 @@ __global__ void records_only_kernel(const CandEntry* uploaded, InlineTable tab, 
     }
 }
 
-template <int DT, int KG>
+template <int DT, int KG, bool FF>
 hipError_t launch_kg(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
                      hipStream_t stream) {
     const unsigned grid = (unsigned)plan.n_groups * (unsigned)plan.blocks_per_group;
-    hipLaunchKernelGGL((screen_kernel<DT, KG>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
+    hipLaunchKernelGGL((screen_kernel<DT, KG, FF>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
     return hipGetLastError();
 }
 
-template <int DT, int KG>
+template <int DT, int KG, bool FF>
 int occupancy_kg() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG>, kThreads, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG, FF>, kThreads, 0) !=
         hipSuccess)
         return 0;
     return n;
 }
 
-template <int DT>
+template <int DT, bool FF>
 int occupancy_dt(int kg) {
     switch (kg) {
-        case 1: return occupancy_kg<DT, 1>();
-        case 2: return occupancy_kg<DT, 2>();
-        case 4: return occupancy_kg<DT, 4>();
-        case 8: return occupancy_kg<DT, 8>();
-        default: return occupancy_kg<DT, 16>();
+        case 1: return occupancy_kg<DT, 1, FF>();
+        case 2: return occupancy_kg<DT, 2, FF>();
+        case 4: return occupancy_kg<DT, 4, FF>();
+        case 8: return occupancy_kg<DT, 8, FF>();
+        default: return occupancy_kg<DT, 16, FF>();
     }
 }
 
-template <int DT>
+template <int DT, bool FF>
 hipError_t launch_dt(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
                      hipStream_t stream) {
     switch (plan.kg) {
-        case 1: return launch_kg<DT, 1>(plan, p, tab, stream);
-        case 2: return launch_kg<DT, 2>(plan, p, tab, stream);
-        case 4: return launch_kg<DT, 4>(plan, p, tab, stream);
-        case 8: return launch_kg<DT, 8>(plan, p, tab, stream);
-        default: return launch_kg<DT, 16>(plan, p, tab, stream);
+        case 1: return launch_kg<DT, 1, FF>(plan, p, tab, stream);
+        case 2: return launch_kg<DT, 2, FF>(plan, p, tab, stream);
+        case 4: return launch_kg<DT, 4, FF>(plan, p, tab, stream);
+        case 8: return launch_kg<DT, 8, FF>(plan, p, tab, stream);
+        default: return launch_kg<DT, 16, FF>(plan, p, tab, stream);
     }
+}
+
+template <bool FF>
+hipError_t launch_ff(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                     hipStream_t stream) {
+    switch (plan.dtype) {
+        case DT_F32: return launch_dt<DT_F32, FF>(plan, p, tab, stream);
+        case DT_F16: return launch_dt<DT_F16, FF>(plan, p, tab, stream);
+        default: return launch_dt<DT_BF16, FF>(plan, p, tab, stream);
+    }
+}
+
+template <bool FF>
+int occupancy(int dtype, int kg) {
+    return dtype == DT_F32 ? occupancy_dt<DT_F32, FF>(kg)
+                           : dtype == DT_F16 ? occupancy_dt<DT_F16, FF>(kg) : occupancy_dt<DT_BF16, FF>(kg);
 }
 
 }  // namespace
 
 hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
-                         hipStream_t stream) {
-    switch (plan.dtype) {
-        case DT_F32: return launch_dt<DT_F32>(plan, p, tab, stream);
-        case DT_F16: return launch_dt<DT_F16>(plan, p, tab, stream);
-        default: return launch_dt<DT_BF16>(plan, p, tab, stream);
-    }
+                         bool fail_fast, hipStream_t stream) {
+    return fail_fast ? launch_ff<true>(plan, p, tab, stream) : launch_ff<false>(plan, p, tab, stream);
 }
 
 __global__ void zero_fill_kernel(uint4* dst, uint64_t n16) {
@@ -824,16 +1037,16 @@ hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream) {
     return hipGetLastError();
 }
 
-int screen_blocks_per_cu(int dtype, int kg) {
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast) {
     // The occupancy of a kernel does not change during the process.
-    static int cache[3][5] = {{-1, -1, -1, -1, -1}, {-1, -1, -1, -1, -1}, {-1, -1, -1, -1, -1}};
+    static int cache[2][3][5] = {};  // value + 1, 0 = not queried yet
     const int ki = kg == 1 ? 0 : kg == 2 ? 1 : kg == 4 ? 2 : kg == 8 ? 3 : 4;
     const int di = dtype == DT_F32 ? 0 : dtype == DT_F16 ? 1 : 2;
-    int v = __atomic_load_n(&cache[di][ki], __ATOMIC_RELAXED);
+    int* slot = &cache[fail_fast ? 1 : 0][di][ki];
+    int v = __atomic_load_n(slot, __ATOMIC_RELAXED) - 1;
     if (v < 0) {
-        v = dtype == DT_F32 ? occupancy_dt<DT_F32>(kg)
-                            : dtype == DT_F16 ? occupancy_dt<DT_F16>(kg) : occupancy_dt<DT_BF16>(kg);
-        __atomic_store_n(&cache[di][ki], v, __ATOMIC_RELAXED);
+        v = fail_fast ? occupancy<true>(dtype, kg) : occupancy<false>(dtype, kg);
+        __atomic_store_n(slot, v + 1, __ATOMIC_RELAXED);
     }
     return v;
 }

@@ -111,7 +111,7 @@ def test_screen_argument_errors(L):
     assert screen_rc(ref, good, atol=-1.0) == kb.KB_ERR_INVALID_ARG
     assert screen_rc(ref, good, rtol=float("nan")) == kb.KB_ERR_INVALID_ARG
     assert screen_rc(ref, good, atol=float("inf")) == kb.KB_ERR_INVALID_ARG
-    assert screen_rc(ref, good, flags=2) == kb.KB_ERR_INVALID_ARG
+    assert screen_rc(ref, good, flags=4) == kb.KB_ERR_INVALID_ARG
     assert screen_rc(ref, good, stats=None) == kb.KB_ERR_INVALID_ARG
     assert screen_rc(desc(0x10000, kb.KB_U32, (64,)), good) == kb.KB_ERR_DTYPE
     assert screen_rc(ref, good, ws_bytes=16) == kb.KB_ERR_WORKSPACE
