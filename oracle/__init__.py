@@ -45,6 +45,24 @@ class Stats(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class RowStats(ctypes.Structure):
+    _fields_ = [("mean", ctypes.c_double), ("p50", ctypes.c_double), ("p90", ctypes.c_double),
+                ("p95", ctypes.c_double), ("p99", ctypes.c_double), ("tail90", ctypes.c_double),
+                ("tail95", ctypes.c_double), ("tail99", ctypes.c_double),
+                ("speedup", ctypes.c_double), ("n", ctypes.c_int32), ("valid", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class RungScore(ctypes.Structure):
+    _fields_ = [("latency", ctypes.c_double), ("score", ctypes.c_double),
+                ("speedup", ctypes.c_double), ("valid", ctypes.c_int32), ("_pad", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "_pad"}
+
+
 _lib = None
 
 
@@ -93,6 +111,15 @@ def lib():
             getattr(L, name).argtypes = [vp, vp, u64]
         L.kbo_uniform_n.argtypes = [vp, f32, f32, vp, u64]
         L.kbo_match16_n.argtypes = [ctypes.c_int, vp, vp, f32, f32, u32, vp, u64]
+        d, i = ctypes.c_double, ctypes.c_int
+        L.kbo_quantile_sorted.argtypes = [vp, i, d]
+        L.kbo_quantile_sorted.restype = d
+        L.kbo_row_stats.argtypes = [vp, i, ctypes.POINTER(RowStats)]
+        L.kbo_rung_score_of.argtypes = [d, i, d, d, d]
+        L.kbo_rung_score_of.restype = d
+        L.kbo_rung_stats.argtypes = [vp, i, i, i, i, i, d, d, d, ctypes.POINTER(RowStats),
+                                     ctypes.POINTER(RungScore)]
+        L.kbo_rung_stats.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -213,6 +240,48 @@ def locate(ref, cand, dtype, atol, rtol, max_abs, max_rel, flags=0):
     if rc:
         raise ValueError("bad dtype")
     return tuple(out)
+
+
+# ---- rung benchmarker statistics (kbo_rung.c) ----
+
+ALPHA, BETA = 0.02, 0.01  # Appendix A.2
+
+
+def quantile_sorted(x, p):
+    """p-quantile of a 1-D array sorted ascending (linear interpolation)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    return lib().kbo_quantile_sorted(x.ctypes.data, x.size, float(p))
+
+
+def row_stats(t):
+    """Statistics of one row of timing samples (dict; speedup NaN)."""
+    t = np.ascontiguousarray(t, dtype=np.float64)
+    out = RowStats()
+    lib().kbo_row_stats(t.ctypes.data, t.size, ctypes.byref(out))
+    return out.as_dict()
+
+
+def rung_score_of(latency, rung, budget, alpha=ALPHA, beta=BETA):
+    return lib().kbo_rung_score_of(float(latency), int(rung), float(budget), float(alpha),
+                                   float(beta))
+
+
+def rung_stats(samples, base=0, rung=0, budget=0.0, alpha=ALPHA, beta=BETA):
+    """samples: array [n_cands][n_shapes][n_iter] of timing samples (us).
+    Returns (rows: list of n_cands lists of n_shapes dicts, scores: list of
+    n_cands dicts)."""
+    a = np.ascontiguousarray(samples, dtype=np.float64)
+    if a.ndim != 3:
+        raise ValueError("samples must be [n_cands][n_shapes][n_iter]")
+    C, S, N = a.shape
+    rows = (RowStats * (C * S))()
+    scores = (RungScore * C)()
+    rc = lib().kbo_rung_stats(a.ctypes.data, C, S, N, int(base), int(rung), float(budget),
+                              float(alpha), float(beta), rows, scores)
+    if rc:
+        raise ValueError("bad sizes")
+    return ([[rows[c * S + s].as_dict() for s in range(S)] for c in range(C)],
+            [scores[c].as_dict() for c in range(C)])
 
 
 def match(c, r, atol, rtol, flags=0):

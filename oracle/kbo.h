@@ -15,7 +15,10 @@
  *     kbo_partial below;
  *   - the seeded inputs such tests run on: a Philox4x32-10 counter-based
  *     stream (Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as
- *     1, 2, 3", SC'11) mapped to uniform and normal floats.
+ *     1, 2, 3", SC'11) mapped to uniform and normal floats;
+ *   - the rung benchmarker's statistics over timing samples (kbo_rung.c):
+ *     mean, quantiles and tail ratios per shape, speedups, and the runtime
+ *     score of Eq. 2.
  *
  * Enumerations use the same numeric codes as the library's C interface so
  * that a test can pass one code to both sides; that interface is the only
@@ -130,6 +133,36 @@ void kbo_uniform_n(const uint32_t* x, float a, float b, float* out, uint64_t n);
 /* out[i] = match(widen(c[i]), widen(r[i])) for 16-bit storage c, r. */
 void kbo_match16_n(int dtype, const uint16_t* c, const uint16_t* r, float atol, float rtol,
                    uint32_t flags, uint8_t* out, uint64_t n);
+
+/* ---- rung benchmarker statistics (kbo_rung.c) ---- */
+
+/* One (candidate, shape) row of timing samples (us). */
+typedef struct {
+    double mean, p50, p90, p95, p99;
+    double tail90, tail95, tail99; /* p90/p50, p95/p50, p99/p50 */
+    double speedup;                /* baseline row mean / this row mean */
+    int32_t n, valid;
+} kbo_row_t;
+
+/* One candidate at one rung. */
+typedef struct {
+    double latency, score, speedup;
+    int32_t valid, _pad;
+} kbo_score_t;
+
+/* The p-quantile of x[0..n) sorted ascending, n >= 1 (linear interpolation
+ * at position (n - 1) p). */
+double kbo_quantile_sorted(const double* x, int n, double p);
+/* Statistics of one row (speedup left NaN). */
+void kbo_row_stats(const double* t, int n, kbo_row_t* out);
+/* 1e6 / max(1, latency) + alpha rung + beta budget. */
+double kbo_rung_score_of(double latency, int rung, double budget, double alpha, double beta);
+/* Every row of samples[n_cands][n_shapes][n_iter] and every candidate's
+ * score; base = the baseline candidate's index, or -1 for none (speedups
+ * NaN).  Returns 0, or -1 on bad sizes. */
+int kbo_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, int base,
+                   int rung, double budget, double alpha, double beta, kbo_row_t* rows,
+                   kbo_score_t* scores);
 
 #ifdef __cplusplus
 }

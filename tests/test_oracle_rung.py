@@ -1,0 +1,127 @@
+"""Pins of the oracle's rung statistics (CPU).
+
+Each check ties the oracle to something other than its own formulas:
+numpy's linear percentile (the library definition the quantile reading
+follows), closed forms on the samples 1..N and on constant rows, and the
+properties the paper states for the runtime score (Eq. 2 and Section 3.1).
+A plausible slip -- h = N p instead of (N - 1) p, a reversed sort, a mean
+over N - 1, the ratio upside down, the clamp on the wrong side of 1 us, a
+dropped rung term -- fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+QS = (0.5, 0.9, 0.95, 0.99)
+KEYS = ("p50", "p90", "p95", "p99")
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 10, 16, 17, 60, 63, 64, 65, 100, 101, 1000, 4096])
+def test_quantiles_match_numpy_linear(n):
+    rng = np.random.default_rng(n)
+    for trial in range(5):
+        t = rng.lognormal(3.0, 0.3, n)
+        st = oracle.row_stats(t)
+        for q, k in zip(QS, KEYS):
+            want = float(np.percentile(t, 100 * q, method="linear"))
+            # numpy evaluates the same interpolation in a different but
+            # equivalent form: a few units in the last place apart at most
+            assert math.isclose(st[k], want, rel_tol=4e-16, abs_tol=0.0), (n, q, st[k], want)
+
+
+@pytest.mark.parametrize("n", [1, 2, 11, 21, 101, 1001])
+def test_closed_forms_on_one_to_n(n):
+    """Samples 1..N in any order: mean (N + 1) / 2; q(p) = 1 + (N - 1) p
+    exactly where (N - 1) p is an integer."""
+    t = np.arange(1, n + 1, dtype=np.float64)
+    np.random.default_rng(n).shuffle(t)
+    st = oracle.row_stats(t)
+    assert st["mean"] == (n + 1) / 2
+    assert st["p50"] == (n + 1) / 2
+    if n == 101:
+        assert (st["p90"], st["p95"], st["p99"]) == (91.0, 96.0, 100.0)
+        assert st["tail90"] == 91.0 / 51.0
+    if n == 1001:
+        assert (st["p90"], st["p95"], st["p99"]) == (901.0, 951.0, 991.0)
+    if n == 1:
+        assert all(st[k] == 1.0 for k in KEYS)
+
+
+def test_two_samples_interpolate():
+    st = oracle.row_stats(np.array([30.0, 10.0]))
+    assert st["p50"] == 20.0
+    assert st["p90"] == 10.0 + 0.9 * 20.0
+    assert st["p99"] == 10.0 + 0.99 * 20.0
+    assert st["mean"] == 20.0
+
+
+def test_constant_rows_and_order():
+    st = oracle.row_stats(np.full(60, 123.25))
+    assert st["mean"] == 123.25 and all(st[k] == 123.25 for k in KEYS)
+    assert st["tail90"] == st["tail95"] == st["tail99"] == 1.0
+    rng = np.random.default_rng(5)
+    for n in (4, 16, 60):
+        t = rng.gamma(2.0, 10.0, n) + 50.0
+        st = oracle.row_stats(t)
+        assert t.min() <= st["p50"] <= st["p90"] <= st["p95"] <= st["p99"] <= t.max()
+        assert 1.0 <= st["tail90"] <= st["tail95"] <= st["tail99"]
+
+
+def test_invalid_rows():
+    for bad in ([1.0, float("nan")], [1.0, float("inf")], [1.0, 0.0], [2.0, -1.0]):
+        st = oracle.row_stats(np.array(bad))
+        assert st["valid"] == 0 and math.isnan(st["mean"]) and math.isnan(st["p50"])
+    rows, sc = oracle.rung_stats(np.array([[[1.0, 2.0]], [[1.0, float("nan")]]]), base=0)
+    assert sc[0]["valid"] == 1 and sc[1]["valid"] == 0
+    assert sc[1]["score"] == -math.inf and math.isnan(sc[1]["latency"])
+    assert math.isnan(rows[1][0]["speedup"])
+
+
+def test_speedup_is_a_ratio_of_means():
+    """Appendix A.5: speedup per shape = mean base time / mean optimized time."""
+    base = np.array([[2.0, 2.0, 2.0, 2.0], [8.0, 8.0, 8.0, 8.0]])
+    fast = np.array([[1.0, 1.0, 0.5, 1.5], [4.0, 3.0, 5.0, 4.0]])  # means 1 and 4
+    rows, sc = oracle.rung_stats(np.stack([base, fast]), base=0)
+    assert rows[1][0]["speedup"] == 2.0 and rows[1][1]["speedup"] == 2.0
+    assert rows[0][0]["speedup"] == 1.0
+    assert sc[0]["latency"] == 5.0 and sc[1]["latency"] == 2.5 and sc[1]["speedup"] == 2.0
+    rows, sc = oracle.rung_stats(np.stack([base, fast]), base=-1)
+    assert math.isnan(rows[1][0]["speedup"]) and math.isnan(sc[1]["speedup"])
+
+
+def test_score_properties():
+    """Eq. 2 and Section 3.1: the leading term is executions per second with
+    the latency in us, clamped at 1 us; gamma(r) = alpha r + beta b_r is small
+    and favours later rungs, which have larger budgets (repeats 4, 16, 60 in
+    Appendix A.2)."""
+    a, b = oracle.ALPHA, oracle.BETA
+    assert (a, b) == (0.02, 0.01)
+    budgets = {0: 4, 1: 16, 2: 60}
+    # executions per second: 250 us -> 4000 per second, plus gamma
+    assert oracle.rung_score_of(250.0, 0, 0.0) == 4000.0
+    # every latency at or below 1 us scores the same
+    s1 = {oracle.rung_score_of(x, 1, 16.0) for x in (1e-3, 0.5, 1.0)}
+    assert len(s1) == 1 and s1.pop() == 1e6 + a * 1 + b * 16
+    # equal latency: later rung (larger budget) scores higher, by gamma only
+    for lat in (3.0, 250.0, 2606.0):
+        s = [oracle.rung_score_of(lat, r, budgets[r]) for r in (0, 1, 2)]
+        assert s[0] < s[1] < s[2]
+        assert math.isclose(s[2] - s[0], a * 2 + b * (60 - 4), rel_tol=1e-9)
+    # faster is always better, whatever the rungs, once the gap exceeds gamma
+    assert oracle.rung_score_of(1000.0, 0, 4) > oracle.rung_score_of(1001.0, 2, 60)
+    # gamma breaks near-ties: latencies whose leading terms differ by less
+    # than gamma(2) - gamma(0) rank by rung
+    assert oracle.rung_score_of(2606.0, 2, 60) > oracle.rung_score_of(2605.9, 0, 4)
+
+
+def test_incumbent_score_is_consistent():
+    """Section 4.4 prints the MatVec incumbent's score, 384.36, at rung 2.
+    With the repeat count as b_r that is a latency of about 2.6 ms; the check
+    is that this latency scores 384.36 to the printed precision -- a partial
+    pin (the latency itself is not printed)."""
+    lat = 1e6 / (384.36 - (0.02 * 2 + 0.01 * 60))
+    assert 2600.0 < lat < 2612.0
+    assert round(oracle.rung_score_of(lat, 2, 60), 2) == 384.36
