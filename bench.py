@@ -173,6 +173,43 @@ def gen_throughput(dev, kb, n, dtype):
     return res
 
 
+def rung_stats_leg(dev, kb, synth, C=1024, S=3, N=60):
+    """kb_rung_stats on 1024 candidates x 3 shapes x 60 iterations (the
+    last rung of the paper's schedule): kernel time, plus the samples and
+    scores for the CPU-baseline leg's comparison."""
+    import torch
+    t = synth.timing_samples(C, S, N, seed=7)
+    d = t.to(dev)
+    rows, scores = kb.kb_rung_stats(d, 0, 2, 60.0)
+    torch.cuda.synchronize()
+    us = []
+    for _ in range(20):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kb.kb_rung_stats(d, 0, 2, 60.0, rows=rows, scores=scores)
+        e1.record()
+        torch.cuda.synchronize()
+        us.append(e0.elapsed_time(e1) * 1e3)
+    grows, gscores = kb.rung_records(rows, scores, C, S)
+    leg = {"candidates": C, "shapes": S, "iterations": N, "us": round(sorted(us)[len(us) // 2], 1),
+           "sample_bytes": C * S * N * 8}
+    return leg, (t.numpy(), grows, gscores)
+
+
+def rung_cpu_baseline(samples, grows, gscores):
+    """The oracle on the same timing samples, single-threaded (CPU-baseline
+    leg): its time, and whether every score and row field is the same bits."""
+    import oracle
+    t0 = time.perf_counter()
+    orows, oscores = oracle.rung_stats(samples, 0, 2, 60.0)
+    ms = (time.perf_counter() - t0) * 1e3
+    same = all(g["score"] == o["score"] and g["latency_us"] == o["latency"]
+               for g, o in zip(gscores, oscores)) and \
+        all(g["p99_over_p50"] == o["tail99"] and g["mean_us"] == o["mean"]
+            for gr, orr in zip(grows, orows) for g, o in zip(gr, orr))
+    return {"ms": round(ms, 2), "cores": 1, "kind": "oracle", "bit_identical_to_gpu": bool(same)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -311,6 +348,10 @@ def main():
                         "vs_full_kernel": round(kern_ms / ffm, 2),
                         "candidate_elements_read_frac": round(sum(r["numel"] for r in frec) / (K * n), 4),
                         "n_failed": sum(r["mismatches"] > 0 for r in frec)}
+    # the rung benchmarker's statistics (kb_rung_stats) over synthetic timing
+    # samples (the CPU-baseline leg compares them with the oracle)
+    log("rung statistics")
+    out["rung_stats"], rung_data = rung_stats_leg(dev, kb, synth)
     if not args.no_stream_context:
         log("stream context")
         out["stream_context"] = stream_context(dev)
@@ -320,6 +361,7 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        out["cpu_baseline"]["rung_stats"] = rung_cpu_baseline(*rung_data)
     print(json.dumps(out), flush=True)
 
 

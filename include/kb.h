@@ -285,6 +285,67 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
                      float rtol, uint32_t flags, const kb_stats* stats, kb_locate* d_loc,
                      hipStream_t stream);
 
+/* ------------------------------------------------------------------ rung -- */
+
+/* Longest row of timing samples kb_rung_stats takes. */
+#define KB_RUNG_MAX_ITER 4096
+
+/* Statistics of one (candidate, shape) row of timing samples, 80 bytes.
+ *   mean_us          (t_1 + ... + t_n) / n, the sum left to right in binary64
+ *                    (Appendix A.5: the mean time per shape);
+ *   pXX_us           the XX-th percentile: linear interpolation between the
+ *                    order statistics around position h = (n - 1) XX/100,
+ *                    counted from 0: x[k] + (h - k)(x[k+1] - x[k]),
+ *                    k = floor(h), each operation rounded once;
+ *   pXX_over_p50     the tail ratios of Table A.3;
+ *   speedup_vs_base  the baseline's mean for the same shape / mean_us
+ *                    (Appendix A.5), NaN without a baseline;
+ *   n_samples        n;
+ *   valid            1 iff every sample is finite and > 0 (else every
+ *                    double field is NaN). */
+typedef struct kb_sample_stats {
+    double mean_us;
+    double p50_us, p90_us, p95_us, p99_us;
+    double p90_over_p50, p95_over_p50, p99_over_p50;
+    double speedup_vs_base;
+    int32_t n_samples;
+    int32_t valid;
+} kb_sample_stats;
+
+/* One candidate at one rung, 32 bytes.
+ *   latency_us       the mean over the rung's shapes of the row means, left
+ *                    to right (Eq. 1's expectation over shapes, the shapes
+ *                    weighted equally);
+ *   score            S = 1e6 / max(1, latency_us) + alpha rung + beta budget
+ *                    (Eq. 2 with gamma(r) = alpha r + beta b_r, Section 3.1),
+ *                    summed in that order; -inf for an invalid candidate;
+ *   speedup_vs_base  the baseline's latency / latency_us;
+ *   valid            1 iff all the candidate's rows are valid. */
+typedef struct kb_rung_score {
+    double latency_us;
+    double score;
+    double speedup_vs_base;
+    int32_t valid;
+    int32_t reserved;
+} kb_rung_score;
+
+/* The rung benchmarker's statistics (Sections 3.1-3.2, Appendices A.2 and
+ * A.5), stream-ordered on `stream`:
+ *   samples   device, [n_cands][n_shapes][n_iter] timing samples in us
+ *             (binary64, 8-byte aligned), one row per (candidate, shape);
+ *   n_iter    timed iterations per row, 1..KB_RUNG_MAX_ITER;
+ *   base      the baseline candidate's index, or -1 for none;
+ *   rung      r >= 0; budget: b_r (finite, >= 0; the caller's unit, e.g. the
+ *             rung's repeat count); alpha, beta: finite (the paper uses 0.02
+ *             and 0.01);
+ *   rows      device, n_cands * n_shapes kb_sample_stats (8-byte aligned);
+ *   scores    device, n_cands kb_rung_score (8-byte aligned).
+ * Every field is the definition's value to the last bit.  No workspace.
+ * Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, int base, int rung,
+                  double budget, double alpha, double beta, kb_sample_stats* rows,
+                  kb_rung_score* scores, hipStream_t stream);
+
 /* ------------------------------------------------------------- generator -- */
 
 /* Fill device dst[0..n) with elements offset .. offset+n-1 of the seeded

@@ -83,13 +83,36 @@ class KbLocate(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
 
 
+class KbSampleStats(ctypes.Structure):
+    _fields_ = [("mean_us", ctypes.c_double), ("p50_us", ctypes.c_double),
+                ("p90_us", ctypes.c_double), ("p95_us", ctypes.c_double),
+                ("p99_us", ctypes.c_double), ("p90_over_p50", ctypes.c_double),
+                ("p95_over_p50", ctypes.c_double), ("p99_over_p50", ctypes.c_double),
+                ("speedup_vs_base", ctypes.c_double), ("n_samples", ctypes.c_int32),
+                ("valid", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class KbRungScore(ctypes.Structure):
+    _fields_ = [("latency_us", ctypes.c_double), ("score", ctypes.c_double),
+                ("speedup_vs_base", ctypes.c_double), ("valid", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
+assert ctypes.sizeof(KbSampleStats) == 80
+assert ctypes.sizeof(KbRungScore) == 32
 assert ctypes.sizeof(KbStats) == 80
 assert ctypes.sizeof(KbLocate) == 32
 assert ctypes.sizeof(KbTensor) == 144
 
 EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
            "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
-           "kb_screen_locate", "kb_last_error", "kb_version")
+           "kb_screen_locate", "kb_rung_stats", "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -123,6 +146,9 @@ def lib():
         L.kb_screen_locate.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32,
                                        f32, u32, vp, vp, vp]
         L.kb_screen_locate.restype = i32
+        f64 = ctypes.c_double
+        L.kb_rung_stats.argtypes = [vp, i32, i32, i32, i32, i32, f64, f64, f64, vp, vp, vp]
+        L.kb_rung_stats.restype = i32
         L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
         L.kb_gen_inputs.restype = i32
         L.kb_last_error.argtypes = []
@@ -285,6 +311,50 @@ def locate(ref, cands, atol, rtol, flags=0, stream=None):
     d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)
     recs, _ = kb_screen_stats(d_stats, len(cands), stream=stream)
     return recs, kb_screen_locate(ref, cands, atol, rtol, d_stats, flags, stream=stream)
+
+
+RUNG_MAX_ITER = 4096
+RUNG_ALPHA, RUNG_BETA = 0.02, 0.01
+
+
+def kb_rung_stats(samples, base=0, rung=0, budget=0.0, alpha=RUNG_ALPHA, beta=RUNG_BETA,
+                  rows=None, scores=None, stream=None):
+    """Enqueue the rung statistics of samples, a contiguous float64 device
+    tensor [n_cands][n_shapes][n_iter] of timing samples (us).  Returns the
+    (rows, scores) device buffers; read them with rung_records."""
+    torch = _torch()
+    if samples.dtype != torch.float64 or samples.dim() != 3 or not samples.is_contiguous():
+        raise ValueError("samples must be a contiguous float64 [n_cands][n_shapes][n_iter] tensor")
+    C, S, N = samples.shape
+    if rows is None:
+        rows = torch.empty(max(1, C * S) * ctypes.sizeof(KbSampleStats), dtype=torch.uint8,
+                           device=samples.device)
+    if scores is None:
+        scores = torch.empty(max(1, C) * ctypes.sizeof(KbRungScore), dtype=torch.uint8,
+                             device=samples.device)
+    _check(lib().kb_rung_stats(ctypes.c_void_p(samples.data_ptr()), C, S, N, int(base), int(rung),
+                               float(budget), float(alpha), float(beta),
+                               ctypes.c_void_p(rows.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
+                               _stream_handle(stream)))
+    return rows, scores
+
+
+def rung_records(rows, scores, n_cands, n_shapes):
+    """Host copies: (rows as n_cands lists of n_shapes dicts, scores as a
+    list of n_cands dicts).  Synchronizes with the device."""
+    rb = rows.cpu().numpy().tobytes()
+    sb = scores.cpu().numpy().tobytes()
+    R = (KbSampleStats * (n_cands * n_shapes)).from_buffer_copy(rb[:n_cands * n_shapes * 80])
+    Sc = (KbRungScore * n_cands).from_buffer_copy(sb[:n_cands * 32])
+    return ([[R[c * n_shapes + s].as_dict() for s in range(n_shapes)] for c in range(n_cands)],
+            [Sc[c].as_dict() for c in range(n_cands)])
+
+
+def rung_stats(samples, base=0, rung=0, budget=0.0, alpha=RUNG_ALPHA, beta=RUNG_BETA, stream=None):
+    """Enqueue, then read back: (rows, scores) as lists of dicts."""
+    C, S, _ = samples.shape
+    rows, scores = kb_rung_stats(samples, base, rung, budget, alpha, beta, stream=stream)
+    return rung_records(rows, scores, C, S)
 
 
 def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):

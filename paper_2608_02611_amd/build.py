@@ -12,7 +12,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkb.so")
-SOURCES = ["kb_api.hip", "kb_gen.hip", "kb_screen.hip", "kb_locate.hip"]
+SOURCES = ["kb_api.hip", "kb_gen.hip", "kb_screen.hip", "kb_locate.hip", "kb_rung.hip"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-ffp-contract=off",
          "-fhip-fp32-correctly-rounded-divide-sqrt",

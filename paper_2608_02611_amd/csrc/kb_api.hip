@@ -14,6 +14,7 @@
 
 #include "kb_device.hpp"
 #include "kb_internal.hpp"
+#include "kb_rung.hpp"
 
 namespace kb {
 namespace {
@@ -425,6 +426,30 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
     p.stats = d_stats;
     e = launch_screen(P, p, tab, fail_fast, stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen: kernel launch");
+    return KB_OK;
+}
+
+int kb_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, int base, int rung,
+                  double budget, double alpha, double beta, kb_sample_stats* rows,
+                  kb_rung_score* scores, hipStream_t stream) {
+    clear_error();
+    if (samples == nullptr || rows == nullptr || scores == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_stats: null samples, rows or scores");
+    if (n_cands < 1 || n_shapes < 1 || n_iter < 1 || n_iter > KB_RUNG_MAX_ITER)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_stats: n_cands=%d n_shapes=%d n_iter=%d out of range",
+                    n_cands, n_shapes, n_iter);
+    if ((int64_t)n_cands * n_shapes > (1 << 30))
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_stats: too many rows");
+    if (base < -1 || base >= n_cands)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_stats: base %d not in [-1, %d)", base, n_cands);
+    if (rung < 0 || !std::isfinite(budget) || budget < 0.0 || !std::isfinite(alpha) ||
+        !std::isfinite(beta))
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_stats: bad rung, budget, alpha or beta");
+    if (((uintptr_t)samples & 7u) || ((uintptr_t)rows & 7u) || ((uintptr_t)scores & 7u))
+        return fail(KB_ERR_ALIGNMENT, "kb_rung_stats: samples, rows or scores not 8-byte aligned");
+    RungParams p{n_cands, n_shapes, n_iter, base, rung, budget, alpha, beta};
+    hipError_t e = launch_rung_stats(p, samples, rows, scores, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_rung_stats: launch");
     return KB_OK;
 }
 

@@ -210,6 +210,38 @@ def _c5(device, seed, shape, K=8):
 BUILDERS = {"c1": _c1, "c2": _c2, "c3": _c3, "c4": _c4, "c5": _c5}
 
 
+# ------------------------------------------------------------ timing samples
+
+RUNG_REPEATS = (4, 16, 60)  # timed iterations on rungs 0, 1, 2
+
+
+def timing_samples(n_cands, n_shapes, n_iter, seed=0, device="cpu", shape_us=None):
+    """Seeded synthetic timing samples (us), float64 [n_cands][n_shapes][n_iter].
+
+    Recipe (the shape of the paper's measurements, not its data):
+      - shape s has a base latency shape_us[s] (default: 50 us doubling per
+        shape, like a sweep over growing sizes);
+      - candidate c is slower than the best by a factor spread_c drawn
+        log-uniformly from [1, 30] (the rung-0 score spread of Fig. 2 reaches
+        about 30x), candidate 0 (the baseline) at 5x;
+      - each iteration adds half-normal jitter of 0.3% and, with probability
+        3%, a spike of 2-25% (tail ratios p99/p50 of about 1.01-1.25, the
+        range of Table A.3).
+    """
+    g = torch.Generator(device="cpu").manual_seed(0x5EED0000 + seed)
+    if shape_us is None:
+        shape_us = [50.0 * (2 ** s) for s in range(n_shapes)]
+    lat = torch.tensor(shape_us, dtype=torch.float64)
+    spread = torch.exp(torch.rand(n_cands, generator=g, dtype=torch.float64) * math.log(30.0))
+    spread[0] = 5.0
+    mean = spread[:, None, None] * lat[None, :, None]
+    jitter = torch.randn(n_cands, n_shapes, n_iter, generator=g, dtype=torch.float64).abs() * 0.003
+    spike = (torch.rand(n_cands, n_shapes, n_iter, generator=g, dtype=torch.float64) < 0.03)
+    spike_amt = 0.02 + 0.23 * torch.rand(n_cands, n_shapes, n_iter, generator=g, dtype=torch.float64)
+    t = mean * (1.0 + jitter + spike.double() * spike_amt)
+    return t.to(device)
+
+
 def build(name, device="cpu", seed=0, scale=1.0, K=None):
     """Workload `name` on `device`; scale < 1 shrinks N (and K=None keeps K)."""
     spec = SPECS[name]

@@ -212,3 +212,32 @@ def test_locate_argument_errors(L):
     assert f(ctypes.byref(ref), arr, 1, 1e-5, 1e-5, 0, 0x3000, 0x4008, None) == kb.KB_ERR_ALIGNMENT
     bad = desc(0x10000, kb.KB_U32, (64,))
     assert f(ctypes.byref(bad), arr, 1, 1e-5, 1e-5, 0, 0x3000, 0x4000, None) == kb.KB_ERR_DTYPE
+
+
+def test_rung_argument_errors(L):
+    f = kb.lib().kb_rung_stats
+    ok = dict(samples=0x10000, C=3, S=2, N=16, base=0, rung=1, budget=16.0, alpha=0.02, beta=0.01,
+              rows=0x20000, scores=0x30000)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["samples"], a["C"], a["S"], a["N"], a["base"], a["rung"], a["budget"], a["alpha"],
+                 a["beta"], a["rows"], a["scores"], None)
+
+    assert call(samples=None) == kb.KB_ERR_INVALID_ARG
+    assert call(rows=None) == kb.KB_ERR_INVALID_ARG
+    assert call(scores=None) == kb.KB_ERR_INVALID_ARG
+    assert call(C=0) == kb.KB_ERR_INVALID_ARG
+    assert call(S=0) == kb.KB_ERR_INVALID_ARG
+    assert call(N=0) == kb.KB_ERR_INVALID_ARG
+    assert call(N=kb.RUNG_MAX_ITER + 1) == kb.KB_ERR_INVALID_ARG
+    assert call(base=3) == kb.KB_ERR_INVALID_ARG
+    assert call(base=-2) == kb.KB_ERR_INVALID_ARG
+    assert call(rung=-1) == kb.KB_ERR_INVALID_ARG
+    assert call(budget=-1.0) == kb.KB_ERR_INVALID_ARG
+    assert call(budget=float("inf")) == kb.KB_ERR_INVALID_ARG
+    assert call(alpha=float("nan")) == kb.KB_ERR_INVALID_ARG
+    assert call(samples=0x10004) == kb.KB_ERR_ALIGNMENT
+    assert call(rows=0x20004) == kb.KB_ERR_ALIGNMENT
+    assert call(scores=0x30002) == kb.KB_ERR_ALIGNMENT
+    assert "kb_rung_stats" in kb.kb_last_error()
