@@ -120,6 +120,10 @@ def lib():
         L.kbo_rung_stats.argtypes = [vp, i, i, i, i, i, d, d, d, ctypes.POINTER(RowStats),
                                      ctypes.POINTER(RungScore)]
         L.kbo_rung_stats.restype = ctypes.c_int
+        L.kbo_rung_promote.argtypes = [vp, vp, i, i, i, i, vp, vp, vp]
+        L.kbo_rung_promote.restype = ctypes.c_int
+        L.kbo_rung_survival.argtypes = [vp, vp, vp, i, i, vp, vp]
+        L.kbo_rung_survival.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -282,6 +286,36 @@ def rung_stats(samples, base=0, rung=0, budget=0.0, alpha=ALPHA, beta=BETA):
         raise ValueError("bad sizes")
     return ([[rows[c * S + s].as_dict() for s in range(S)] for c in range(C)],
             [scores[c].as_dict() for c in range(C)])
+
+
+def rung_promote(scores, valid, base=0, num=2, den=5):
+    """The promotion decision over one rung's candidates: (rank, order,
+    promoted) as int32 arrays."""
+    sc = np.ascontiguousarray(scores, dtype=np.float64)
+    va = np.ascontiguousarray(valid, dtype=np.int32)
+    n = sc.size
+    rank = np.empty(n, np.int32)
+    order = np.empty(n, np.int32)
+    prom = np.empty(n, np.int32)
+    rc = lib().kbo_rung_promote(sc.ctypes.data, va.ctypes.data, n, int(base), int(num), int(den),
+                                rank.ctypes.data, order.ctypes.data, prom.ctypes.data)
+    if rc:
+        raise ValueError("bad arguments")
+    return rank, order, prom
+
+
+def rung_survival(entering, failed, promoted, original):
+    """Table A.1's Fail% and Promotion% per rung (two float64 arrays)."""
+    e = np.ascontiguousarray(entering, dtype=np.int32)
+    f = np.ascontiguousarray(failed, dtype=np.int32)
+    p = np.ascontiguousarray(promoted, dtype=np.int32)
+    fp = np.empty(e.size)
+    pp = np.empty(e.size)
+    rc = lib().kbo_rung_survival(e.ctypes.data, f.ctypes.data, p.ctypes.data, e.size, int(original),
+                                 fp.ctypes.data, pp.ctypes.data)
+    if rc:
+        raise ValueError("bad arguments")
+    return fp, pp
 
 
 def match(c, r, atol, rtol, flags=0):

@@ -164,6 +164,20 @@ int kbo_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter,
                    int rung, double budget, double alpha, double beta, kbo_row_t* rows,
                    kbo_score_t* scores);
 
+/* Promotion decision over n candidates' scores (valid[i] = 0 for invalid
+ * candidates, whose score is -inf): rank[i] = position of candidate i (0 =
+ * best), order[r] = candidate at position r, promoted[i] = 1 for the first
+ * ceil(n_eligible num / den) valid non-baseline candidates in rank order and
+ * for a valid baseline.  base = -1 for none.  Returns 0, or -1 on bad
+ * arguments (0 <= num <= den, den >= 1). */
+int kbo_rung_promote(const double* score, const int32_t* valid, int n, int base, int num, int den,
+                     int32_t* rank, int32_t* order, int32_t* promoted);
+
+/* Table A.1's columns from per-rung counts: fail_pct[r] = 100 failed[r] /
+ * entering[r], promo_pct[r] = 100 promoted[r] / original. */
+int kbo_rung_survival(const int32_t* entering, const int32_t* failed, const int32_t* promoted,
+                      int n_rungs, int original, double* fail_pct, double* promo_pct);
+
 #ifdef __cplusplus
 }
 #endif

@@ -34,6 +34,20 @@
  *   row has NaN statistics, and a candidate with an invalid row has latency
  *   and speedup NaN and score -inf (it ranks below every valid candidate).
  *
+ * The promotion decision D (Section 3.4: rank by score with deterministic
+ * tie-breaking, promote the top fraction, prune the rest):
+ *   rank    candidates ordered by score, higher first, equal scores by the
+ *           lower index (the deterministic tie-break); invalid candidates
+ *           score -inf and so come last;
+ *   promote of the valid candidates other than the baseline, the first
+ *           ceil(n_eligible num / den) in rank order (integer arithmetic),
+ *           and the baseline itself when it is valid -- Fig. 4 promotes
+ *           "6 candidates + baseline" and "2 candidates + baseline".  The
+ *           paper does not print its fraction; with 2/5 this rule yields
+ *           Fig. 4's counts (15 successful candidates -> 6, then 4 -> 2).
+ *   survival per rung (Table A.1): Fail% = failed / entering, Promotion% =
+ *           promoted / the original candidate count, in percent.
+ *
  * Pins (tests/test_oracle_rung.py): quantiles against numpy's linear
  * percentile; closed forms on the samples 1..N; constant rows; the paper's
  * stated properties of the score (latencies under 1 us all score 1e6 + gamma,
@@ -124,6 +138,57 @@ int kbo_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter,
         }
         const double bl = base >= 0 ? scores[base].latency : NAN;
         scores[c].speedup = scores[c].valid ? bl / scores[c].latency : NAN;
+    }
+    return 0;
+}
+
+/* Candidate j ranks before candidate i. */
+static int better(const double* score, int j, int i) {
+    return score[j] > score[i] || (score[j] == score[i] && j < i);
+}
+
+static const double* g_sort_score;
+static int cmp_rank(const void* a, const void* b) {
+    const int i = *(const int*)a, j = *(const int*)b;
+    if (better(g_sort_score, i, j)) return -1;
+    if (better(g_sort_score, j, i)) return 1;
+    return 0;
+}
+
+int kbo_rung_promote(const double* score, const int32_t* valid, int n, int base, int num, int den,
+                     int32_t* rank, int32_t* order, int32_t* promoted) {
+    if (n < 1 || base < -1 || base >= n || num < 0 || den < 1 || num > den) return -1;
+    int* idx = (int*)malloc(sizeof(int) * (size_t)n);
+    for (int i = 0; i < n; ++i) idx[i] = i;
+    g_sort_score = score;
+    qsort(idx, (size_t)n, sizeof(int), cmp_rank);
+    int n_eligible = 0;
+    for (int i = 0; i < n; ++i) n_eligible += valid[i] && i != base;
+    const long long keep = ((long long)n_eligible * num + den - 1) / den;
+    long long taken = 0;
+    for (int r = 0; r < n; ++r) {
+        const int i = idx[r];
+        order[r] = i;
+        rank[i] = r;
+        int p = 0;
+        if (i == base) {
+            p = valid[i] != 0;
+        } else if (valid[i] && taken < keep) {
+            p = 1;
+            ++taken;
+        }
+        promoted[i] = p;
+    }
+    free(idx);
+    return 0;
+}
+
+int kbo_rung_survival(const int32_t* entering, const int32_t* failed, const int32_t* promoted,
+                      int n_rungs, int original, double* fail_pct, double* promo_pct) {
+    if (n_rungs < 1 || original < 1) return -1;
+    for (int r = 0; r < n_rungs; ++r) {
+        fail_pct[r] = entering[r] > 0 ? 100.0 * (double)failed[r] / (double)entering[r] : 0.0;
+        promo_pct[r] = 100.0 * (double)promoted[r] / (double)original;
     }
     return 0;
 }

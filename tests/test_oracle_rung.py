@@ -125,3 +125,72 @@ def test_incumbent_score_is_consistent():
     lat = 1e6 / (384.36 - (0.02 * 2 + 0.01 * 60))
     assert 2600.0 < lat < 2612.0
     assert round(oracle.rung_score_of(lat, 2, 60), 2) == 384.36
+
+
+# ------------------------------------------------------------- promotion ---
+
+def test_survival_reproduces_table_a1_matvec():
+    """Fig. 4 prints the MatVec run's counts: 21 enter rung 0, 5 fail, 7 are
+    promoted; 7 enter rung 1, 2 fail, 3 are promoted; 3 enter rung 2, none
+    fail.  Table A.1's MatVec row (Fail% of those entering, Promotion% of
+    the original 21) must follow: 23.8, 33.3, 28.6, 14.3."""
+    fail, promo = oracle.rung_survival([21, 7, 3], [5, 2, 0], [7, 3, 3], 21)
+    assert [round(x, 1) for x in fail[:2]] == [23.8, 28.6]
+    assert [round(x, 1) for x in promo[:2]] == [33.3, 14.3]
+    assert fail[2] == 0.0
+
+
+def test_promotion_rule_reproduces_fig4_counts():
+    """With the fraction 2/5 of the successful non-baseline candidates (and
+    the baseline carried), the rule promotes Fig. 4's numbers: 16 successes
+    at rung 0 (15 candidates + baseline) -> 6 candidates + baseline; 5 at
+    rung 1 (4 + baseline) -> 2 + baseline -- whatever the scores."""
+    rng = np.random.default_rng(44)
+    for trial in range(50):
+        s0 = rng.uniform(100, 1000, 21)
+        v0 = np.ones(21, np.int32)
+        v0[rng.choice(np.arange(1, 21), 5, replace=False)] = 0  # 5 failures, baseline 0 passes
+        s0[v0 == 0] = -np.inf
+        _, _, p0 = oracle.rung_promote(s0, v0, base=0, num=2, den=5)
+        assert p0.sum() == 7 and p0[0] == 1
+        survivors = np.flatnonzero(p0)
+        v1 = np.ones(7, np.int32)
+        v1[rng.choice(np.arange(1, 7), 2, replace=False)] = 0  # 2 fail at rung 1
+        s1 = np.where(v1 == 1, rng.uniform(100, 1000, 7), -np.inf)
+        _, _, p1 = oracle.rung_promote(s1, v1, base=0, num=2, den=5)
+        assert p1.sum() == 3 and p1[0] == 1
+        assert survivors.size == 7
+
+
+def test_ranking_matches_a_library_sort():
+    """Ranks against Python's sort on the key (-score, index): higher scores
+    first, equal scores by the lower index; invalid (-inf) last."""
+    rng = np.random.default_rng(7)
+    for n in (1, 2, 5, 21, 100, 1000):
+        s = np.round(rng.uniform(0, 10, n), 0)  # many ties
+        v = (rng.uniform(size=n) > 0.2).astype(np.int32)
+        s[v == 0] = -np.inf
+        rank, order, _ = oracle.rung_promote(s, v, base=-1, num=1, den=2)
+        want = sorted(range(n), key=lambda i: (-s[i], i))
+        assert list(order) == want
+        assert all(rank[order[r]] == r for r in range(n))
+
+
+def test_promotion_hand_cases():
+    inf = np.inf
+    # ties broken by index; baseline carried although it ranks last
+    rank, order, p = oracle.rung_promote([1.0, 5.0, 5.0, 2.0, 9.0], [1] * 5, base=0, num=1, den=2)
+    assert list(order) == [4, 1, 2, 3, 0] and list(p) == [1, 1, 0, 0, 1]
+    # fraction 0: only the baseline; fraction 1: every valid candidate
+    _, _, p = oracle.rung_promote([3.0, 2.0, 1.0], [1, 1, 1], base=1, num=0, den=5)
+    assert list(p) == [0, 1, 0]
+    _, _, p = oracle.rung_promote([3.0, -inf, 1.0], [1, 0, 1], base=0, num=5, den=5)
+    assert list(p) == [1, 0, 1]
+    # an invalid baseline is not carried; no baseline at all
+    _, _, p = oracle.rung_promote([-inf, 4.0, 8.0, 6.0], [0, 1, 1, 1], base=0, num=1, den=3)
+    assert list(p) == [0, 0, 1, 0]
+    _, _, p = oracle.rung_promote([4.0, 8.0, 6.0], [1, 1, 1], base=-1, num=2, den=3)
+    assert list(p) == [0, 1, 1]
+    # ceil, in integers: 7 eligible at 2/5 -> 3 (14/5 = 2.8)
+    _, _, p = oracle.rung_promote(np.arange(8.0), [1] * 8, base=0, num=2, den=5)
+    assert p.sum() == 4 and list(np.flatnonzero(p)) == [0, 5, 6, 7]
