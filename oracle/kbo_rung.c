@@ -37,8 +37,9 @@
  * The promotion decision D (Section 3.4: rank by score with deterministic
  * tie-breaking, promote the top fraction, prune the rest):
  *   rank    candidates ordered by score, higher first, equal scores by the
- *           lower index (the deterministic tie-break); invalid candidates
- *           score -inf and so come last;
+ *           lower index (the deterministic tie-break); an invalid
+ *           candidate (or a NaN score) ranks as -inf, so invalid ones come
+ *           last, in index order;
  *   promote of the valid candidates other than the baseline, the first
  *           ceil(n_eligible num / den) in rank order (integer arithmetic),
  *           and the baseline itself when it is valid -- Fig. 4 promotes
@@ -142,9 +143,10 @@ int kbo_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter,
     return 0;
 }
 
-/* Candidate j ranks before candidate i. */
-static int better(const double* score, int j, int i) {
-    return score[j] > score[i] || (score[j] == score[i] && j < i);
+/* Candidate j ranks before candidate i (keys: the score of a valid
+ * candidate, -inf for an invalid one or a NaN score). */
+static int better(const double* key, int j, int i) {
+    return key[j] > key[i] || (key[j] == key[i] && j < i);
 }
 
 static const double* g_sort_score;
@@ -159,8 +161,12 @@ int kbo_rung_promote(const double* score, const int32_t* valid, int n, int base,
                      int32_t* rank, int32_t* order, int32_t* promoted) {
     if (n < 1 || base < -1 || base >= n || num < 0 || den < 1 || num > den) return -1;
     int* idx = (int*)malloc(sizeof(int) * (size_t)n);
-    for (int i = 0; i < n; ++i) idx[i] = i;
-    g_sort_score = score;
+    double* key = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int i = 0; i < n; ++i) {
+        idx[i] = i;
+        key[i] = valid[i] && !isnan(score[i]) ? score[i] : -INFINITY;
+    }
+    g_sort_score = key;
     qsort(idx, (size_t)n, sizeof(int), cmp_rank);
     int n_eligible = 0;
     for (int i = 0; i < n; ++i) n_eligible += valid[i] && i != base;
@@ -180,6 +186,7 @@ int kbo_rung_promote(const double* score, const int32_t* valid, int n, int base,
         promoted[i] = p;
     }
     free(idx);
+    free(key);
     return 0;
 }
 

@@ -194,3 +194,13 @@ def test_promotion_hand_cases():
     # ceil, in integers: 7 eligible at 2/5 -> 3 (14/5 = 2.8)
     _, _, p = oracle.rung_promote(np.arange(8.0), [1] * 8, base=0, num=2, den=5)
     assert p.sum() == 4 and list(np.flatnonzero(p)) == [0, 5, 6, 7]
+
+
+def test_invalid_and_nan_rank_last():
+    """Pruned candidates (invalid, or a NaN score) rank after every valid
+    one, in index order, whatever their score field holds."""
+    s = np.array([np.nan, 5.0, 7.0, 1e9, 2.0])
+    v = np.array([1, 1, 1, 0, 1], np.int32)
+    rank, order, p = oracle.rung_promote(s, v, base=-1, num=1, den=1)
+    assert list(order) == [2, 1, 4, 0, 3]
+    assert list(p) == [1, 1, 1, 0, 1]
