@@ -191,8 +191,19 @@ def rung_stats_leg(dev, kb, synth, C=1024, S=3, N=60):
         torch.cuda.synchronize()
         us.append(e0.elapsed_time(e1) * 1e3)
     grows, gscores = kb.rung_records(rows, scores, C, S)
+    # the promotion decision over those scores (2/5 of the candidates, the
+    # baseline carried)
+    pus = []
+    for _ in range(20):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rank, order, prom = kb.kb_rung_promote(scores, C, 0, 2, 5)
+        e1.record()
+        torch.cuda.synchronize()
+        pus.append(e0.elapsed_time(e1) * 1e3)
     leg = {"candidates": C, "shapes": S, "iterations": N, "us": round(sorted(us)[len(us) // 2], 1),
-           "sample_bytes": C * S * N * 8}
+           "sample_bytes": C * S * N * 8, "promote_us": round(sorted(pus)[len(pus) // 2], 1),
+           "promoted": int(prom.sum().item())}
     return leg, (t.numpy(), grows, gscores)
 
 

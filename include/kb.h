@@ -346,6 +346,38 @@ int kb_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, 
                   double budget, double alpha, double beta, kb_sample_stats* rows,
                   kb_rung_score* scores, hipStream_t stream);
 
+/* The promotion decision D of Section 3.4 (Algorithm 1's promote-or-prune
+ * step) over one rung's candidates, stream-ordered on `stream`:
+ *   scores    device, n_cands kb_rung_score (as kb_rung_stats writes them);
+ *             the ranking key is `score` for a valid candidate and -inf for
+ *             an invalid one or a NaN score;
+ *   base      the baseline's index, or -1 for none;
+ *   frac_num / frac_den   the promoted fraction, 0 <= num <= den, den >= 1;
+ *   rank      device, n_cands int32: candidate i's position, 0 = best;
+ *             higher keys first, equal keys by the lower index (the
+ *             deterministic tie-break);
+ *   order     device, n_cands int32: the candidate at each position;
+ *   promoted  device, n_cands int32: 1 for the first
+ *             ceil(n_eligible frac_num / frac_den) valid non-baseline
+ *             candidates in rank order (n_eligible = their count, computed
+ *             in integers) and for a valid baseline, which is always
+ *             carried to the next rung (Fig. 4: "6 candidates + baseline");
+ *             0 for the pruned.
+ * All arrays 4-byte aligned (scores 8).  n_cands <= KB_PROMOTE_MAX.
+ * Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+#define KB_PROMOTE_MAX 65536
+int kb_rung_promote(const kb_rung_score* scores, int n_cands, int base, int frac_num, int frac_den,
+                    int32_t* rank, int32_t* order, int32_t* promoted, hipStream_t stream);
+
+/* Per-rung survival, the columns of Table A.1 (host only, no device work):
+ *   fail_pct[r]  = 100 failed[r] / entering[r] (0 when nothing entered);
+ *   promo_pct[r] = 100 promoted[r] / original (the initial pool, baseline
+ *                  included).
+ * Errors: KB_ERR_INVALID_ARG (null arrays, n_rungs < 1, original < 1, a
+ * negative count, failed > entering). */
+int kb_rung_survival(const int32_t* entering, const int32_t* failed, const int32_t* promoted,
+                     int n_rungs, int original, double* fail_pct, double* promo_pct);
+
 /* ------------------------------------------------------------- generator -- */
 
 /* Fill device dst[0..n) with elements offset .. offset+n-1 of the seeded

@@ -112,7 +112,8 @@ assert ctypes.sizeof(KbTensor) == 144
 
 EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
            "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
-           "kb_screen_locate", "kb_rung_stats", "kb_last_error", "kb_version")
+           "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_last_error",
+           "kb_version")
 
 _lib = None
 
@@ -149,6 +150,10 @@ def lib():
         f64 = ctypes.c_double
         L.kb_rung_stats.argtypes = [vp, i32, i32, i32, i32, i32, f64, f64, f64, vp, vp, vp]
         L.kb_rung_stats.restype = i32
+        L.kb_rung_promote.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.kb_rung_promote.restype = i32
+        L.kb_rung_survival.argtypes = [vp, vp, vp, i32, i32, vp, vp]
+        L.kb_rung_survival.restype = i32
         L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
         L.kb_gen_inputs.restype = i32
         L.kb_last_error.argtypes = []
@@ -355,6 +360,35 @@ def rung_stats(samples, base=0, rung=0, budget=0.0, alpha=RUNG_ALPHA, beta=RUNG_
     C, S, _ = samples.shape
     rows, scores = kb_rung_stats(samples, base, rung, budget, alpha, beta, stream=stream)
     return rung_records(rows, scores, C, S)
+
+
+PROMOTE_MAX = 65536
+
+
+def kb_rung_promote(scores, n_cands, base=0, frac_num=2, frac_den=5, stream=None):
+    """Enqueue the promotion decision over a device buffer of n_cands
+    kb_rung_score (e.g. the scores kb_rung_stats returned).  Returns device
+    int32 tensors (rank, order, promoted)."""
+    torch = _torch()
+    dev = scores.device
+    rank = torch.empty(n_cands, dtype=torch.int32, device=dev)
+    order = torch.empty(n_cands, dtype=torch.int32, device=dev)
+    promoted = torch.empty(n_cands, dtype=torch.int32, device=dev)
+    _check(lib().kb_rung_promote(ctypes.c_void_p(scores.data_ptr()), int(n_cands), int(base),
+                                 int(frac_num), int(frac_den), ctypes.c_void_p(rank.data_ptr()),
+                                 ctypes.c_void_p(order.data_ptr()),
+                                 ctypes.c_void_p(promoted.data_ptr()), _stream_handle(stream)))
+    return rank, order, promoted
+
+
+def kb_rung_survival(entering, failed, promoted, original):
+    """Table A.1's Fail% and Promotion% per rung (host only): two lists."""
+    n = len(entering)
+    arr = lambda v: (ctypes.c_int32 * max(1, n))(*[int(x) for x in v])
+    fp = (ctypes.c_double * max(1, n))()
+    pp = (ctypes.c_double * max(1, n))()
+    _check(lib().kb_rung_survival(arr(entering), arr(failed), arr(promoted), n, int(original), fp, pp))
+    return list(fp)[:n], list(pp)[:n]
 
 
 def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):

@@ -453,6 +453,44 @@ int kb_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, 
     return KB_OK;
 }
 
+int kb_rung_promote(const kb_rung_score* scores, int n_cands, int base, int frac_num, int frac_den,
+                    int32_t* rank, int32_t* order, int32_t* promoted, hipStream_t stream) {
+    clear_error();
+    if (scores == nullptr || rank == nullptr || order == nullptr || promoted == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_promote: null scores, rank, order or promoted");
+    if (n_cands < 1 || n_cands > KB_PROMOTE_MAX)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_promote: n_cands = %d not in [1, %d]", n_cands,
+                    KB_PROMOTE_MAX);
+    if (base < -1 || base >= n_cands)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_promote: base %d not in [-1, %d)", base, n_cands);
+    if (frac_den < 1 || frac_num < 0 || frac_num > frac_den)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_promote: fraction %d/%d not in [0, 1]", frac_num,
+                    frac_den);
+    if (((uintptr_t)scores & 7u) || ((uintptr_t)rank & 3u) || ((uintptr_t)order & 3u) ||
+        ((uintptr_t)promoted & 3u))
+        return fail(KB_ERR_ALIGNMENT, "kb_rung_promote: misaligned array");
+    hipError_t e = launch_rung_promote(scores, n_cands, base, frac_num, frac_den, rank, order,
+                                       promoted, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_rung_promote: launch");
+    return KB_OK;
+}
+
+int kb_rung_survival(const int32_t* entering, const int32_t* failed, const int32_t* promoted,
+                     int n_rungs, int original, double* fail_pct, double* promo_pct) {
+    clear_error();
+    if (entering == nullptr || failed == nullptr || promoted == nullptr || fail_pct == nullptr ||
+        promo_pct == nullptr || n_rungs < 1 || original < 1)
+        return fail(KB_ERR_INVALID_ARG, "kb_rung_survival: null array or bad count");
+    for (int r = 0; r < n_rungs; ++r)
+        if (entering[r] < 0 || failed[r] < 0 || promoted[r] < 0 || failed[r] > entering[r])
+            return fail(KB_ERR_INVALID_ARG, "kb_rung_survival: inconsistent counts at rung %d", r);
+    for (int r = 0; r < n_rungs; ++r) {
+        fail_pct[r] = entering[r] > 0 ? 100.0 * (double)failed[r] / (double)entering[r] : 0.0;
+        promo_pct[r] = 100.0 * (double)promoted[r] / (double)original;
+    }
+    return KB_OK;
+}
+
 int kb_screen_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
     clear_error();
     if (workspace == nullptr || workspace_bytes == 0)

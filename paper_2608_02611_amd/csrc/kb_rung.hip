@@ -12,7 +12,8 @@
 //                    across the lanes;
 // rows_block_kernel  longer rows (up to kRungMaxIter): one work-group per
 //                    row, bitonic sort in LDS;
-// scores_kernel      one thread per candidate: latency, score, speedups.
+// scores_kernel      one thread per candidate: latency, score, speedups;
+// promote_kernel     the promotion decision over the scores.
 //
 // Every sum runs left to right in binary64, as the definitions read (the
 // rows are short, so a sequential sum costs little), and every formula is
@@ -213,7 +214,65 @@ __global__ __launch_bounds__(kThreads) void scores_kernel(RungParams p, kb_sampl
     }
 }
 
+// The promotion decision D (Section 3.4): rank by score, ties to the lower
+// index, and promote the first ceil(n_eligible num / den) valid non-baseline
+// candidates plus a valid baseline.  Ranking is by counting: candidate i's
+// rank is the number of candidates that come before it, so one thread per
+// candidate scans every key (staged through LDS in tiles of the work-group
+// size) and no sort or atomic is needed; the ranks are a permutation, and
+// `order` is their inverse.
+__device__ __forceinline__ double rank_key(const kb_rung_score& s) {
+    return s.valid != 0 && s.score == s.score ? s.score : -__builtin_inf();
+}
+
+__global__ __launch_bounds__(kThreads) void promote_kernel(const kb_rung_score* __restrict__ scores,
+                                                            int n, int base, int num, int den,
+                                                            int32_t* __restrict__ rank,
+                                                            int32_t* __restrict__ order,
+                                                            int32_t* __restrict__ promoted) {
+    __shared__ double s_key[kThreads];
+    __shared__ uint8_t s_elig[kThreads];
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    const bool me = i < n;
+    const double ki = me ? rank_key(scores[i]) : 0.0;
+    const bool valid_i = me && scores[i].valid != 0;
+    int before = 0, before_elig = 0, n_elig = 0;
+    for (int t0 = 0; t0 < n; t0 += kThreads) {
+        const int j = t0 + threadIdx.x;
+        if (j < n) {
+            s_key[threadIdx.x] = rank_key(scores[j]);
+            s_elig[threadIdx.x] = scores[j].valid != 0 && j != base;
+        }
+        __syncthreads();
+        const int m = min(kThreads, n - t0);
+        for (int u = 0; u < m; ++u) {
+            const int j2 = t0 + u;
+            const double kj = s_key[u];
+            const bool b = kj > ki || (kj == ki && j2 < i);
+            before += b;
+            before_elig += b && s_elig[u];
+            n_elig += s_elig[u];
+        }
+        __syncthreads();
+    }
+    if (!me) return;
+    const long long keep = ((long long)n_elig * num + den - 1) / den;
+    rank[i] = before;
+    order[before] = i;
+    int p;
+    if (i == base) p = valid_i ? 1 : 0;
+    else p = valid_i && before_elig < keep ? 1 : 0;
+    promoted[i] = p;
+}
+
 }  // namespace
+
+hipError_t launch_rung_promote(const kb_rung_score* scores, int n, int base, int num, int den,
+                               int32_t* rank, int32_t* order, int32_t* promoted, hipStream_t stream) {
+    hipLaunchKernelGGL(promote_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
+                       scores, n, base, num, den, rank, order, promoted);
+    return hipGetLastError();
+}
 
 hipError_t launch_rung_stats(const RungParams& p, const double* samples, kb_sample_stats* rows,
                              kb_rung_score* scores, hipStream_t stream) {

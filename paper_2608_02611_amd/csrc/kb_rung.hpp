@@ -1,4 +1,5 @@
-// kb_rung.hpp -- declarations of the rung-statistics kernels (kb_rung.hip),
+// kb_rung.hpp -- declarations of the rung kernels (kb_rung.hip): statistics
+// and the promotion decision,
 // shared with the host side of the C interface.
 #pragma once
 
@@ -17,5 +18,8 @@ struct RungParams {
 
 hipError_t launch_rung_stats(const RungParams& p, const double* samples, kb_sample_stats* rows,
                              kb_rung_score* scores, hipStream_t stream);
+
+hipError_t launch_rung_promote(const kb_rung_score* scores, int n, int base, int num, int den,
+                               int32_t* rank, int32_t* order, int32_t* promoted, hipStream_t stream);
 
 }  // namespace kb

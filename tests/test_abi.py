@@ -241,3 +241,44 @@ def test_rung_argument_errors(L):
     assert call(rows=0x20004) == kb.KB_ERR_ALIGNMENT
     assert call(scores=0x30002) == kb.KB_ERR_ALIGNMENT
     assert "kb_rung_stats" in kb.kb_last_error()
+
+
+def test_promote_argument_errors(L):
+    f = kb.lib().kb_rung_promote
+    ok = dict(sc=0x10000, n=5, base=0, num=2, den=5, rank=0x20000, order=0x30000, prom=0x40000)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["sc"], a["n"], a["base"], a["num"], a["den"], a["rank"], a["order"], a["prom"], None)
+
+    assert call(sc=None) == kb.KB_ERR_INVALID_ARG
+    assert call(rank=None) == kb.KB_ERR_INVALID_ARG
+    assert call(order=None) == kb.KB_ERR_INVALID_ARG
+    assert call(prom=None) == kb.KB_ERR_INVALID_ARG
+    assert call(n=0) == kb.KB_ERR_INVALID_ARG
+    assert call(n=kb.PROMOTE_MAX + 1) == kb.KB_ERR_INVALID_ARG
+    assert call(base=5) == kb.KB_ERR_INVALID_ARG
+    assert call(base=-2) == kb.KB_ERR_INVALID_ARG
+    assert call(den=0) == kb.KB_ERR_INVALID_ARG
+    assert call(num=-1) == kb.KB_ERR_INVALID_ARG
+    assert call(num=6) == kb.KB_ERR_INVALID_ARG
+    assert call(sc=0x10004) == kb.KB_ERR_ALIGNMENT
+    assert call(order=0x30002) == kb.KB_ERR_ALIGNMENT
+    assert "kb_rung_promote" in kb.kb_last_error()
+
+
+def test_survival_host_function(L):
+    """The library's survival accounting against the oracle's (host only)."""
+    import oracle
+    cases = [([21, 7, 3], [5, 2, 0], [7, 3, 3], 21), ([31, 8, 3], [5, 2, 0], [8, 3, 3], 31),
+             ([26, 6], [5, 0], [6, 4], 26), ([1], [0], [0], 1), ([0, 0], [0, 0], [0, 0], 5)]
+    for entering, failed, promoted, orig in cases:
+        g = kb.kb_rung_survival(entering, failed, promoted, orig)
+        o = oracle.rung_survival(entering, failed, promoted, orig)
+        assert g[0] == list(o[0]) and g[1] == list(o[1])
+    fail, promo = kb.kb_rung_survival([21, 7], [5, 2], [7, 3], 21)
+    assert [round(x, 1) for x in fail + promo] == [23.8, 28.6, 33.3, 14.3]
+    with pytest.raises(kb.KbError):
+        kb.kb_rung_survival([3], [4], [0], 3)
+    with pytest.raises(kb.KbError):
+        kb.kb_rung_survival([3], [1], [1], 0)
