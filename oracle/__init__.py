@@ -318,6 +318,77 @@ def rung_survival(entering, failed, promoted, original):
     return fp, pp
 
 
+# ---- multi-output candidates ----
+
+STATUS_OK, REJECT_NULL, REJECT_DTYPE, REJECT_SHAPE, REJECT_LAYOUT = 0, 1, 2, 3, 4
+
+
+def gate_status(ref, cand):
+    """The policy gate of one output (Section 3.2: the output's shape and
+    dtype against the reference's), plus the two checks a tensor view needs
+    before it can be read: data present, dense row-major layout.  ref and
+    cand are dicts {"null": bool, "dtype": int, "shape": tuple, "strides":
+    tuple} (cand may be None: a missing output).  The first failing check,
+    in the order null, dtype, shape, layout."""
+    if cand is None:
+        return REJECT_NULL
+    numel = 1
+    for d in cand["shape"]:
+        numel *= d
+    if cand["null"] and numel != 0:
+        return REJECT_NULL
+    if cand["dtype"] != ref["dtype"]:
+        return REJECT_DTYPE
+    if tuple(cand["shape"]) != tuple(ref["shape"]):
+        return REJECT_SHAPE
+    if numel != 0:
+        expect = 1
+        for d, st in zip(reversed(cand["shape"]), reversed(cand["strides"])):
+            if d != 1 and st != expect:
+                return REJECT_LAYOUT
+            expect *= d
+    return STATUS_OK
+
+
+def rejected_record(status):
+    rec = {f: 0 for f in ("numel", "mismatches", "nan_count", "pos_inf_count", "neg_inf_count",
+                          "bitwise_equal", "passed")}
+    rec.update({"sum_sq_diff": 0.0, "sum_sq_ref": 0.0, "rel_l2": 0.0, "max_abs_err": 0.0,
+                "max_rel_err": 0.0, "status": status})
+    return rec
+
+
+def screen_multi(refs, cands, atol, rtol, flags=0):
+    """Multi-output screen.  refs: list of (meta, storage, dtype name);
+    cands: list of per-candidate lists of (meta or None, storage or None);
+    atol, rtol: per-output lists.  One gate over all outputs: a candidate is
+    read only if every output passes; otherwise each of its records has the
+    first failing status of the first failing output.  Returns (records as
+    records[o][k], passed[k]: every output passes and matches)."""
+    n_out = len(refs)
+    status = []
+    for row in cands:
+        st = STATUS_OK
+        for o in range(n_out):
+            st = gate_status(refs[o][0], row[o][0])
+            if st != STATUS_OK:
+                break
+        status.append(st)
+    records = [[None] * len(cands) for _ in range(n_out)]
+    for k, row in enumerate(cands):
+        for o in range(n_out):
+            if status[k] != STATUS_OK:
+                records[o][k] = rejected_record(status[k])
+            else:
+                r = screen(refs[o][1], row[o][1], refs[o][2], atol[o], rtol[o], flags)
+                r["status"] = STATUS_OK
+                records[o][k] = r
+    passed = [int(status[k] == STATUS_OK and all(records[o][k]["mismatches"] == 0
+                                                  for o in range(n_out)))
+              for k in range(len(cands))]
+    return records, passed
+
+
 def match(c, r, atol, rtol, flags=0):
     return bool(lib().kbo_match(c, r, atol, rtol, flags))
 

@@ -282,3 +282,48 @@ def test_survival_host_function(L):
         kb.kb_rung_survival([3], [4], [0], 3)
     with pytest.raises(kb.KbError):
         kb.kb_rung_survival([3], [1], [1], 0)
+
+
+def test_gate_matches_the_oracle_on_random_views(L):
+    """kb_policy_check (library host code) against the oracle's gate on
+    random descriptors: dtypes, shapes, strides, null data."""
+    import random
+    import oracle
+    rnd = random.Random(2024)
+
+    def rand_meta(base):
+        shape = list(base["shape"])
+        kind = rnd.random()
+        if kind < 0.15:
+            shape = [max(0, d + rnd.choice([-1, 1])) for d in shape]
+        elif kind < 0.2:
+            shape = shape + [1]
+        dtype = base["dtype"] if rnd.random() > 0.15 else rnd.choice([0, 1, 2])
+        strides, acc = [], 1
+        for d in reversed(shape):
+            strides.append(acc)
+            acc *= d
+        strides = list(reversed(strides))
+        if rnd.random() < 0.25 and len(shape) > 1:
+            i = rnd.randrange(len(shape))
+            strides[i] = rnd.choice([0, 1, 2, 3, strides[i] * 2, strides[i] + 1])
+        return {"null": rnd.random() < 0.1, "dtype": dtype, "shape": tuple(shape),
+                "strides": tuple(strides)}
+
+    def desc_of(m):
+        return desc(None if m["null"] else 0x20000, m["dtype"], m["shape"], m["strides"])
+
+    for trial in range(2000):
+        nd = rnd.randrange(0, 4)
+        shape = tuple(rnd.choice([0, 1, 2, 3, 5]) for _ in range(nd))
+        ref_m = {"null": False, "dtype": rnd.choice([0, 1, 2]), "shape": shape, "strides": None}
+        strides, acc = [], 1
+        for d in reversed(shape):
+            strides.append(acc)
+            acc *= d
+        ref_m["strides"] = tuple(reversed(strides))
+        cands = [rand_meta(ref_m) for _ in range(4)]
+        rc, st = gate(desc(0x10000, ref_m["dtype"], shape, ref_m["strides"]),
+                      [desc_of(m) for m in cands])
+        assert rc == kb.KB_OK
+        assert list(st) == [oracle.gate_status(ref_m, m) for m in cands], (ref_m, cands)
