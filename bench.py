@@ -16,11 +16,13 @@ The JSON line also carries the roofline of the screening kernel (HIP events
 on the launch stream around each launch inside the timed region; the
 algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
 read of every candidate and the reference once), the CPU oracle timed on a
-bounded sample of the same workload, the generator's throughput, and two
-optional passes over the same candidates: the position search
-(kb_screen_locate) and the fail-fast screen (KB_FAIL_FAST), whose kernel
-time and share of candidate elements read are reported beside the full
-screen's.
+bounded sample of the same workload, the generator's throughput, two
+optional passes over the same candidates (the position search,
+kb_screen_locate, and the fail-fast screen, KB_FAIL_FAST, whose kernel time
+and share of candidate elements read are reported beside the full
+screen's), a multi-output screen (kb_screen_multi) of attention-style
+output pairs, and the rung statistics and promotion decision
+(kb_rung_stats, kb_rung_promote) over synthetic timing samples.
 
 roofline.traffic is the kernel's HBM traffic per launch from hardware
 counters (FETCH_SIZE and WRITE_SIZE, each scaled by the reading of the same
@@ -171,6 +173,40 @@ def gen_throughput(dev, kb, n, dtype):
                      "GB_per_s_written": round(n * out.element_size() / ms / 1e6, 1)}
     del out
     return res
+
+
+def multi_output_leg(dev, kb, K=16):
+    """kb_screen_multi on an attention-style output pair: out bf16
+    [4, 32, 2048, 128] and lse fp32 [4, 32, 2048], K candidates (in-tolerance
+    noise on both outputs).  Kernel time over both outputs and the
+    algorithmic GB/s ((K + 1) x the bytes of one output tuple)."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(3)
+    out = torch.randn(4, 32, 2048, 128, generator=g, device=dev).to(torch.bfloat16)
+    lse = torch.randn(4, 32, 2048, generator=g, device=dev) + 8.0
+    refs = [out, lse]
+    cands = []
+    for k in range(K):
+        gk = torch.Generator(device=dev).manual_seed(100 + k)
+        cands.append([(out.float() * (1 + 1e-3 * torch.randn(out.shape, generator=gk, device=dev)))
+                      .to(torch.bfloat16),
+                      lse + 1e-6 * torch.randn(lse.shape, generator=gk, device=dev)])
+    d_stats, ws = kb.kb_screen_multi(refs, cands, [1e-2, 1e-4], [1e-2, 1e-4])
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kb.kb_screen_multi(refs, cands, [1e-2, 1e-4], [1e-2, 1e-4], workspace=ws, d_stats=d_stats)
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    m = sorted(ms)[len(ms) // 2]
+    tup = out.numel() * 2 + lse.numel() * 4
+    recs, _ = kb.kb_screen_stats(d_stats, 2 * K)
+    return {"outputs": ["bf16 [4,32,2048,128]", "f32 [4,32,2048]"], "K": K, "ms": round(m, 4),
+            "algorithmic_GB_per_s": round((K + 1) * tup / (m * 1e-3) / 1e9, 1),
+            "n_passed": sum(1 for k in range(K) if recs[k]["passed"] and recs[K + k]["passed"])}
 
 
 def rung_stats_leg(dev, kb, synth, C=1024, S=3, N=60):
@@ -361,6 +397,8 @@ def main():
                         "n_failed": sum(r["mismatches"] > 0 for r in frec)}
     # the rung benchmarker's statistics (kb_rung_stats) over synthetic timing
     # samples (the CPU-baseline leg compares them with the oracle)
+    log("multi-output")
+    out["multi_output"] = multi_output_leg(dev, kb)
     log("rung statistics")
     out["rung_stats"], rung_data = rung_stats_leg(dev, kb, synth)
     if not args.no_stream_context:

@@ -285,6 +285,46 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
                      float rtol, uint32_t flags, const kb_stats* stats, kb_locate* d_loc,
                      hipStream_t stream);
 
+/* ---------------------------------------------------------- multi-output -- */
+
+/* Most outputs per candidate kb_screen_multi takes. */
+#define KB_MAX_OUTPUTS 64
+
+/* Bytes of device workspace kb_screen_multi needs (0 on invalid arguments):
+ * the sum, over outputs, of kb_screen_workspace_bytes for that output's
+ * reference, each rounded up to 256.  Initialise it with
+ * kb_screen_workspace_init (same contract as for kb_screen). */
+size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int n_cands);
+
+/* Screen candidates whose output is a tuple of n_outputs tensors against a
+ * tuple of references (a kernel returning several tensors: the
+ * correctness indicator K(p) of Section 3.1 then needs all of them, and the
+ * policy check of Section 3.2 covers each output's shape and dtype).
+ *   refs        host array of n_outputs reference descriptors (as for
+ *               kb_screen; outputs may differ in dtype and shape);
+ *   cands       host array [n_cands][n_outputs] of descriptors, candidate-
+ *               major;
+ *   atol, rtol  host arrays of n_outputs tolerances;
+ *   flags       as for kb_screen, applied to every output;
+ *   d_stats     n_outputs * n_cands records, output-major: output o of
+ *               candidate k at d_stats[o * n_cands + k].
+ * One gate over all outputs: candidate k is accepted only if every output
+ * passes kb_policy_check against its reference; otherwise no output of it
+ * is read and every one of its records has status = the first failing check
+ * of the first failing output (in output order).  Accepted candidates get
+ * the kb_screen record of each output.  The outputs are screened one after
+ * another on `stream`.  Errors (nothing launched) as for kb_screen. */
+int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands, int n_cands,
+                    const float* atol, const float* rtol, uint32_t flags, void* workspace,
+                    size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream);
+
+/* Verdict over multi-output records in host memory (output-major, as
+ * kb_screen_multi writes them): a candidate passes iff every output has
+ * status OK and no mismatch; it counts as rejected if any output was
+ * rejected, else as failed.  passed: optional host array of n_cands flags. */
+int kb_summarize_multi(const kb_stats* h_stats, int n_outputs, int n_cands, kb_summary* summary,
+                       int32_t* passed);
+
 /* ------------------------------------------------------------------ rung -- */
 
 /* Longest row of timing samples kb_rung_stats takes. */

@@ -112,8 +112,8 @@ assert ctypes.sizeof(KbTensor) == 144
 
 EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
            "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
-           "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_last_error",
-           "kb_version")
+           "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_screen_multi",
+           "kb_screen_multi_workspace_bytes", "kb_summarize_multi", "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -154,6 +154,15 @@ def lib():
         L.kb_rung_promote.restype = i32
         L.kb_rung_survival.argtypes = [vp, vp, vp, i32, i32, vp, vp]
         L.kb_rung_survival.restype = i32
+        L.kb_screen_multi_workspace_bytes.argtypes = [ctypes.POINTER(KbTensor), i32, i32]
+        L.kb_screen_multi_workspace_bytes.restype = ctypes.c_size_t
+        L.kb_screen_multi.argtypes = [ctypes.POINTER(KbTensor), i32, ctypes.POINTER(KbTensor), i32,
+                                      ctypes.POINTER(f32), ctypes.POINTER(f32), u32, vp,
+                                      ctypes.c_size_t, vp, vp]
+        L.kb_screen_multi.restype = i32
+        L.kb_summarize_multi.argtypes = [ctypes.POINTER(KbStats), i32, i32, ctypes.POINTER(KbSummary),
+                                         ctypes.POINTER(ctypes.c_int32)]
+        L.kb_summarize_multi.restype = i32
         L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
         L.kb_gen_inputs.restype = i32
         L.kb_last_error.argtypes = []
@@ -389,6 +398,54 @@ def kb_rung_survival(entering, failed, promoted, original):
     pp = (ctypes.c_double * max(1, n))()
     _check(lib().kb_rung_survival(arr(entering), arr(failed), arr(promoted), n, int(original), fp, pp))
     return list(fp)[:n], list(pp)[:n]
+
+
+MAX_OUTPUTS = 64
+
+
+def kb_screen_multi(refs, cands, atol, rtol, flags=0, workspace=None, d_stats=None, stream=None):
+    """Enqueue the screen of multi-output candidates.  refs: list of
+    n_outputs reference tensors; cands: list of n_cands lists of n_outputs
+    tensors (or None); atol, rtol: per-output lists (or one value for all).
+    Returns (d_stats, workspace); the records are output-major."""
+    torch = _torch()
+    n_out, n = len(refs), len(cands)
+    if isinstance(atol, (int, float)):
+        atol = [atol] * n_out
+    if isinstance(rtol, (int, float)):
+        rtol = [rtol] * n_out
+    R = (KbTensor * max(1, n_out))(*[describe(r) for r in refs])
+    C = (KbTensor * max(1, n * n_out))(*[describe(c) for row in cands for c in row])
+    if workspace is None:
+        nbytes = lib().kb_screen_multi_workspace_bytes(R, n_out, max(1, n))
+        if nbytes == 0:
+            raise KbError(KB_ERR_INVALID_ARG, "no multi-output workspace size for these arguments")
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=refs[0].device)
+        kb_screen_workspace_init(workspace, stream)
+    if d_stats is None:
+        d_stats = alloc_stats(max(1, n * n_out), refs[0].device)
+    A = (ctypes.c_float * max(1, n_out))(*[float(x) for x in atol])
+    T = (ctypes.c_float * max(1, n_out))(*[float(x) for x in rtol])
+    _check(lib().kb_screen_multi(R, n_out, C, n, A, T, int(flags),
+                                 ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                 ctypes.c_void_p(d_stats.data_ptr()), _stream_handle(stream)))
+    return d_stats, workspace
+
+
+def screen_multi(refs, cands, atol, rtol, flags=0, stream=None):
+    """Gate + screen + readback of multi-output candidates: (records[o][k]
+    dicts, summary dict, passed list)."""
+    n_out, n = len(refs), len(cands)
+    d_stats, _ = kb_screen_multi(refs, cands, atol, rtol, flags, stream=stream)
+    recs, _ = kb_screen_stats(d_stats, n * n_out, stream=stream)
+    host = (KbStats * max(1, n * n_out))()
+    for i, r in enumerate(recs):
+        for name, _ in KbStats._fields_:
+            setattr(host[i], name, r[name])
+    summ = KbSummary()
+    passed = (ctypes.c_int32 * max(1, n))()
+    _check(lib().kb_summarize_multi(host, n_out, n, ctypes.byref(summ), passed))
+    return ([recs[o * n:(o + 1) * n] for o in range(n_out)], summ.as_dict(), list(passed)[:n])
 
 
 def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):

@@ -284,6 +284,106 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
 
 }  // namespace kb
 
+namespace kb {
+
+// The screen of n_cands candidates whose gate statuses are already known
+// (status[k] == KB_STATUS_OK: read and compared; otherwise a record of
+// that status, not read).  Shared by kb_screen and kb_screen_multi; `who`
+// names the caller in error messages.  The caller has validated ref,
+// cands, n_cands, atol, rtol and flags.
+int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* cands, int n_cands,
+                       const int32_t* status, float atol, float rtol, uint32_t flags, void* workspace,
+                       size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream) {
+    int rc = KB_OK;
+    const bool fail_fast = (flags & KB_FAIL_FAST) != 0;
+    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "reference is not contiguous");
+    const uint64_t numel = tensor_numel(*ref);
+    const int dtype = ref->dtype;
+    int n_acc = 0;
+    for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
+
+    ScreenPlan P;
+    if (!make_plan(n_cands, n_acc, numel, dtype,
+                   resident_blocks(dtype, plan_group_size(n_cands, dtype), fail_fast), fail_fast, &P))
+        return fail(KB_ERR_INVALID_ARG, "%s: no launch plan (numel=%llu)", who,
+                    (unsigned long long)numel);
+    if (workspace == nullptr || workspace_bytes < P.total)
+        return fail(KB_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who,
+                    workspace_bytes, P.total);
+    if (!aligned16(ref->data) || !aligned16(workspace) || !aligned16(d_stats))
+        return fail(KB_ERR_ALIGNMENT, "%s: reference, workspace or d_stats not 16-byte aligned", who);
+    for (int k = 0; k < n_cands; ++k)
+        if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
+            return fail(KB_ERR_ALIGNMENT, "%s: candidate %d data not 16-byte aligned", who, k);
+
+    // Launch table: accepted candidates in call order padded to whole groups
+    // (padding points at the reference and writes no record), then rejected
+    // ones.  Up to kInlineCands entries travel in the kernel arguments; a
+    // larger table is uploaded to the workspace through the pinned staging
+    // ring.
+    const int n_groups = P.n_groups;
+    const int rej_start = n_groups * P.kg;
+    const int n_table = rej_start + (n_cands - n_acc);
+    const bool table_inline = n_table <= kInlineCands;
+    InlineTable tab;
+    auto fill = [&](CandEntry* t) {
+        int w = 0;
+        for (int k = 0; k < n_cands; ++k)
+            if (status[k] == KB_STATUS_OK) t[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
+        while (w < rej_start) t[w++] = CandEntry{ref->data, -1, KB_STATUS_OK};
+        for (int k = 0; k < n_cands; ++k)
+            if (status[k] != KB_STATUS_OK) t[w++] = CandEntry{nullptr, k, status[k]};
+    };
+    char* ws = (char*)workspace;
+    const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
+    if (table_inline) {
+        fill(tab.e);
+    } else {
+        rc = staging().upload(
+            (size_t)n_table * sizeof(CandEntry), [&](void* host) { fill((CandEntry*)host); },
+            ws + P.off_table, stream);
+        if (rc != KB_OK) return rc;
+    }
+    hipError_t e;
+    if (n_acc == 0 || numel == 0) {
+        e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, stream);
+        if (e != hipSuccess) return fail_hip(e, (std::string(who) + ": records launch").c_str());
+        return KB_OK;
+    }
+    ScreenParams p{};
+    p.ref = ref->data;
+    p.table = d_table;
+    p.numel = numel;
+    p.n_vec = P.n_vec;
+    p.atol = atol;
+    p.rtol = rtol;
+    p.flags = flags;
+    p.n_acc = n_acc;
+    p.n_cands = n_cands;
+    p.n_table = n_table;
+    p.rej_start = rej_start;
+    p.table_inline = table_inline ? 1 : 0;
+    p.n_groups = P.n_groups;
+    p.blocks_per_group = P.blocks_per_group;
+    p.n_super = P.n_super;
+    p.ff_round = P.ff_round;
+    p.tickets1 = (uint32_t*)(ws + P.off_tickets1);
+    p.tickets2 = (uint32_t*)(ws + P.off_tickets2);
+    p.ff_flags = (uint32_t*)(ws + P.off_ff_flags);
+    p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
+    p.part_ssd = (double*)(ws + P.off_part_ssd);
+    p.part_ssr = (double*)(ws + P.off_part_ssr);
+    p.part_ssrc = (double*)(ws + P.off_part_ssrc);
+    p.part2 = (Part2*)(ws + P.off_part2);
+    p.part2_ssr = (double*)(ws + P.off_part2_ssr);
+    p.stats = d_stats;
+    e = launch_screen(P, p, tab, fail_fast, stream);
+    if (e != hipSuccess) return fail_hip(e, (std::string(who) + ": kernel launch").c_str());
+    return KB_OK;
+}
+
+}  // namespace kb
+
 using namespace kb;
 
 extern "C" {
@@ -339,93 +439,119 @@ int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float a
         return fail(KB_ERR_INVALID_ARG, "kb_screen: atol and rtol must be finite and >= 0");
     if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
         return fail(KB_ERR_INVALID_ARG, "kb_screen: unknown flags 0x%x", flags);
-    const bool fail_fast = (flags & KB_FAIL_FAST) != 0;
     std::vector<int32_t> status((size_t)n_cands);
     int rc = kb_policy_check(ref, cands, n_cands, status.data());
     if (rc != KB_OK) return rc;
-    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "reference is not contiguous");
-    const uint64_t numel = tensor_numel(*ref);
-    const int dtype = ref->dtype;
-    int n_acc = 0;
-    for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
+    return screen_with_status("kb_screen", ref, cands, n_cands, status.data(), atol, rtol, flags,
+                              workspace, workspace_bytes, d_stats, stream);
+}
 
-    ScreenPlan P;
-    if (!make_plan(n_cands, n_acc, numel, dtype,
-                   resident_blocks(dtype, plan_group_size(n_cands, dtype), fail_fast), fail_fast, &P))
-        return fail(KB_ERR_INVALID_ARG, "kb_screen: no launch plan (numel=%llu)",
-                    (unsigned long long)numel);
-    if (workspace == nullptr || workspace_bytes < P.total)
-        return fail(KB_ERR_WORKSPACE, "kb_screen: workspace of %zu bytes, %zu needed",
-                    workspace_bytes, P.total);
-    if (!aligned16(ref->data) || !aligned16(workspace) || !aligned16(d_stats))
-        return fail(KB_ERR_ALIGNMENT, "kb_screen: reference, workspace or d_stats not 16-byte aligned");
-    for (int k = 0; k < n_cands; ++k)
-        if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
-            return fail(KB_ERR_ALIGNMENT, "kb_screen: candidate %d data not 16-byte aligned", k);
+// Multi-output candidates: the workspace of output o starts at the sum of
+// the 256-byte-aligned single-output sizes of outputs 0..o-1.
+static bool multi_layout(const kb_tensor* refs, int n_outputs, int n_cands, size_t* offsets,
+                         size_t* total) {
+    size_t off = 0;
+    for (int o = 0; o < n_outputs; ++o) {
+        if (!shape_valid(refs[o]) || !is_float_dtype(refs[o].dtype)) return false;
+        const size_t b = kb_screen_workspace_bytes(n_cands, tensor_numel(refs[o]), refs[o].dtype);
+        if (b == 0) return false;
+        if (offsets) offsets[o] = off;
+        off += align_up(b, 256);
+    }
+    *total = off;
+    return true;
+}
 
-    // Launch table: accepted candidates in call order padded to whole groups
-    // (padding points at the reference and writes no record), then rejected
-    // ones.  Up to kInlineCands entries travel in the kernel arguments; a
-    // larger table is uploaded to the workspace through the pinned staging
-    // ring.
-    const int n_groups = P.n_groups;
-    const int rej_start = n_groups * P.kg;
-    const int n_table = rej_start + (n_cands - n_acc);
-    const bool table_inline = n_table <= kInlineCands;
-    InlineTable tab;
-    auto fill = [&](CandEntry* t) {
-        int w = 0;
+size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int n_cands) {
+    if (refs == nullptr || n_outputs < 1 || n_outputs > KB_MAX_OUTPUTS || n_cands < 1) return 0;
+    size_t total = 0;
+    return multi_layout(refs, n_outputs, n_cands, nullptr, &total) ? total : 0;
+}
+
+int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands, int n_cands,
+                    const float* atol, const float* rtol, uint32_t flags, void* workspace,
+                    size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream) {
+    clear_error();
+    if (refs == nullptr || cands == nullptr || atol == nullptr || rtol == nullptr || d_stats == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: null refs, cands, atol, rtol or d_stats");
+    if (n_outputs < 1 || n_outputs > KB_MAX_OUTPUTS || n_cands < 1)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: n_outputs = %d or n_cands = %d out of range",
+                    n_outputs, n_cands);
+    for (int o = 0; o < n_outputs; ++o)
+        if (!std::isfinite(atol[o]) || !std::isfinite(rtol[o]) || atol[o] < 0.f || rtol[o] < 0.f)
+            return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: atol/rtol of output %d not finite and >= 0",
+                        o);
+    if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: unknown flags 0x%x", flags);
+    // One gate over all outputs: a candidate is accepted only if every output
+    // passes; otherwise every output's record carries the first failing
+    // check, in output order.
+    std::vector<int32_t> combined((size_t)n_cands, KB_STATUS_OK), st((size_t)n_cands);
+    std::vector<kb_tensor> col((size_t)n_cands);
+    for (int o = 0; o < n_outputs; ++o) {
+        for (int k = 0; k < n_cands; ++k) col[k] = cands[(size_t)k * n_outputs + o];
+        const int rc = kb_policy_check(&refs[o], col.data(), n_cands, st.data());
+        if (rc != KB_OK) return fail(rc, "kb_screen_multi: reference %d: %s", o, g_error.c_str());
+        if (!is_contiguous(refs[o]))
+            return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: reference %d is not contiguous", o);
         for (int k = 0; k < n_cands; ++k)
-            if (status[k] == KB_STATUS_OK) t[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
-        while (w < rej_start) t[w++] = CandEntry{ref->data, -1, KB_STATUS_OK};
+            if (combined[k] == KB_STATUS_OK) combined[k] = st[k];
+    }
+    std::vector<size_t> offs((size_t)n_outputs);
+    size_t total = 0;
+    if (!multi_layout(refs, n_outputs, n_cands, offs.data(), &total))
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: no workspace layout");
+    if (workspace == nullptr || workspace_bytes < total)
+        return fail(KB_ERR_WORKSPACE, "kb_screen_multi: workspace of %zu bytes, %zu needed",
+                    workspace_bytes, total);
+    // Validate every output before launching anything.
+    if (!aligned16(workspace) || !aligned16(d_stats))
+        return fail(KB_ERR_ALIGNMENT, "kb_screen_multi: workspace or d_stats not 16-byte aligned");
+    for (int o = 0; o < n_outputs; ++o) {
+        if (!aligned16(refs[o].data))
+            return fail(KB_ERR_ALIGNMENT, "kb_screen_multi: reference %d not 16-byte aligned", o);
         for (int k = 0; k < n_cands; ++k)
-            if (status[k] != KB_STATUS_OK) t[w++] = CandEntry{nullptr, k, status[k]};
-    };
+            if (combined[k] == KB_STATUS_OK && !aligned16(cands[(size_t)k * n_outputs + o].data))
+                return fail(KB_ERR_ALIGNMENT, "kb_screen_multi: candidate %d output %d not 16-byte aligned",
+                            k, o);
+    }
     char* ws = (char*)workspace;
-    const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
-    if (table_inline) {
-        fill(tab.e);
-    } else {
-        rc = staging().upload(
-            (size_t)n_table * sizeof(CandEntry), [&](void* host) { fill((CandEntry*)host); },
-            ws + P.off_table, stream);
+    for (int o = 0; o < n_outputs; ++o) {
+        for (int k = 0; k < n_cands; ++k) col[k] = cands[(size_t)k * n_outputs + o];
+        const size_t bytes = (o + 1 < n_outputs ? offs[o + 1] : total) - offs[o];
+        const int rc = screen_with_status("kb_screen_multi", &refs[o], col.data(), n_cands, combined.data(),
+                                          atol[o], rtol[o], flags, ws + offs[o], bytes,
+                                          d_stats + (size_t)o * n_cands, stream);
         if (rc != KB_OK) return rc;
     }
-    hipError_t e;
-    if (n_acc == 0 || numel == 0) {
-        e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, stream);
-        if (e != hipSuccess) return fail_hip(e, "kb_screen: records launch");
-        return KB_OK;
+    return KB_OK;
+}
+
+int kb_summarize_multi(const kb_stats* h_stats, int n_outputs, int n_cands, kb_summary* summary,
+                       int32_t* passed) {
+    clear_error();
+    if (h_stats == nullptr || summary == nullptr || n_outputs < 1 || n_cands < 0)
+        return fail(KB_ERR_INVALID_ARG, "kb_summarize_multi: null argument or bad count");
+    kb_summary s{n_cands, 0, 0, 0, -1, -1};
+    for (int k = 0; k < n_cands; ++k) {
+        bool rejected = false, failed = false;
+        for (int o = 0; o < n_outputs; ++o) {
+            const kb_stats& st = h_stats[(size_t)o * n_cands + k];
+            if (st.status != KB_STATUS_OK) rejected = true;
+            else if (st.mismatches != 0) failed = true;
+        }
+        const bool ok = !rejected && !failed;
+        if (passed) passed[k] = ok ? 1 : 0;
+        if (ok) {
+            s.n_passed++;
+            if (s.first_passed < 0) s.first_passed = k;
+            continue;
+        }
+        if (rejected) s.n_rejected++;
+        else s.n_failed++;
+        if (s.first_failed < 0) s.first_failed = k;
     }
-    ScreenParams p{};
-    p.ref = ref->data;
-    p.table = d_table;
-    p.numel = numel;
-    p.n_vec = P.n_vec;
-    p.atol = atol;
-    p.rtol = rtol;
-    p.flags = flags;
-    p.n_acc = n_acc;
-    p.n_cands = n_cands;
-    p.n_table = n_table;
-    p.rej_start = rej_start;
-    p.table_inline = table_inline ? 1 : 0;
-    p.n_groups = P.n_groups;
-    p.blocks_per_group = P.blocks_per_group;
-    p.n_super = P.n_super;
-    p.ff_round = P.ff_round;
-    p.tickets1 = (uint32_t*)(ws + P.off_tickets1);
-    p.tickets2 = (uint32_t*)(ws + P.off_tickets2);
-    p.ff_flags = (uint32_t*)(ws + P.off_ff_flags);
-    p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
-    p.part_ssd = (double*)(ws + P.off_part_ssd);
-    p.part_ssr = (double*)(ws + P.off_part_ssr);
-    p.part_ssrc = (double*)(ws + P.off_part_ssrc);
-    p.part2 = (Part2*)(ws + P.off_part2);
-    p.part2_ssr = (double*)(ws + P.off_part2_ssr);
-    p.stats = d_stats;
-    e = launch_screen(P, p, tab, fail_fast, stream);
-    if (e != hipSuccess) return fail_hip(e, "kb_screen: kernel launch");
+    *summary = s;
     return KB_OK;
 }
 

@@ -217,12 +217,18 @@ __global__ __launch_bounds__(kThreads) void scores_kernel(RungParams p, kb_sampl
 // The promotion decision D (Section 3.4): rank by score, ties to the lower
 // index, and promote the first ceil(n_eligible num / den) valid non-baseline
 // candidates plus a valid baseline.  Ranking is by counting: candidate i's
-// rank is the number of candidates that come before it, so one thread per
-// candidate scans every key (staged through LDS in tiles of the work-group
-// size) and no sort or atomic is needed; the ranks are a permutation, and
-// `order` is their inverse.
+// rank is the number of candidates that come before it.  One wave per
+// candidate: its lanes split the scan over all keys (read from L2), and a
+// butterfly sums their counts; no sort or atomic is needed, the ranks are a
+// permutation, and `order` is their inverse.
 __device__ __forceinline__ double rank_key(const kb_rung_score& s) {
     return s.valid != 0 && s.score == s.score ? s.score : -__builtin_inf();
+}
+
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+    return v;
 }
 
 __global__ __launch_bounds__(kThreads) void promote_kernel(const kb_rung_score* __restrict__ scores,
@@ -230,32 +236,25 @@ __global__ __launch_bounds__(kThreads) void promote_kernel(const kb_rung_score* 
                                                             int32_t* __restrict__ rank,
                                                             int32_t* __restrict__ order,
                                                             int32_t* __restrict__ promoted) {
-    __shared__ double s_key[kThreads];
-    __shared__ uint8_t s_elig[kThreads];
-    const int i = blockIdx.x * kThreads + threadIdx.x;
-    const bool me = i < n;
-    const double ki = me ? rank_key(scores[i]) : 0.0;
-    const bool valid_i = me && scores[i].valid != 0;
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (i >= n) return;  // whole waves
+    const double ki = rank_key(scores[i]);
+    const bool valid_i = scores[i].valid != 0;
     int before = 0, before_elig = 0, n_elig = 0;
-    for (int t0 = 0; t0 < n; t0 += kThreads) {
-        const int j = t0 + threadIdx.x;
-        if (j < n) {
-            s_key[threadIdx.x] = rank_key(scores[j]);
-            s_elig[threadIdx.x] = scores[j].valid != 0 && j != base;
-        }
-        __syncthreads();
-        const int m = min(kThreads, n - t0);
-        for (int u = 0; u < m; ++u) {
-            const int j2 = t0 + u;
-            const double kj = s_key[u];
-            const bool b = kj > ki || (kj == ki && j2 < i);
-            before += b;
-            before_elig += b && s_elig[u];
-            n_elig += s_elig[u];
-        }
-        __syncthreads();
+    for (int j = lane; j < n; j += 64) {
+        const kb_rung_score sj = scores[j];
+        const double kj = rank_key(sj);
+        const bool elig = sj.valid != 0 && j != base;
+        const bool b = kj > ki || (kj == ki && j < i);
+        before += b;
+        before_elig += b && elig;
+        n_elig += elig;
     }
-    if (!me) return;
+    before = wave_sum_i32(before);
+    before_elig = wave_sum_i32(before_elig);
+    n_elig = wave_sum_i32(n_elig);
+    if (lane != 0) return;
     const long long keep = ((long long)n_elig * num + den - 1) / den;
     rank[i] = before;
     order[before] = i;
@@ -269,7 +268,8 @@ __global__ __launch_bounds__(kThreads) void promote_kernel(const kb_rung_score* 
 
 hipError_t launch_rung_promote(const kb_rung_score* scores, int n, int base, int num, int den,
                                int32_t* rank, int32_t* order, int32_t* promoted, hipStream_t stream) {
-    hipLaunchKernelGGL(promote_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
+    const int per_block = kThreads / 64;
+    hipLaunchKernelGGL(promote_kernel, dim3((n + per_block - 1) / per_block), dim3(kThreads), 0, stream,
                        scores, n, base, num, den, rank, order, promoted);
     return hipGetLastError();
 }
