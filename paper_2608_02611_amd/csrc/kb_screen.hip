@@ -213,7 +213,12 @@ __device__ __forceinline__ float rel_quotients(const float s[kE], const float r[
     float qm = 0.f;
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
-        const float d = fabsf(s[i]), a = fabsf(r[i]);
+        const float d = fabsf(s[i]);
+        float a = fabsf(r[i]);
+        // (opaque: the binary64 conversions stay in this rare path instead
+        // of being hoisted into every chunk, where they would hold 16
+        // registers across the candidate loop)
+        if constexpr (GUARD) opaque(a);
         const bool pass = GUARD ? __builtin_fma(-(double)O, (double)a, (double)d) > 0.0
                                 : fmaf(-O, a, d) > 0.f;
         if (pass) qm = fmaxf(qm, d / a);
@@ -460,7 +465,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         // the work-group's shared max-rel values
 #pragma unroll
         for (int j = 0; j < KG; ++j)
-            orel[j] = max(orel[j], __builtin_amdgcn_readfirstlane(s_rel[j]));
+            orel[j] = max(orel[j], (uint32_t)__builtin_amdgcn_readfirstlane(s_rel[j]));
 
         // Reference side, once per element for all KG candidates.
         float r[kE], tol[kE];
