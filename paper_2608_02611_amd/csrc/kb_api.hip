@@ -171,12 +171,12 @@ Staging& staging() {
 // Work-groups of the screening kernel for (dtype, kg) resident on the
 // current device at once; 0 if the device cannot be queried (then the plan
 // falls back to a fixed total).
-int resident_blocks(int dtype, int kg, bool fail_fast = false) {
+int resident_blocks(int dtype, int kg, bool fail_fast = false, bool wide = false) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
-    return cus * screen_blocks_per_cu(dtype, kg, fail_fast);
+    return cus * screen_blocks_per_cu(dtype, kg, fail_fast, wide);
 }
 int plan_group_size(int n_cands, int dtype) {
     // Measured on the five screening workloads: groups of 4 for fp32 and
@@ -303,8 +303,9 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
 
     ScreenPlan P;
-    if (!make_plan(n_cands, n_acc, numel, dtype,
-                   resident_blocks(dtype, plan_group_size(n_cands, dtype), fail_fast), fail_fast, &P))
+    const int kg = plan_group_size(n_cands, dtype);
+    const bool wide = use_wide_kernel(dtype, kg, fail_fast, numel);
+    if (!make_plan(n_cands, n_acc, numel, dtype, resident_blocks(dtype, kg, fail_fast, wide), fail_fast, &P))
         return fail(KB_ERR_INVALID_ARG, "%s: no launch plan (numel=%llu)", who,
                     (unsigned long long)numel);
     if (workspace == nullptr || workspace_bytes < P.total)
@@ -335,6 +336,7 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
             if (status[k] != KB_STATUS_OK) t[w++] = CandEntry{nullptr, k, status[k]};
     };
     char* ws = (char*)workspace;
+    P.wide = wide ? 1 : 0;
     const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
     if (table_inline) {
         fill(tab.e);
@@ -416,8 +418,9 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out) {
     if (out == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_screen_launch: out is NULL");
     if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "dtype %d not screenable", dtype);
     ScreenPlan P;
-    if (!make_plan(n_cands, n_cands, numel, dtype, resident_blocks(dtype, plan_group_size(n_cands, dtype)),
-                   false, &P))
+    const int kg = plan_group_size(n_cands, dtype);
+    if (!make_plan(n_cands, n_cands, numel, dtype,
+                   resident_blocks(dtype, kg, false, use_wide_kernel(dtype, kg, false, numel)), false, &P))
         return fail(KB_ERR_INVALID_ARG, "no launch plan for n_cands=%d numel=%llu", n_cands,
                     (unsigned long long)numel);
     out->group_size = P.kg;

@@ -49,6 +49,7 @@ struct ScreenPlan {
     uint64_t n_vec;       // full 16-byte vectors per tensor
     int n_super;          // ceil(blocks_per_group / 16): first-level combine groups
     int ff_round;         // fail-fast launch: candidate groups per round
+    int wide;             // launch the 5-waves-per-SIMD build (use_wide_kernel)
     // workspace byte offsets
     size_t off_tickets1, off_tickets2, off_ff_flags, off_table, off_part_u32, off_part_ssd,
         off_part_ssr, off_part_ssrc, off_part2, off_part2_ssr, total;
@@ -74,9 +75,20 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
 // Candidates per group the plan picks for n_cands candidates.
 int plan_group_size(int n_cands, int dtype);
 
-// Work-groups of the screening kernel for (dtype, kg, fail-fast) resident
-// per CU (occupancy query, cached), or 0 on failure.
-int screen_blocks_per_cu(int dtype, int kg, bool fail_fast);
+// Whether a plain launch takes the screening kernel built for 5 waves per
+// SIMD (fp32, 4 candidates per group, at least 2^22 elements).  fp32 at 4
+// candidates needs 99 VGPRs, which allocate as 104: 4 waves per SIMD.  Built
+// for 5 it fits 96 with a 16-byte spill.  Measured: 12% faster on 2^30 fp32
+// elements per tensor; 5% slower on 2^18 elements (1024 candidates), whose
+// 2048 work-groups make two whole rounds at 4 per CU but not at 5.
+constexpr uint64_t kWideMinNumel = 1ull << 22;
+inline bool use_wide_kernel(int dtype, int kg, bool fail_fast, uint64_t numel) {
+    return dtype == KB_F32 && kg == 4 && !fail_fast && numel >= kWideMinNumel;
+}
+
+// Work-groups of the screening kernel for (dtype, kg, fail-fast, wide)
+// resident per CU (occupancy query, cached), or 0 on failure.
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide = false);
 
 // Candidate groups per round of a fail-fast launch (see make_plan).
 constexpr int kFailFastRound = 2;

@@ -932,9 +932,12 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
 // round the work-groups of failed groups would idle while those of the live
 // ones did all their work.)  Fewer groups per round re-read the reference
 // once more per round; more groups per round balance less well.
-template <int DT, int KG, bool FF>
-__global__ __launch_bounds__(kThreads, min_waves(DT, KG)) void screen_kernel(ScreenParams p,
-                                                                            InlineTable tab) {
+// WIDE: the same kernel built for 5 waves per SIMD instead of 4 (only fp32
+// with 4 candidates per group, plain launches on large tensors; see
+// use_wide_kernel).
+template <int DT, int KG, bool FF, bool WIDE = false>
+__global__ __launch_bounds__(kThreads, WIDE ? 5 : min_waves(DT, KG)) void screen_kernel(
+    ScreenParams p, InlineTable tab) {
     int id = blockIdx.x, g0 = 0, R = p.n_groups;
     if constexpr (FF) {
         const int per_round = p.ff_round * p.blocks_per_group;
@@ -967,14 +970,21 @@ template <int DT, int KG, bool FF>
 hipError_t launch_kg(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
                      hipStream_t stream) {
     const unsigned grid = (unsigned)plan.n_groups * (unsigned)plan.blocks_per_group;
+    if constexpr (DT == DT_F32 && KG == 4 && !FF) {
+        if (plan.wide) {
+            hipLaunchKernelGGL((screen_kernel<DT, KG, FF, true>), dim3(grid), dim3(kThreads), 0, stream,
+                               p, tab);
+            return hipGetLastError();
+        }
+    }
     hipLaunchKernelGGL((screen_kernel<DT, KG, FF>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
     return hipGetLastError();
 }
 
-template <int DT, int KG, bool FF>
+template <int DT, int KG, bool FF, bool WIDE = false>
 int occupancy_kg() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG, FF>, kThreads, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG, FF, WIDE>, kThreads, 0) !=
         hipSuccess)
         return 0;
     return n;
@@ -1042,15 +1052,17 @@ hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream) {
     return hipGetLastError();
 }
 
-int screen_blocks_per_cu(int dtype, int kg, bool fail_fast) {
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide) {
     // The occupancy of a kernel does not change during the process.
-    static int cache[2][3][5] = {};  // value + 1, 0 = not queried yet
+    static int cache[3][3][5] = {};  // value + 1, 0 = not queried yet
     const int ki = kg == 1 ? 0 : kg == 2 ? 1 : kg == 4 ? 2 : kg == 8 ? 3 : 4;
     const int di = dtype == DT_F32 ? 0 : dtype == DT_F16 ? 1 : 2;
-    int* slot = &cache[fail_fast ? 1 : 0][di][ki];
+    wide = wide && use_wide_kernel(dtype, kg, fail_fast, ~0ull);
+    int* slot = &cache[fail_fast ? 1 : wide ? 2 : 0][di][ki];
     int v = __atomic_load_n(slot, __ATOMIC_RELAXED) - 1;
     if (v < 0) {
-        v = fail_fast ? occupancy<true>(dtype, kg) : occupancy<false>(dtype, kg);
+        v = wide ? occupancy_kg<DT_F32, 4, false, true>()
+                 : fail_fast ? occupancy<true>(dtype, kg) : occupancy<false>(dtype, kg);
         __atomic_store_n(slot, v + 1, __ATOMIC_RELAXED);
     }
     return v;
