@@ -11,9 +11,14 @@
 // A wave scans its chunks in increasing index order and stops looking for a
 // position as soon as one of its lanes has found it: every later chunk of
 // the wave holds larger indices.  On a failing candidate the first mismatch
-// is usually in a wave's first chunk, so most of the pass is skipped.  The
-// per-lane first hits are reduced to a wave minimum (DPP) and merged into the
-// output with a 64-bit atomic minimum; "none" is all-ones, which reads as -1.
+// is usually in a wave's first chunk, so most of the pass is skipped.  Per
+// element only the three predicates are evaluated, into 8-bit lane masks;
+// an index is formed only for a chunk whose ballot shows a hit (the lane's
+// lowest set bit, then a wave minimum by DPP), and the wave's finds are
+// merged into the output with a 64-bit atomic minimum ("none" is all-ones,
+// which reads as -1).  Work-group ids are mapped like the screen's, so that
+// the candidates of one stripe run on one XCD and share the reference stripe
+// in its L2.
 #include "kb_device.hpp"
 #include "kb_internal.hpp"
 
@@ -79,6 +84,21 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) { return ~wave_max_u32(~v); }
+
+// The smallest in-chunk index among the elements of this lane whose bit is
+// set in m (bit i = element i of the lane), or all-ones if none.
+template <int DT>
+__device__ __forceinline__ uint32_t first_in_lane(uint32_t m, int lane) {
+    if (m == 0u) return ~0u;
+    if constexpr (DT == DT_F32) {
+        // elements 0..3 are 4l..4l+3, elements 4..7 are 256+4l..256+4l+3
+        return (m & 0xFu) ? 4u * lane + __builtin_ctz(m) : 256u + 4u * lane + __builtin_ctz(m >> 4);
+    } else {
+        return 8u * lane + __builtin_ctz(m);
+    }
+}
+
 // The three predicates of one element (the definitions of the screening
 // statistics, element by element).
 struct Hit {
@@ -114,8 +134,10 @@ template <int DT>
 __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTable tab) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int k = blockIdx.x % p.n;
-    const int stripe = blockIdx.x / p.n;
+    const int xcd = blockIdx.x & 7;  // p.stripes is a multiple of 8
+    const int slot = blockIdx.x >> 3;
+    const int k = slot % p.n;
+    const int stripe = (slot / p.n) * 8 + xcd;
     const void* cand = tab.e[k].data;
     const int index = tab.e[k].index;
     const float max_abs = p.stats[index].max_abs_err;
@@ -124,6 +146,7 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
     const bool want_rel = max_rel > 0.f;
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
 
+    // the wave's finds (wave-uniform), all-ones until found
     uint64_t f_mism = kNone, f_abs = kNone, f_rel = kNone;
     bool need_mism = true, need_abs = want_abs, need_rel = want_rel;
     const uint64_t n_chunks = p.numel / kChunk;
@@ -132,20 +155,29 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
          chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += wstride) {
         const LaneChunk<DT> rc = load_lane<DT>(p.ref, chunk, lane);
         const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, lane);
-        const uint64_t base = chunk * kChunk;
+        uint32_t mm = 0u, ma = 0u, mr = 0u;  // bit i: element i of this lane qualifies
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
             const Hit h = classify(widen_bits<DT>(cc.bits(i)), widen_bits<DT>(rc.bits(i)), p.atol, p.rtol,
                                    equal_nan, max_abs, max_rel, need_abs, need_rel);
-            const uint64_t idx = base + LaneChunk<DT>::offset(lane, i);
-            if (need_mism && h.mism && f_mism == kNone) f_mism = idx;
-            if (h.abs && f_abs == kNone) f_abs = idx;
-            if (h.rel && f_rel == kNone) f_rel = idx;
+            mm |= (uint32_t)h.mism << i;
+            ma |= (uint32_t)h.abs << i;
+            mr |= (uint32_t)h.rel << i;
         }
         // a position found anywhere in this chunk is below everything later
-        if (need_mism && ballot(f_mism != kNone)) need_mism = false;
-        if (need_abs && ballot(f_abs != kNone)) need_abs = false;
-        if (need_rel && ballot(f_rel != kNone)) need_rel = false;
+        const uint64_t base = chunk * kChunk;
+        if (need_mism && ballot(mm != 0u)) {
+            f_mism = base + wave_min_u32(first_in_lane<DT>(mm, lane));
+            need_mism = false;
+        }
+        if (need_abs && ballot(ma != 0u)) {
+            f_abs = base + wave_min_u32(first_in_lane<DT>(ma, lane));
+            need_abs = false;
+        }
+        if (need_rel && ballot(mr != 0u)) {
+            f_rel = base + wave_min_u32(first_in_lane<DT>(mr, lane));
+            need_rel = false;
+        }
     }
     // Ragged tail (numel mod 512 elements): stripe 0, one element per thread.
     if (stripe == 0) {
