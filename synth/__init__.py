@@ -6,14 +6,22 @@ they will be screened on.  It holds none of the screening arithmetic and none
 of the library's generator; the parity tests hand the same bytes to the HIP
 library (on the GPU) and to the CPU oracle (after a copy to the host).
 
-Workloads (the five screening configurations; readings of their wording are
-listed in DESIGN.md):
+Workloads (the five screening configurations):
 
-  c1  K=4,    N=65,536 fp32,        atol=rtol=1e-5
-  c2  K=16,   4096x4096 bf16,       atol=rtol=1e-2
-  c3  K=1024, 256x1024 fp32,        atol=1e-6, rtol=1e-5
-  c4  K=64,   8x2048x4096 fp16,     atol=rtol=1e-3
-  c5  K=8,    2^30 fp32,            atol=1e-8, rtol=1e-6
+  c1  K=4,    N=65,536 fp32,        atol=rtol=1e-5: reference N(0,1); a copy,
+      a copy with U(+-1e-6) noise, one with 5 NaNs at drawn indices, one with
+      1% of its elements scaled by 1.01;
+  c2  K=16,   4096x4096 bf16,       atol=rtol=1e-2: reference bf16(64 z);
+      candidate k is bf16(r + r eps), eps ~ U(-s_k, s_k), s_k = 2^(-8 + 2k/15),
+      and candidates 0 and 1 also get a drawn 64x64 tile set to 0;
+  c3  K=1024, 256x1024 fp32,        atol=1e-6, rtol=1e-5: softmax rows of
+      2 z (binary64, rounded); candidate k adds s_k z, s_k log-spaced 1e-9..1e-3;
+  c4  K=64,   8x2048x4096 fp16,     atol=rtol=1e-3: reference fp16(z); by k mod
+      4: a copy, last-bit flips on 0.1% of elements, 64 infinities with the
+      sign of r, both;
+  c5  K=8,    2^30 fp32,            atol=1e-8, rtol=1e-6: Student-t (3) with
+      subnormals, signed zeros and infinities; per element with probability
+      1/2 a zero-sign flip, a subnormal flush or a 1e-7 relative change.
 
 Every workload also has a scaled form (`scale` < 1 shrinks N, keeping the
 recipe) for the oracle-sized parity cases.
