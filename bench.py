@@ -281,9 +281,9 @@ def main():
                     help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the screening path is built and measured on a single "
-              "MI355X (multi-GPU sharding is a design note, not part of this build); "
-              "run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the screening library runs on a single MI355X "
+              "(sharding over several GPUs is described, not implemented); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import __graft_entry__
