@@ -442,8 +442,30 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     const uint32_t off = 16u * (uint32_t)lane;
     const uint64_t n_chunks = p.numel / kChunk;
     const uint64_t wstride = (uint64_t)p.blocks_per_group * kWaves;
-    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave; chunk < n_chunks && (!FF || alive != 0u);
-         chunk += wstride) {
+    const uint64_t first = (uint64_t)stripe * kWaves + wave;
+    // Wave priority in stages (plain launch).  Every wave has the same number
+    // of chunks (within one), but the SIMD arbiter issues the oldest wave
+    // first among waves of equal priority, so on a full device the oldest
+    // work-groups of a CU ran ahead and the youngest ended their loops about
+    // 40% later (measured per work-group with the real-time clock): the
+    // device then spent the last fifth of the pass with ever fewer waves
+    // reading.  A wave therefore starts at priority 3 and drops one level
+    // after 1/2, 3/4 and 7/8 of its chunks.  A wave that runs ahead yields to
+    // every wave not yet as far, the waves regroup at each step, and the
+    // spread at the end is that of the last eighth only.  (Measured on the
+    // 16 x 4096^2 bf16, 1024 x 256 x 1024 fp32, 64 x 8 x 2048 x 4096 fp16 and
+    // 8 x 2^30 fp32 screens: 4.5%, 9%, 3.5% and 3.5% faster.)
+    const uint64_t n_mine = first < n_chunks ? (n_chunks - first + wstride - 1) / wstride : 0;
+    const uint64_t drop1 = n_mine / 2, drop2 = n_mine * 3 / 4, drop3 = n_mine * 7 / 8;
+    uint64_t n_seen = 0;
+    if constexpr (!FF) __builtin_amdgcn_s_setprio(3);
+    for (uint64_t chunk = first; chunk < n_chunks && (!FF || alive != 0u); chunk += wstride) {
+        if constexpr (!FF) {
+            if (n_seen == drop1) __builtin_amdgcn_s_setprio(2);
+            if (n_seen == drop2) __builtin_amdgcn_s_setprio(1);
+            if (n_seen == drop3) __builtin_amdgcn_s_setprio(0);
+            ++n_seen;
+        }
         const uint64_t cb = chunk * chunk_bytes<DT>();
         // Re-materialise the lane offset inside the loop so that instruction
         // selection sees (scalar base + zero-extended 32-bit offset) and
@@ -615,6 +637,8 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             }
         }
     }
+
+    if constexpr (!FF) __builtin_amdgcn_s_setprio(0);
 
     // Ragged tail: the last numel mod 512 elements, by stripe 0 of each
     // group, one element per thread, exact path (out-of-range lanes and
