@@ -6,11 +6,12 @@ outputs already resident in HBM: the policy gate, the screening kernel (one
 coalesced read of the reference and the K candidates, per-candidate
 statistics) and the readback of the K records with the pass/fail verdict.
 Steps are pipelined the way a screening service runs them: the kernel of
-step i writes its records straight into one of two pinned host buffers, and
-while it runs the host takes the verdict of step i-1 (after that step's
-event).  value = K * numel * element bytes / step time (GB/s).  A few fully
-synchronous steps (launch, copy back, wait) are timed too and reported as
-sync_step_ms.
+step i writes its records straight into one of 2 * BATCH pinned host
+buffers (a ring), one completion event follows every BATCH steps, and while
+the device works on the current batch the host takes the verdicts of the
+batch before it (after that batch's event).  value = K * numel * element
+bytes / step time (GB/s).  A few fully synchronous steps (launch, copy
+back, wait) are timed too and reported as sync_step_ms.
 
 Before the timed region the device runs about 0.2 s of back-to-back
 launches (untimed), so that the timed steps run at the sustained clock, and
@@ -18,10 +19,11 @@ the W warmup steps run the same pipelined loop as the timed ones.
 
 The JSON line also carries the roofline of the screening kernel.  Its
 duration is measured with a pair of HIP events on the launch stream around
-the timed region (the per-step completion events carry no timestamps): the
+the timed region (the completion events carry no timestamps): the
 launches follow each other on the device and it is never idle in that
-loop, so the interval divided by K is the kernel's time per launch,
-including the dispatch gap between kernels.  The
+loop, so the interval divided by the number of steps is the kernel's time
+per launch, including the dispatch gap between kernels and the share of
+the completion events.  The
 algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
 read of every candidate and the reference once.  Also: the CPU oracle timed on a
 bounded sample of the same workload, the generator's throughput, two
@@ -52,6 +54,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+# Steps per completion event of the pipelined loop: an event recorded
+# between two launches was measured to add about 3.3 us to that step (the
+# device's signal between kernels), so the host takes the verdicts in
+# batches of BATCH steps over a ring of 2 * BATCH pinned record slots.
+BATCH = 4
 METRIC = "candidate GB/s screened (K\u00d7N\u00d7dtype bytes/s) and % of MI355X HBM peak"
 KERNEL_SOURCES = ["paper_2608_02611_amd/csrc/kb_screen.hip", "paper_2608_02611_amd/csrc/kb_device.hpp",
                   "paper_2608_02611_amd/csrc/kb_internal.hpp"]
@@ -298,8 +305,37 @@ def main():
     w = synth.build(args.config, dev, seed=0)
     torch.cuda.synchronize()
     K, n, b = len(w.cands), w.numel, w.dtype_bytes
-    scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol, host_slots=2)
+    scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol, host_slots=2 * BATCH)
     plan = scr.launch_plan()
+
+    def pipelined(n, timing=None):
+        """n steps into the ring of 2 * BATCH pinned record slots; after
+        every BATCH steps one completion event, and the verdicts of the
+        batch before it (whose event has then been reached).  Returns the
+        summary of the last step."""
+        evs = []
+        summary = None
+
+        def take(b):
+            nonlocal summary
+            evs[b].synchronize()
+            for s in range(b * BATCH, min(n, (b + 1) * BATCH)):
+                summary = scr.summarize(s % (2 * BATCH))
+
+        if timing is not None:
+            timing[0].record()
+        for i in range(n):
+            scr.launch(i % (2 * BATCH))
+            if (i + 1) % BATCH == 0 or i == n - 1:
+                e = torch.cuda.Event()
+                e.record()
+                evs.append(e)
+                if len(evs) >= 2:
+                    take(len(evs) - 2)
+        if timing is not None:
+            timing[1].record()
+        take(len(evs) - 1)
+        return summary
 
     # Untimed: bring the device to its sustained clock (about 0.2 s of
     # back-to-back launches; a timed loop right after a short warmup was
@@ -309,35 +345,19 @@ def main():
     t_warm = time.perf_counter() + 0.2
     while time.perf_counter() < t_warm:
         for i in range(20):
-            scr.launch(i & 1)
+            scr.launch(i % (2 * BATCH))
         torch.cuda.synchronize()
     log("warmup", args.warmup)
-    warm = [torch.cuda.Event() for _ in range(max(1, args.warmup))]
-    for i in range(args.warmup):
-        scr.launch(i & 1)
-        warm[i].record()
-        if i > 0:
-            warm[i - 1].synchronize()
-            scr.summarize((i - 1) & 1)
+    if args.warmup > 0:
+        pipelined(args.warmup)
     torch.cuda.synchronize()
-    # per-step completion events (no timestamps); the kernel time comes from
-    # the timing pair around the whole timed region
+    # the kernel time comes from a timing pair around the whole timed region
     first = torch.cuda.Event(enable_timing=True)
     last = torch.cuda.Event(enable_timing=True)
-    ends = [torch.cuda.Event() for _ in range(args.steps)]
     log("timing", args.steps, "steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    first.record()
-    for i in range(args.steps):
-        scr.launch(i & 1)
-        ends[i].record()
-        if i > 0:
-            ends[i - 1].synchronize()
-            summary = scr.summarize((i - 1) & 1)
-    last.record()
-    ends[args.steps - 1].synchronize()
-    summary = scr.summarize((args.steps - 1) & 1)
+    summary = pipelined(args.steps, (first, last))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -353,7 +373,8 @@ def main():
         sync.launch()
         sync.read()
     sync_ms = (time.perf_counter() - ts) * 1e3 / 10
-    assert sync.records() == scr.records((args.steps - 1) & 1), "pipelined and synchronous records differ"
+    assert sync.records() == scr.records((args.steps - 1) % (2 * BATCH)), \
+        "pipelined and synchronous records differ"
     screened = K * n * b
     algorithmic = (K + 1) * n * b
     value = screened / (ms_per_step * 1e-3) / 1e9
