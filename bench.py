@@ -5,28 +5,32 @@ One step is one pass of the screening hot path over one batch of candidate
 outputs already resident in HBM: the policy gate, the screening kernel (one
 coalesced read of the reference and the K candidates, per-candidate
 statistics) and the readback of the K records with the pass/fail verdict.
-Steps are pipelined the way a screening service runs them: the kernel of
-step i writes its records straight into one of 2 * BATCH pinned host
-buffers (a ring), one completion event follows every BATCH steps, and while
-the device works on the current batch the host takes the verdicts of the
-batch before it (after that batch's event).  value = K * numel * element
-bytes / step time (GB/s).  A few fully synchronous steps (launch, copy
-back, wait) are timed too and reported as sync_step_ms.
+Steps are pipelined the way a screening service runs independent batches:
+they alternate over two streams, each with its own workspace, so that a
+pass starts on the work-group slots the previous pass frees while its last
+work-groups finish; the kernel of each step writes its records straight
+into one of 2 * BATCH pinned host buffers (a ring per stream), one
+completion event per stream follows every BATCH steps of that stream, and
+while the device works on the current batch the host takes the verdicts of
+the batch before it (after that batch's events).  value = K * numel *
+element bytes / step time (GB/s).  A few fully synchronous steps (launch,
+copy back, wait) are timed too and reported as sync_step_ms.
 
 Before the timed region the device runs about 0.2 s of back-to-back
 launches (untimed), so that the timed steps run at the sustained clock, and
 the W warmup steps run the same pipelined loop as the timed ones.
 
 The JSON line also carries the roofline of the screening kernel.  Its
-duration is measured with a pair of HIP events on the launch stream around
-the timed region (the completion events carry no timestamps): the
-launches follow each other on the device and it is never idle in that
-loop, so the interval divided by the number of steps is the kernel's time
-per launch, including the dispatch gap between kernels and the share of
-the completion events.  The
+duration is measured right after the timed steps: the same number of
+launches back to back on one stream between a pair of HIP events on that
+stream, with nothing else in between, so the interval divided by the
+launches is the kernel's time per launch, including the dispatch gap
+between kernels (and agreeing with a kernel trace of the run).  The
 algorithmic bytes are (K+1) * numel * element bytes per launch, a compulsory
-read of every candidate and the reference once.  Also: the CPU oracle timed on a
-bounded sample of the same workload, the generator's throughput, two
+read of every candidate and the reference once.  Also: single launches
+timed warm and cold (after a 512 MiB read that evicts the caches), the CPU
+oracle timed on a bounded sample of the same workload, the generator's
+throughput, two
 optional passes over the same candidates (the position search,
 kb_screen_locate, and the fail-fast screen, KB_FAIL_FAST, whose kernel time
 and share of candidate elements read are reported beside the full
@@ -139,6 +143,33 @@ def stream_context(dev, nbytes=1 << 30):
         ms = s.elapsed_time(e) / 10
         res[name] = {"bytes": moved, "ms": round(ms, 4), "GB_per_s": round(moved / ms / 1e6, 1)}
     del src, dst, x
+    return res
+
+
+def single_launch(scr, stream, dev, reps=10, flush_bytes=512 << 20):
+    """One launch at a time, each between its own pair of events: warm (the
+    previous launch's data may still sit in L2 and the 256 MB last-level
+    cache) and cold (a 512 MiB buffer read just before, outside the event
+    pair, evicts them; read rather than written, so that no dirty lines are
+    left to be written back during the launch).  Medians in ms; each
+    includes one launch's dispatch and the events' own signal."""
+    import torch
+    buf = torch.ones(flush_bytes // 4, dtype=torch.float32, device=dev)
+    res = {}
+    for name, flush in (("warm_ms", False), ("cold_ms", True)):
+        ms = []
+        for _ in range(reps):
+            if flush:
+                buf.sum()
+                torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            scr.launch(0)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        res[name] = round(sorted(ms)[len(ms) // 2], 5)
+    del buf
     return res
 
 
@@ -280,6 +311,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--streams", type=int, default=2,
+                    help="streams the pipelined steps alternate over (each with its own workspace)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gen", action="store_true")
@@ -305,35 +338,47 @@ def main():
     w = synth.build(args.config, dev, seed=0)
     torch.cuda.synchronize()
     K, n, b = len(w.cands), w.numel, w.dtype_bytes
-    scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol, host_slots=2 * BATCH)
+    # One screener (workspace, ring of record slots) per stream; steps
+    # alternate over the streams.
+    streams = [torch.cuda.Stream() for _ in range(args.streams)]
+    scrs = [kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, host_slots=2 * BATCH) for st in streams]
+    scr = scrs[0]
     plan = scr.launch_plan()
+    S = len(scrs)
 
-    def pipelined(n, timing=None):
-        """n steps into the ring of 2 * BATCH pinned record slots; after
-        every BATCH steps one completion event, and the verdicts of the
-        batch before it (whose event has then been reached).  Returns the
+    def slot_of(i):
+        return scrs[i % S], (i // S) % (2 * BATCH)
+
+    def pipelined(n):
+        """n steps, step i on stream i mod S into that stream's ring of
+        2 * BATCH pinned record slots; after every BATCH steps per stream
+        one completion event per stream, and the verdicts of the batch
+        before it (whose events have then been reached).  Returns the
         summary of the last step."""
+        per_batch = BATCH * S
         evs = []
         summary = None
 
-        def take(b):
+        def take(bi):
             nonlocal summary
-            evs[b].synchronize()
-            for s in range(b * BATCH, min(n, (b + 1) * BATCH)):
-                summary = scr.summarize(s % (2 * BATCH))
+            for e in evs[bi]:
+                e.synchronize()
+            for i in range(bi * per_batch, min(n, (bi + 1) * per_batch)):
+                sc, sl = slot_of(i)
+                summary = sc.summarize(sl)
 
-        if timing is not None:
-            timing[0].record()
         for i in range(n):
-            scr.launch(i % (2 * BATCH))
-            if (i + 1) % BATCH == 0 or i == n - 1:
-                e = torch.cuda.Event()
-                e.record()
-                evs.append(e)
+            sc, sl = slot_of(i)
+            sc.launch(sl)
+            if (i + 1) % per_batch == 0 or i == n - 1:
+                batch = []
+                for st in streams:
+                    e = torch.cuda.Event()
+                    e.record(st)
+                    batch.append(e)
+                evs.append(batch)
                 if len(evs) >= 2:
                     take(len(evs) - 2)
-        if timing is not None:
-            timing[1].record()
         take(len(evs) - 1)
         return summary
 
@@ -351,18 +396,23 @@ def main():
     if args.warmup > 0:
         pipelined(args.warmup)
     torch.cuda.synchronize()
-    # the kernel time comes from a timing pair around the whole timed region
-    first = torch.cuda.Event(enable_timing=True)
-    last = torch.cuda.Event(enable_timing=True)
     log("timing", args.steps, "steps")
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    summary = pipelined(args.steps, (first, last))
+    summary = pipelined(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    # the launches run back to back on the device: the device time per launch
-    # over the timed region
+    # The kernel alone, for the roofline: the same number of launches back to
+    # back on one stream, between a pair of HIP events on that stream (no
+    # completion events in between), so that the interval divided by the
+    # launches is the kernel's time per launch including the dispatch gap.
+    first = torch.cuda.Event(enable_timing=True)
+    last = torch.cuda.Event(enable_timing=True)
+    first.record(streams[0])
+    for i in range(args.steps):
+        scr.launch(i % (2 * BATCH))
+    last.record(streams[0])
+    torch.cuda.synchronize()
     kern_ms = first.elapsed_time(last) / args.steps
     # synchronous steps: launch, copy the records back, wait
     sync = kb.Screener(w.ref, w.cands, w.atol, w.rtol)
@@ -373,8 +423,9 @@ def main():
         sync.launch()
         sync.read()
     sync_ms = (time.perf_counter() - ts) * 1e3 / 10
-    assert sync.records() == scr.records((args.steps - 1) % (2 * BATCH)), \
-        "pipelined and synchronous records differ"
+    for i in range(max(0, args.steps - S), args.steps):
+        sc, sl = slot_of(i)
+        assert sync.records() == sc.records(sl), "pipelined and synchronous records differ"
     screened = K * n * b
     algorithmic = (K + 1) * n * b
     value = screened / (ms_per_step * 1e-3) / 1e9
@@ -399,6 +450,7 @@ def main():
         "config": {"workload": "%s: %s" % (args.config, WORKLOADS[args.config]), "K": K,
                    "numel": n, "storage_dtype": str(w.ref.dtype).replace("torch.", ""),
                    "atol": w.atol, "rtol": w.rtol, "launch": plan,
+                   "pipeline": {"streams": S, "steps_per_completion_event": BATCH},
                    "verdicts": summ},
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
@@ -406,6 +458,10 @@ def main():
                      "traffic": counted_traffic(args.config), "kernel_ms": round(kern_ms, 5),
                      "algorithmic_bytes_per_launch": algorithmic, "kernel_digest": kernel_digest()},
     }
+    # one launch at a time, warm and after a cache flush
+    sl = single_launch(scr, streams[0], dev)
+    sl["cold_algorithmic_GB_per_s"] = round(algorithmic / (sl["cold_ms"] * 1e-3) / 1e9, 1)
+    out["single_launch"] = sl
     if args.copy_calibration:
         log("copy calibration")
         copy_calibration(dev)
