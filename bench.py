@@ -225,7 +225,8 @@ def multi_output_leg(dev, kb, K=16):
     """kb_screen_multi on an attention-style output pair: out fp16
     [4, 32, 2048, 128] and lse fp32 [4, 32, 2048], K candidates (in-tolerance
     noise on both outputs).  Kernel time over both outputs and the
-    algorithmic GB/s ((K + 1) x the bytes of one output tuple).  (fp16, so
+    algorithmic GB/s ((K + 1) x the bytes of one output tuple), calls back
+    to back with the arguments marshalled once.  (fp16, so
     that its launches are not the same kernel instantiation as the headline
     workload's, whose profile they would otherwise mix into.)"""
     import torch
@@ -239,19 +240,23 @@ def multi_output_leg(dev, kb, K=16):
         cands.append([(out.float() * (1 + 1e-3 * torch.randn(out.shape, generator=gk, device=dev)))
                       .to(torch.float16),
                       lse + 1e-6 * torch.randn(lse.shape, generator=gk, device=dev)])
-    d_stats, ws = kb.kb_screen_multi(refs, cands, [1e-2, 1e-4], [1e-2, 1e-4])
+    ms_ = kb.MultiScreener(refs, cands, [1e-2, 1e-4], [1e-2, 1e-4])
+    for _ in range(3):
+        ms_.launch()
     torch.cuda.synchronize()
+    # calls back to back (arguments marshalled once), timed as one region
     ms = []
-    for _ in range(10):
+    for _ in range(5):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        kb.kb_screen_multi(refs, cands, [1e-2, 1e-4], [1e-2, 1e-4], workspace=ws, d_stats=d_stats)
+        for _ in range(10):
+            ms_.launch()
         e1.record()
         torch.cuda.synchronize()
-        ms.append(e0.elapsed_time(e1))
+        ms.append(e0.elapsed_time(e1) / 10)
     m = sorted(ms)[len(ms) // 2]
     tup = out.numel() * 2 + lse.numel() * 4
-    recs, _ = kb.kb_screen_stats(d_stats, 2 * K)
+    recs = ms_.records()
     return {"outputs": ["f16 [4,32,2048,128]", "f32 [4,32,2048]"], "K": K, "ms": round(m, 4),
             "algorithmic_GB_per_s": round((K + 1) * tup / (m * 1e-3) / 1e9, 1),
             "n_passed": sum(1 for k in range(K) if recs[k]["passed"] and recs[K + k]["passed"])}

@@ -432,6 +432,46 @@ def kb_screen_multi(refs, cands, atol, rtol, flags=0, workspace=None, d_stats=No
     return d_stats, workspace
 
 
+class MultiScreener:
+    """Repeated kb_screen_multi calls over one fixed set of buffers, with the
+    argument marshalling (descriptors, tolerances, workspace, records, stream
+    handle) done once at construction, as Screener does for one output."""
+
+    def __init__(self, refs, cands, atol, rtol, flags=0, stream=None):
+        torch = _torch()
+        self.n_out, self.n = len(refs), len(cands)
+        if isinstance(atol, (int, float)):
+            atol = [atol] * self.n_out
+        if isinstance(rtol, (int, float)):
+            rtol = [rtol] * self.n_out
+        self._keep = (list(refs), [list(row) for row in cands])
+        self._R = (KbTensor * max(1, self.n_out))(*[describe(r) for r in refs])
+        self._C = (KbTensor * max(1, self.n * self.n_out))(*[describe(c) for row in cands for c in row])
+        self._A = (ctypes.c_float * max(1, self.n_out))(*[float(x) for x in atol])
+        self._T = (ctypes.c_float * max(1, self.n_out))(*[float(x) for x in rtol])
+        self.flags = int(flags)
+        self._L = lib()
+        nbytes = self._L.kb_screen_multi_workspace_bytes(self._R, self.n_out, max(1, self.n))
+        if nbytes == 0:
+            raise KbError(KB_ERR_INVALID_ARG, "no multi-output workspace size for these arguments")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=refs[0].device)
+        kb_screen_workspace_init(self.workspace, stream)
+        self.d_stats = alloc_stats(max(1, self.n * self.n_out), refs[0].device)
+        self._ws = ctypes.c_void_p(self.workspace.data_ptr())
+        self._st = ctypes.c_void_p(self.d_stats.data_ptr())
+        self._stream = _stream_handle(stream)
+        self.stream = stream
+
+    def launch(self):
+        _check(self._L.kb_screen_multi(self._R, self.n_out, self._C, self.n, self._A, self._T, self.flags,
+                                       self._ws, self.workspace.numel(), self._st, self._stream))
+
+    def records(self):
+        """All n_out * n_cands records, output-major (synchronizes the stream)."""
+        recs, _ = kb_screen_stats(self.d_stats, self.n * self.n_out, stream=self.stream)
+        return recs
+
+
 def screen_multi(refs, cands, atol, rtol, flags=0, stream=None):
     """Gate + screen + readback of multi-output candidates: (records[o][k]
     dicts, summary dict, passed list)."""

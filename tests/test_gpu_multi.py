@@ -138,6 +138,25 @@ def test_single_output_equals_kb_screen(dev):
     assert passed == [1, 1, 1, 0, 1]
 
 
+def test_multiscreener_repeated_launches(dev):
+    """The pre-marshalled MultiScreener: every launch gives the records of
+    kb_screen_multi on the same arguments, call after call on one
+    workspace."""
+    refs = attention_like(dev, seed=9)
+    out, lse, aux = refs
+    atol, rtol = [1e-2, 1e-4, 1e-3], [1e-2, 1e-4, 1e-3]
+    cands = [[perturb(out, 1e-3, 21), lse.clone(), aux.clone()],
+             [out.clone(), perturb(lse, 1e-2, 22), aux.clone()],
+             [out.clone(), lse[:, :, :255].clone(), aux.clone()],
+             [perturb(out, 0.5, 23), perturb(lse, 1e-6, 24), perturb(aux, 1e-4, 25)]]
+    want, _, _ = kb.screen_multi(refs, cands, atol, rtol)
+    ms = kb.MultiScreener(refs, cands, atol, rtol)
+    for rep in range(3):
+        ms.launch()
+        got = ms.records()
+        assert [got[o * 4:(o + 1) * 4] for o in range(3)] == want, rep
+
+
 def test_argument_errors(dev):
     refs = attention_like(dev)
     cands = [[r.clone() for r in refs]]
