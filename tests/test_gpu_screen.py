@@ -288,6 +288,23 @@ def test_stream_ordering_with_side_stream(dev):
     assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), "side stream")
 
 
+def test_two_streams_concurrent_screens(dev):
+    """Screens of the same candidates alternating over two streams, each
+    with its own workspace and ring of pinned record slots, overlapping on
+    the device (the pipelined bench loop): every record is the oracle's."""
+    say("two streams")
+    w = synth.build("c2", dev, seed=6, scale=1 / 16)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    scrs = [kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, host_slots=4) for st in streams]
+    for i in range(16):
+        scrs[i % 2].launch((i // 2) % 4)
+    torch.cuda.synchronize()
+    orc = oracle_records(w.ref, w.cands, w.atol, w.rtol)
+    for sc in scrs:
+        for slot in range(4):
+            assert_records_match(sc.records(slot), orc, "two streams slot %d" % slot)
+
+
 # ------------------------------------------------ exhaustive 16-bit pairs ---
 
 @pytest.mark.parametrize("dt,tol", [("f16", 1e-3), ("bf16", 1e-2)])
