@@ -320,6 +320,34 @@ def kb_screen_locate(ref, cands, atol, rtol, d_stats, flags=0, stream=None):
     return [locs[k].as_dict() for k in range(len(cands))]
 
 
+class Locator:
+    """Repeated kb_screen_locate calls over one fixed set of buffers and
+    records, with the argument marshalling done once (as Screener does for
+    kb_screen): launch() enqueues, read() copies the positions back."""
+
+    def __init__(self, ref, cands, atol, rtol, d_stats, flags=0, stream=None):
+        torch = _torch()
+        self._keep = (ref, list(cands), d_stats)
+        self.n = len(cands)
+        self._ref = describe(ref)
+        self._arr = (KbTensor * max(1, self.n))(*[describe(c) for c in cands])
+        self.out = torch.empty(max(1, self.n) * ctypes.sizeof(KbLocate), dtype=torch.uint8, device=ref.device)
+        self.atol, self.rtol, self.flags = float(atol), float(rtol), int(flags)
+        self._stats = ctypes.c_void_p(d_stats.data_ptr())
+        self._out = ctypes.c_void_p(self.out.data_ptr())
+        self._stream = _stream_handle(stream)
+        self._L = lib()
+
+    def launch(self):
+        _check(self._L.kb_screen_locate(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
+                                        self.flags, self._stats, self._out, self._stream))
+
+    def read(self):
+        host = self.out.cpu()
+        locs = (KbLocate * max(1, self.n)).from_buffer_copy(host.numpy().tobytes())
+        return [locs[k].as_dict() for k in range(self.n)]
+
+
 def locate(ref, cands, atol, rtol, flags=0, stream=None):
     """Screen, then locate: (records, positions)."""
     d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)

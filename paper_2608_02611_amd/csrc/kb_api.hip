@@ -708,9 +708,20 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
     p.flags = flags;
     p.stats = stats;
     p.out = d_loc;
-    // Work-groups per candidate: about 2048 in flight per launch, a multiple
-    // of 8, at most one per 8 chunks (and at least one).
+    // Work-groups per candidate: the launch is one round of the work-groups
+    // resident on the device at once (occupancy x CUs; a launch of more
+    // makes a second, mostly idle round), spread over the launch's
+    // candidates, a multiple of 8 (the XCD count), at least 8 and at most
+    // one per 8 chunks.
     const uint64_t n_chunks = numel / 512;
+    int resident = 0;
+    {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+            resident = cus * locate_blocks_per_cu(ref->dtype);
+    }
+    if (resident <= 0) resident = 2048;
     LocTable tab;
     int k = 0;
     while (k < n_cands) {
@@ -718,8 +729,8 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
         for (; k < n_cands && n < kLocateBatch; ++k)
             if (status[k] == KB_STATUS_OK) tab.e[n++] = LocEntry{cands[k].data, k, 0};
         if (n == 0) break;
-        uint64_t stripes = (2048 + n - 1) / n;
-        stripes = (stripes + 7) / 8 * 8;
+        uint64_t stripes = (uint64_t)resident / n / 8 * 8;
+        if (stripes < 8) stripes = 8;
         const uint64_t cap = n_chunks / 8 > 8 ? n_chunks / 8 / 8 * 8 : 8;
         if (stripes > cap) stripes = cap;
         p.n = n;

@@ -166,6 +166,9 @@ struct LocateParams {
     kb_locate* out;
 };
 hipError_t launch_locate(int dtype, const LocateParams& p, const LocTable& tab, hipStream_t stream);
+// Work-groups of the position-search kernel for dtype resident per CU
+// (occupancy query, cached), or 0 on failure.
+int locate_blocks_per_cu(int dtype);
 // Fill n_words 32-bit words with value.
 hipError_t launch_fill_u32(void* dst, uint64_t n_words, uint32_t value, hipStream_t stream);
 

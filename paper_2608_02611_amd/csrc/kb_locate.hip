@@ -57,19 +57,21 @@ struct LaneChunk {
     }
 };
 
+// One lane's part of chunk `chunk` of a tensor: base is wave-uniform (scalar
+// registers), off = 16 * lane, so a load is a scalar base plus the lane's
+// 32-bit offset.
 template <int DT>
-__device__ __forceinline__ LaneChunk<DT> load_lane(const void* base, uint64_t chunk, int lane) {
+__device__ __forceinline__ LaneChunk<DT> load_lane(const char* base, uint64_t chunk, uint32_t off) {
     LaneChunk<DT> x;
+    typedef const __attribute__((address_space(1))) char* gbytes;
+    const gbytes c = (gbytes)base + chunk * (DT == DT_F32 ? 2048u : 1024u);
+    uint32_t o = off;
+    asm volatile("" : "+v"(o));
+    const v4u32 a = __builtin_nontemporal_load((gvec)(c + o));
+    x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
     if constexpr (DT == DT_F32) {
-        const gvec p = (gvec)base + chunk * 128;
-        const v4u32 a = __builtin_nontemporal_load(p + lane);
-        const v4u32 b = __builtin_nontemporal_load(p + 64 + lane);
-        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
+        const v4u32 b = __builtin_nontemporal_load((gvec)(c + o + 1024u));
         x.w[4] = b.x; x.w[5] = b.y; x.w[6] = b.z; x.w[7] = b.w;
-    } else {
-        const gvec p = (gvec)base + chunk * 64;
-        const v4u32 a = __builtin_nontemporal_load(p + lane);
-        x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
     }
     return x;
 }
@@ -130,51 +132,139 @@ __device__ __forceinline__ Hit classify(float c, float r, float atol, float rtol
     return h;
 }
 
+// How the max-rel predicate is filtered for one candidate (wave-uniform):
+// REL_NONE  no max-rel position wanted (max_rel is 0 or NaN, or found);
+// REL_INF   max_rel = +inf: a zero reference, an infinite difference or a
+//           quotient beyond 2^100 can give it;
+// REL_ALL   max_rel < 2^-100, where T below might round back up to max_rel:
+//           every element is checked by division;
+// REL_FMA   d - T a >= 0 with T = fl(max_rel (1 - 2^-20)): fl(d / a) ==
+//           max_rel needs d / a >= max_rel (1 - 2^-24), and the fma keeps
+//           the sign (an underflow to zero passes).
+enum { REL_NONE = 0, REL_INF = 1, REL_ALL = 2, REL_FMA = 3 };
+
+template <int RM>
+__device__ __forceinline__ bool rel_candidate(float d, float a, float T) {
+    if constexpr (RM == REL_NONE) return false;
+    else if constexpr (RM == REL_INF) return a == 0.f || d == __builtin_inff() || d >= a * 0x1p100f;
+    else if constexpr (RM == REL_ALL) return true;
+    else return fmaf(-T, a, d) >= 0.f;
+}
+
+// One chunk's cheap pass: per element only the wave ballots of the
+// mismatch predicate (M: still looked for), of d == max_abs and of the
+// max-rel filter, OR-ed over the lane's elements (scalar masks, no per-lane
+// state).  A nonzero mask sends the wave to the exact pass.
+struct AnyHits {
+    uint64_t m, a, r;
+};
+
+template <int DT, bool M, int RM>
+__device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const LaneChunk<DT>& cc, float atol,
+                                              float rtol, bool equal_nan, float max_abs, float T) {
+    AnyHits h{0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < kE; ++i) {
+        const float c = widen_bits<DT>(cc.bits(i));
+        const float r = widen_bits<DT>(rc.bits(i));
+        const float d = fabsf(c - r);
+        const float a = fabsf(r);
+        if constexpr (M) {
+            const float tol = __builtin_isfinite(r) ? __fadd_rn(atol, __fmul_rn(rtol, a)) : -1.0f;
+            const bool match = (c == r) || (d <= tol) || (equal_nan && __builtin_isnan(c) && __builtin_isnan(r));
+            h.m |= ballot(!match);
+        }
+        h.a |= ballot(d == max_abs);
+        if constexpr (RM != REL_NONE) h.r |= ballot(rel_candidate<RM>(d, a, T));
+    }
+    return h;
+}
+
+template <int DT, bool M>
+__device__ __forceinline__ AnyHits cheap_pass_rm(int rm, const LaneChunk<DT>& rc, const LaneChunk<DT>& cc,
+                                                 float atol, float rtol, bool equal_nan, float max_abs, float T) {
+    if (rm == REL_FMA) return cheap_pass<DT, M, REL_FMA>(rc, cc, atol, rtol, equal_nan, max_abs, T);
+    if (rm == REL_NONE) return cheap_pass<DT, M, REL_NONE>(rc, cc, atol, rtol, equal_nan, max_abs, T);
+    if (rm == REL_INF) return cheap_pass<DT, M, REL_INF>(rc, cc, atol, rtol, equal_nan, max_abs, T);
+    return cheap_pass<DT, M, REL_ALL>(rc, cc, atol, rtol, equal_nan, max_abs, T);
+}
+
+// A pointer made explicitly wave-uniform (held in scalar registers), so that
+// a load is a scalar base plus the lane's 32-bit offset.
+__device__ __forceinline__ const char* uniform_base(const void* p) {
+    const uint64_t v = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const char*)(((uint64_t)hi << 32) | lo);
+}
+
 template <int DT>
 __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTable tab) {
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // (explicitly wave-uniform, so that the chunk index, the loads' bases and
+    // the per-chunk choices stay in scalar registers and branches)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int xcd = blockIdx.x & 7;  // p.stripes is a multiple of 8
     const int slot = blockIdx.x >> 3;
     const int k = slot % p.n;
     const int stripe = (slot / p.n) * 8 + xcd;
-    const void* cand = tab.e[k].data;
+    const char* cand = uniform_base(tab.e[k].data);
+    const char* ref = uniform_base(p.ref);
     const int index = tab.e[k].index;
-    const float max_abs = p.stats[index].max_abs_err;
-    const float max_rel = p.stats[index].max_rel_err;
+    // the record's fields, made explicitly wave-uniform (they are loaded by
+    // every lane from the same address)
+    const float max_abs = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(p.stats[index].max_abs_err)));
+    const float max_rel = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(p.stats[index].max_rel_err)));
+    const bool has_mism = __builtin_amdgcn_readfirstlane(p.stats[index].mismatches > 0 ? 1 : 0) != 0;
     const bool want_abs = max_abs > 0.f;  // false for 0 and NaN
     const bool want_rel = max_rel > 0.f;
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
+    const int rel_mode = !want_rel ? REL_NONE
+                         : __builtin_isinf(max_rel) ? REL_INF
+                         : max_rel < 0x1p-100f ? REL_ALL : REL_FMA;
+    const float T = max_rel * 0x1.ffffep-1f;
 
-    // the wave's finds (wave-uniform), all-ones until found
+    // the wave's finds (wave-uniform), all-ones until found; a candidate
+    // whose record counts no mismatch has none to look for (the record was
+    // written by the screen under the same tolerances and flags)
     uint64_t f_mism = kNone, f_abs = kNone, f_rel = kNone;
-    bool need_mism = true, need_abs = want_abs, need_rel = want_rel;
+    bool need_mism = has_mism, need_abs = want_abs, need_rel = want_rel;
     const uint64_t n_chunks = p.numel / kChunk;
     const uint64_t wstride = (uint64_t)p.stripes * kWaves;
+    const uint32_t off = 16u * (uint32_t)lane;
     for (uint64_t chunk = (uint64_t)stripe * kWaves + wave;
          chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += wstride) {
-        const LaneChunk<DT> rc = load_lane<DT>(p.ref, chunk, lane);
-        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, lane);
-        uint32_t mm = 0u, ma = 0u, mr = 0u;  // bit i: element i of this lane qualifies
+        const LaneChunk<DT> rc = load_lane<DT>(ref, chunk, off);
+        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, off);
+        // (readfirstlane: the choice of variant is a scalar branch)
+        const int rm = __builtin_amdgcn_readfirstlane(need_rel ? rel_mode : REL_NONE);
+        const AnyHits h = __builtin_amdgcn_readfirstlane(need_mism ? 1 : 0)
+                              ? cheap_pass_rm<DT, true>(rm, rc, cc, p.atol, p.rtol, equal_nan, max_abs, T)
+                              : cheap_pass_rm<DT, false>(rm, rc, cc, p.atol, p.rtol, equal_nan, max_abs, T);
+        const uint64_t any_m = h.m, any_a = need_abs ? h.a : 0u, any_r = h.r;
+        if ((any_m | any_a | any_r) == 0) continue;
+        // Exact pass (rare): the definitions, element by element, into 8-bit
+        // lane masks (bit i: element i of this lane qualifies); a position
+        // found anywhere in this chunk is below everything later.
+        uint32_t mm = 0u, ma = 0u, mr = 0u;
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
             const Hit h = classify(widen_bits<DT>(cc.bits(i)), widen_bits<DT>(rc.bits(i)), p.atol, p.rtol,
-                                   equal_nan, max_abs, max_rel, need_abs, need_rel);
+                                   equal_nan, max_abs, max_rel, any_a != 0, any_r != 0);
             mm |= (uint32_t)h.mism << i;
             ma |= (uint32_t)h.abs << i;
             mr |= (uint32_t)h.rel << i;
         }
-        // a position found anywhere in this chunk is below everything later
         const uint64_t base = chunk * kChunk;
-        if (need_mism && ballot(mm != 0u)) {
+        if (any_m != 0) {
             f_mism = base + wave_min_u32(first_in_lane<DT>(mm, lane));
             need_mism = false;
         }
-        if (need_abs && ballot(ma != 0u)) {
+        if (any_a != 0) {
             f_abs = base + wave_min_u32(first_in_lane<DT>(ma, lane));
             need_abs = false;
         }
-        if (need_rel && ballot(mr != 0u)) {
+        if (any_r != 0 && ballot(mr != 0u)) {
             f_rel = base + wave_min_u32(first_in_lane<DT>(mr, lane));
             need_rel = false;
         }
@@ -218,6 +308,25 @@ hipError_t launch_locate(int dtype, const LocateParams& p, const LocTable& tab, 
         default: hipLaunchKernelGGL(locate_kernel<DT_BF16>, dim3(grid), dim3(kThreads), 0, stream, p, tab); break;
     }
     return hipGetLastError();
+}
+
+int locate_blocks_per_cu(int dtype) {
+    // The occupancy of a kernel does not change during the process.
+    static int cache[3] = {};  // value + 1, 0 = not queried yet
+    const int di = dtype == DT_F32 ? 0 : dtype == DT_F16 ? 1 : 2;
+    int v = __atomic_load_n(&cache[di], __ATOMIC_RELAXED) - 1;
+    if (v < 0) {
+        int n = 0;
+        hipError_t e;
+        switch (dtype) {
+            case DT_F32: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, locate_kernel<DT_F32>, kThreads, 0); break;
+            case DT_F16: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, locate_kernel<DT_F16>, kThreads, 0); break;
+            default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, locate_kernel<DT_BF16>, kThreads, 0); break;
+        }
+        v = e == hipSuccess ? n : 0;
+        __atomic_store_n(&cache[di], v + 1, __ATOMIC_RELAXED);
+    }
+    return v;
 }
 
 hipError_t launch_fill_u32(void* dst, uint64_t n_words, uint32_t value, hipStream_t stream) {
