@@ -11,14 +11,15 @@
 // A wave scans its chunks in increasing index order and stops looking for a
 // position as soon as one of its lanes has found it: every later chunk of
 // the wave holds larger indices.  On a failing candidate the first mismatch
-// is usually in a wave's first chunk, so most of the pass is skipped.  Per
-// element only the three predicates are evaluated, into 8-bit lane masks;
-// an index is formed only for a chunk whose ballot shows a hit (the lane's
-// lowest set bit, then a wave minimum by DPP), and the wave's finds are
-// merged into the output with a 64-bit atomic minimum ("none" is all-ones,
-// which reads as -1).  Work-group ids are mapped like the screen's, so that
-// the candidates of one stripe run on one XCD and share the reference stripe
-// in its L2.
+// is usually in a wave's first chunk.  Per element a cheap pass only ORs
+// three wave ballots (mismatch, d == max abs, the max-rel filter) into
+// scalar masks; a chunk whose masks show a hit is evaluated again from the
+// definitions into 8-bit lane masks, and its index formed (the lane's lowest
+// set bit, then a wave minimum by DPP).  The wave's finds are merged into
+// the output with a 64-bit atomic minimum ("none" is all-ones, which reads
+// as -1).  Work-group ids are mapped like the screen's, so that the
+// candidates of one stripe run on one XCD and share the reference stripe in
+// its L2.
 #include "kb_device.hpp"
 #include "kb_internal.hpp"
 
