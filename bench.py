@@ -58,11 +58,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-# Steps per completion event of the pipelined loop: an event recorded
-# between two launches was measured to add about 3.3 us to that step (the
-# device's signal between kernels), so the host takes the verdicts in
-# batches of BATCH steps over a ring of 2 * BATCH pinned record slots.
-BATCH = 4
+# Steps per stream between completion events of the pipelined loop: an
+# event recorded between two launches was measured to add about 3.3 us to
+# that step (the device's signal between kernels), so the host takes the
+# verdicts in batches of BATCH steps per stream, over a ring of 2 * BATCH
+# pinned record slots per stream (--batch).
+BATCH_DEFAULT = 4
 METRIC = "candidate GB/s screened (K\u00d7N\u00d7dtype bytes/s) and % of MI355X HBM peak"
 KERNEL_SOURCES = ["paper_2608_02611_amd/csrc/kb_screen.hip", "paper_2608_02611_amd/csrc/kb_device.hpp",
                   "paper_2608_02611_amd/csrc/kb_internal.hpp"]
@@ -316,6 +317,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--batch", type=int, default=BATCH_DEFAULT,
+                    help="steps per stream between completion events (verdicts taken per batch)")
     ap.add_argument("--streams", type=int, default=2,
                     help="streams the pipelined steps alternate over (each with its own workspace)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -325,6 +328,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
+    batch = max(1, args.batch)
     if args.gpus != 1:
         print("bench.py measures one GPU: the screening library runs on a single MI355X "
               "(sharding over several GPUs is described, not implemented); run with --gpus 1",
@@ -346,21 +350,21 @@ def main():
     # One screener (workspace, ring of record slots) per stream; steps
     # alternate over the streams.
     streams = [torch.cuda.Stream() for _ in range(args.streams)]
-    scrs = [kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, host_slots=2 * BATCH) for st in streams]
+    scrs = [kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, host_slots=2 * batch) for st in streams]
     scr = scrs[0]
     plan = scr.launch_plan()
     S = len(scrs)
 
     def slot_of(i):
-        return scrs[i % S], (i // S) % (2 * BATCH)
+        return scrs[i % S], (i // S) % (2 * batch)
 
     def pipelined(n):
         """n steps, step i on stream i mod S into that stream's ring of
-        2 * BATCH pinned record slots; after every BATCH steps per stream
+        2 * batch pinned record slots; after every `batch` steps per stream
         one completion event per stream, and the verdicts of the batch
         before it (whose events have then been reached).  Returns the
         summary of the last step."""
-        per_batch = BATCH * S
+        per_batch = batch * S
         evs = []
         summary = None
 
@@ -376,12 +380,12 @@ def main():
             sc, sl = slot_of(i)
             sc.launch(sl)
             if (i + 1) % per_batch == 0 or i == n - 1:
-                batch = []
+                evb = []
                 for st in streams:
                     e = torch.cuda.Event()
                     e.record(st)
-                    batch.append(e)
-                evs.append(batch)
+                    evb.append(e)
+                evs.append(evb)
                 if len(evs) >= 2:
                     take(len(evs) - 2)
         take(len(evs) - 1)
@@ -395,7 +399,7 @@ def main():
     t_warm = time.perf_counter() + 0.2
     while time.perf_counter() < t_warm:
         for i in range(20):
-            scr.launch(i % (2 * BATCH))
+            scr.launch(i % (2 * batch))
         torch.cuda.synchronize()
     log("warmup", args.warmup)
     if args.warmup > 0:
@@ -415,7 +419,7 @@ def main():
     last = torch.cuda.Event(enable_timing=True)
     first.record(streams[0])
     for i in range(args.steps):
-        scr.launch(i % (2 * BATCH))
+        scr.launch(i % (2 * batch))
     last.record(streams[0])
     torch.cuda.synchronize()
     kern_ms = first.elapsed_time(last) / args.steps
@@ -455,7 +459,7 @@ def main():
         "config": {"workload": "%s: %s" % (args.config, WORKLOADS[args.config]), "K": K,
                    "numel": n, "storage_dtype": str(w.ref.dtype).replace("torch.", ""),
                    "atol": w.atol, "rtol": w.rtol, "launch": plan,
-                   "pipeline": {"streams": S, "steps_per_completion_event": BATCH},
+                   "pipeline": {"streams": S, "steps_per_completion_event": batch},
                    "verdicts": summ},
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
@@ -463,6 +467,9 @@ def main():
                      "traffic": counted_traffic(args.config), "kernel_ms": round(kern_ms, 5),
                      "algorithmic_bytes_per_launch": algorithmic, "kernel_digest": kernel_digest()},
     }
+    tr = out["roofline"]["traffic"]
+    # counted HBM bytes per launch over the same kernel time
+    out["roofline"]["traffic_GB_per_s"] = round(tr / (kern_ms * 1e-3) / 1e9, 1) if tr else None
     # one launch at a time, warm and after a cache flush
     sl = single_launch(scr, streams[0], dev)
     sl["cold_algorithmic_GB_per_s"] = round(algorithmic / (sl["cold_ms"] * 1e-3) / 1e9, 1)
