@@ -67,12 +67,16 @@ _lib = None
 
 
 def lib():
-    """Load oracle/libkbo.so, building it first if it is missing."""
+    """Load oracle/libkbo.so, building it first if it is missing.  The
+    environment variable KBO_LIB names another build of the same sources to
+    load instead (the mutation test runs the pins against copies of the
+    oracle with a planted mistake)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
+        path = os.environ.get("KBO_LIB") or _build.LIB
+        if path == _build.LIB and not os.path.exists(path):
             _build.build()
-        L = ctypes.CDLL(_build.LIB)
+        L = ctypes.CDLL(path)
         u32, u64, f32, vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p
         L.kbo_philox4x32_10.argtypes = [ctypes.POINTER(u32), ctypes.POINTER(u32),
                                         ctypes.POINTER(u32)]

@@ -1,0 +1,111 @@
+"""The oracle's pins catch plausible mistakes in the oracle.
+
+Each case plants one mistake (a dropped term, a wrong comparison, a wrong
+operand, sign, index or constant) in a copy of the oracle's C source,
+builds that copy, and runs the pins that cover the function it touches in a
+child process pointed at the copy (KBO_LIB).  At least one pin must fail.
+Only pins take part, never the stored golden records (which the oracle
+itself wrote).  The planted mistakes live here, in the test, on the CPU;
+the oracle's own sources are never modified."""
+import os
+import shutil
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+from oracle import build as oracle_build  # noqa: E402
+
+SCREEN = ["tests/test_oracle_screen.py"]
+PHILOX = ["tests/test_oracle_philox.py"]
+MAPS = ["tests/test_oracle_maps.py", "-k", "not all_inputs"]
+RUNG = ["tests/test_oracle_rung.py"]
+LOCATE = ["tests/test_oracle_locate.py"]
+
+# (name, source file, text, replacement, pins)
+MUTANTS = [
+    ("le_becomes_lt", "kbo.c", "if (d <= tol) return 1;", "if (d < tol) return 1;", SCREEN),
+    ("tolerance_fused", "kbo.c", "float tol = isfinite(r) ? atol + rtol * fabsf(r) : -1.0f;",
+     "float tol = isfinite(r) ? fmaf(rtol, fabsf(r), atol) : -1.0f;", SCREEN),
+    ("tolerance_scaled_by_candidate", "kbo.c", "float tol = isfinite(r) ? atol + rtol * fabsf(r) : -1.0f;",
+     "float tol = isfinite(r) ? atol + rtol * fabsf(c) : -1.0f;", SCREEN),
+    ("equality_clause_dropped", "kbo.c", "if (c == r) return 1; /*", "if (0) return 1; /*", SCREEN),
+    ("equal_nan_ignored", "kbo.c", "if ((flags & KBO_EQUAL_NAN) && isnan(c) && isnan(r)) return 1;",
+     "if (0) return 1;", SCREEN),
+    ("rel_error_over_candidate", "kbo.c", "float q = d / fabsf(r); /* x/0", "float q = d / fabsf(c); /* x/0",
+     SCREEN),
+    ("ref_squares_include_infinities", "kbo.c", "if (isfinite(r)) neumaier_add(&p->sum_sq_ref",
+     "if (!isnan(r)) neumaier_add(&p->sum_sq_ref", SCREEN),
+    ("diff_squares_include_infinities", "kbo.c",
+     "if (isfinite(c) && isfinite(r)) neumaier_add(&p->sum_sq_diff",
+     "if (!isnan(d)) neumaier_add(&p->sum_sq_diff", SCREEN),
+    ("bitwise_on_values", "kbo.c", "p->bitdiff |= cb ^ rb;", "p->bitdiff |= (uint32_t)(c != r);", SCREEN),
+    ("negative_inf_counted_as_positive", "kbo.c", "else if (c == -INFINITY) p->neg_inf_count++;",
+     "else if (c == -INFINITY) p->pos_inf_count++;", SCREEN),
+    ("rel_l2_without_sqrt", "kbo.c", "out->rel_l2 = ssr > 0.0 ? sqrt(ssd / ssr)",
+     "out->rel_l2 = ssr > 0.0 ? (ssd / ssr)", SCREEN),
+    ("philox_multiplier", "kbo.c", "#define PHILOX_M0 0xD2511F53u", "#define PHILOX_M0 0xD2511F55u", PHILOX),
+    ("philox_words_crossed", "kbo.c", "uint32_t y0 = hi1 ^ x1 ^ k0;", "uint32_t y0 = hi0 ^ x1 ^ k0;", PHILOX),
+    ("philox_key_schedule", "kbo.c", "k1 += PHILOX_W1;", "k1 += PHILOX_W0;", PHILOX),
+    ("stream_counter_words_swapped", "kbo.c",
+     "uint32_t ctr[4] = {(uint32_t)b, (uint32_t)(b >> 32), sub, stream_id};",
+     "uint32_t ctr[4] = {(uint32_t)b, (uint32_t)(b >> 32), stream_id, sub};", PHILOX),
+    ("uniform_wrong_bits", "kbo.c", "return (float)(x >> 8) * 0x1p-24f;", "return (float)(x >> 9) * 0x1p-23f;",
+     MAPS),
+    ("normal_sin_cos_swapped", "kbo.c", "double z = odd ? rho * sin(theta) : rho * cos(theta);",
+     "double z = odd ? rho * cos(theta) : rho * sin(theta);", MAPS),
+    ("normal_u1_without_offset", "kbo.c", "double u1 = ((double)xa + 1.0) * 0x1p-32;",
+     "double u1 = ((double)xa + 0.5) * 0x1p-32;", MAPS),
+    ("quantile_position", "kbo_rung.c", "const double h = (double)(n - 1) * p;",
+     "const double h = (double)n * p;", RUNG),
+    ("speedup_inverted", "kbo_rung.c", "r->speedup = r->valid ? b / r->mean : NAN;",
+     "r->speedup = r->valid ? r->mean / b : NAN;", RUNG),
+    ("locate_first_mismatch_last", "kbo.c",
+     "if (out->first_mismatch < 0 && !kbo_match(c, r, atol, rtol, flags))",
+     "if (!kbo_match(c, r, atol, rtol, flags))", LOCATE),
+]
+
+
+def _run_mutant(tmp, name, src, text, repl, pins):
+    """Build the oracle with one planted mistake and run the pins against
+    it: (pytest's exit code, the tail of its output)."""
+    os.makedirs(tmp, exist_ok=True)
+    odir = os.path.join(ROOT, "oracle")
+    for f in os.listdir(odir):
+        if f.endswith((".c", ".h")):
+            shutil.copy(os.path.join(odir, f), os.path.join(tmp, f))
+    path = os.path.join(tmp, src)
+    with open(path) as f:
+        code = f.read()
+    if code.count(text) != 1:
+        return -1, "mutation site of %s not found exactly once" % name
+    with open(path, "w") as f:
+        f.write(code.replace(text, repl))
+    lib = os.path.join(tmp, "libkbo_mutant.so")
+    sources = [os.path.join(tmp, os.path.basename(s)) for s in oracle_build.SOURCES]
+    subprocess.run(["gcc", *oracle_build.CFLAGS, *sources, "-o", lib, "-lm"], check=True,
+                   capture_output=True, text=True)
+    env = dict(os.environ, KBO_LIB=lib)
+    res = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                          *pins], cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return res.returncode, res.stdout[-2000:]
+
+
+@pytest.fixture(scope="module")
+def mutant_results(tmp_path_factory):
+    """Every mutant, built and run against its pins, a few at a time."""
+    base = str(tmp_path_factory.mktemp("mutants"))
+    with ThreadPoolExecutor(max_workers=max(1, min(6, (os.cpu_count() or 2) - 1))) as ex:
+        futs = {m[0]: ex.submit(_run_mutant, os.path.join(base, m[0]), *m) for m in MUTANTS}
+        return {k: f.result() for k, f in futs.items()}
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not available")
+@pytest.mark.parametrize("name", [m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(mutant_results, name):
+    rc, out = mutant_results[name]
+    # pytest exits with 1 when a test failed (2: interrupted or not collected)
+    assert rc == 1, "mutant %s: pins exited with %d (1 = a pin failed):\n%s" % (name, rc, out)
