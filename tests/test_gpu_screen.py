@@ -157,6 +157,78 @@ def test_random_ragged(dev, dt):
             run_case(ref, cands, atol, rtol, int(rng.integers(0, 2)), "%s n=%d K=%d" % (dt, n, K))
 
 
+# ------------------------------------- rare paths of the chunk loop ---
+# Each case reaches a rule of the definition that the kernel's fast path
+# only meets through a rare branch, at sizes that run the chunk loop (not
+# only the ragged tail, which applies the definition element by element).
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_signed_zero_is_the_only_difference(dev, dt):
+    """A candidate that differs from the reference only in the sign of one
+    zero: it matches everywhere, but it is not bitwise identical."""
+    say("signed zero only", dt)
+    rng = np.random.default_rng(31)
+    n = 512 * 64 + 7
+    r32 = rng.standard_normal(n).astype(np.float32)
+    r32[rng.integers(0, n, n // 10)] = 0.0
+    zeros = np.flatnonzero(r32 == 0.0)
+    inner = zeros[(zeros > 512 * 8) & (zeros < n - 512)]
+    conv = {"f32": lambda x: x, "f16": lambda x: x.astype(np.float16).view(np.uint16),
+            "bf16": lambda x: (x.view(np.uint32) >> 16).astype(np.uint16)}[dt]
+    r = conv(r32)
+    sign = np.float32(-0.0) if dt == "f32" else np.uint16(0x8000)
+    cands = []
+    for pos in (inner[0], inner[len(inner) // 2], zeros[-1]):
+        c = r.copy()
+        c[pos] = sign
+        cands.append(c)
+    recs = run_case(to_dev(r, dt, dev), [to_dev(c, dt, dev) for c in cands], 0.0, 0.0, 0, "signed zero " + dt)
+    assert all(x["bitwise_equal"] == 0 and x["mismatches"] == 0 for x in recs)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_all_differences_tiny(dev, dt):
+    """Differences all far below 2^-60: their binary32 squares would
+    underflow, so the sum of squared differences needs binary64 squares."""
+    say("tiny differences", dt)
+    rng = np.random.default_rng(32)
+    n = 512 * 48 + 100
+    r32 = (rng.standard_normal(n) * 2.0**-70).astype(np.float32)
+    c32 = (r32 * (1.0 + rng.uniform(-1, 1, n) * 2.0**-9)).astype(np.float32)
+    if dt == "bf16":
+        r = (r32.view(np.uint32) >> 16).astype(np.uint16)
+        c = (c32.view(np.uint32) >> 16).astype(np.uint16)
+    else:
+        r, c = r32, c32
+    recs = run_case(to_dev(r, dt, dev), [to_dev(c, dt, dev)], 0.0, 1e-3, 0, "tiny " + dt)
+    assert 0.0 < recs[0]["sum_sq_diff"] < 2.0**-140
+
+
+def test_max_rel_underflow_blind_spot(dev):
+    """The max-rel filter's blind spot: with subnormal references, the
+    residual d - O|r| of an element whose quotient exceeds the running
+    maximum O can round to zero.  Every wave first meets elements of
+    quotient fl(5/7) (r = 7 s, c = 12 s, s = 2^-149), then, in its last
+    chunk, elements of quotient fl(8/11) (r = 11 s, c = 19 s), whose
+    residual 8 s - fl(5/7) 11 s is below s / 2.  The record must hold
+    fl(8/11)."""
+    say("max-rel blind spot")
+    n = 1 << 21
+    plan = kb.kb_screen_launch(1, n, kb.KB_F32)
+    wstride = 4 * plan["blocks_per_group"]  # chunks per round of the group's waves
+    n_chunks = n // 512
+    assert n_chunks >= 2 * wstride, plan
+    s = np.float32(2.0**-149)
+    r = np.full(n, 7, dtype=np.float32) * s
+    c = np.full(n, 12, dtype=np.float32) * s
+    last = (n_chunks - wstride) * 512  # every wave's last chunk
+    r[last:] = np.float32(11) * s
+    c[last:] = np.float32(19) * s
+    recs = run_case(to_dev(r, "f32", dev), [to_dev(c, "f32", dev)], 0.0, 0.0, 0, "blind spot")
+    assert recs[0]["max_rel_err"] == float(np.float32(8.0) / np.float32(11.0))
+
+
 # ----------------------------------------------- the five workloads ---
 
 SCALED = [("c1", 1.0, None), ("c2", 1 / 64, None), ("c3", 1.0, None), ("c4", 1 / 64, None),
