@@ -202,6 +202,37 @@ def test_sparse_random_failures(dev, dt):
                 check_partial(g, o, "sparse %s cand %d" % (dt, k))
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_one_group_many_super_groups(dev, dt):
+    """Four candidates over millions of elements: one group, screened in one
+    round that spans every resident work-group, so the finish's second level
+    combines more than 48 super-groups, with the per-candidate read counts
+    and reference sums of the mode.  Three candidates pass (their records are
+    whole), one fails in its last element."""
+    n = 12 * (1 << 20) + 333
+    rng = np.random.default_rng(77)
+    r32 = rng.standard_normal(n).astype(np.float32)
+    cands = [(r32 + r32 * rng.uniform(-2e-3, 2e-3, n)).astype(np.float32) for _ in range(3)]
+    bad = r32.copy()
+    bad[n - 1] += np.float32(9.0)
+    cands.insert(2, bad)
+    plan = kb.kb_screen_launch(4, n, {"f32": kb.KB_F32, "bf16": kb.KB_BF16}[dt])
+    say("fail-fast one group", dt, plan)
+    assert plan["n_groups"] == 1 and (plan["blocks_per_group"] + 15) // 16 > 48, plan
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cd = [to_dev(CONV[dt](c), dt, dev) for c in cands]
+    full, fsum = kb.screen(ref, cd, ATOL, RTOL, 0)
+    fast, ssum = kb.screen(ref, cd, ATOL, RTOL, FF)
+    orc = oracle_records(ref, cd, ATOL, RTOL, 0)
+    assert_records_match(full, orc, "full one group %s" % dt)
+    assert ssum == fsum and fsum["n_failed"] == 1, (ssum, fsum)
+    for k, (g, f, o) in enumerate(zip(fast, full, orc)):
+        if o["mismatches"] == 0:
+            assert same_bits(g, f), (k, g, f)
+        else:
+            check_partial(g, o, "one group %s cand %d" % (dt, k))
+
+
 def test_workspace_left_clean(dev):
     """Fail, then pass, on one workspace and one record buffer: the second
     call must read the (now passing) candidates in full."""

@@ -98,6 +98,29 @@ def test_workloads(dev, name, scale, K):
     check(w.ref, w.cands, w.atol, w.rtol, 0, name)
 
 
+def test_max_rel_filter_near_misses(dev):
+    """The max-rel search filters with d - T a >= 0, T just below max_rel,
+    and confirms by division.  Here every chunk but the last full one holds
+    a near miss (ratio 0.5 - 2^-23, which passes the filter but is not the
+    maximum 0.5), so every wave meets one in its first chunk and must go on
+    to the one element whose ratio is 0.5, in the last full chunk.  binary32
+    only: the ratios of two 16-bit values cannot come that close to 0.5
+    without equalling it."""
+    n_chunks = 200
+    n = 512 * n_chunks + 77
+    rng = np.random.default_rng(31)
+    r32 = np.ones(n, np.float32)
+    c32 = r32.copy()
+    near = np.arange(n_chunks - 1) * 512 + rng.integers(0, 512, n_chunks - 1)
+    c32[near] = np.float32(1.5) - np.float32(2.0 ** -23)
+    hit = (n_chunks - 1) * 512 + 300
+    c32[hit] = 1.5
+    ref = to_dev(r32, "f32", dev)
+    cand = to_dev(c32, "f32", dev)
+    locs = check(ref, [cand], 1.0, 0.0, 0, "near misses")
+    assert locs[0] == {"first_mismatch": -1, "max_abs_index": hit, "max_rel_index": hit}, locs
+
+
 def test_rejected_and_identical(dev):
     r = torch.randn(5000, device=dev)
     cands = [r.clone(), None, r.to(torch.float16), r.clone()]

@@ -94,11 +94,17 @@ def test_gate_and_verdicts(dev):
         [perturb(out, 0.5, 2), perturb(lse, 1e-2, 3), perturb(aux, 0.1, 4)],  # fail everywhere
         [out.clone(), lse.clone(), aux.clone()],                        # bit-identical
         [out.clone(), lse.clone(), aux.t().contiguous().t()],           # layout in the last output
+        [out.half(), lse[:, :, :255].clone(), aux.clone()],             # dtype (0), then shape (1)
+        [out.clone(), None, aux.t().contiguous().t()],                  # missing (1), then layout (2)
     ]
     recs, summ, passed = compare(refs, cands, atol, rtol, 0, "gate")
-    assert passed == [1, 0, 0, 0, 0, 0, 0, 1, 0]
-    assert [recs[0][k]["status"] for k in range(9)] == [0, 0, 3, 2, 4, 1, 0, 0, 4]
-    assert summ["n_rejected"] == 5 and summ["n_failed"] == 2 and summ["n_passed"] == 2
+    assert passed == [1, 0, 0, 0, 0, 0, 0, 1, 0, 0, 0]
+    assert [recs[0][k]["status"] for k in range(11)] == [0, 0, 3, 2, 4, 1, 0, 0, 4, 2, 1]
+    # a candidate that fails the gate on several outputs carries the first
+    # failing check, in output order, in every output's record
+    assert [recs[o][9]["status"] for o in range(3)] == [2, 2, 2]
+    assert [recs[o][10]["status"] for o in range(3)] == [1, 1, 1]
+    assert summ["n_rejected"] == 7 and summ["n_failed"] == 2 and summ["n_passed"] == 2
     assert recs[1][1]["mismatches"] == 1 and recs[0][1]["mismatches"] == 0
     assert recs[2][7]["bitwise_equal"] == 1
 

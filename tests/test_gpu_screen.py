@@ -235,6 +235,32 @@ SCALED = [("c1", 1.0, None), ("c2", 1 / 64, None), ("c3", 1.0, None), ("c4", 1 /
           ("c5", 1 / 256, None)]
 
 
+# ------------------------------------------------------- launch shapes ---
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_one_group_many_super_groups(dev, dt):
+    """At most four candidates over millions of elements form one group that
+    gets a stripe per resident work-group: the finish's second level then
+    combines more than 48 super-groups of 16 stripes (more than 64 takes its
+    lanes two passes), which no other case reaches."""
+    n = 12 * (1 << 20) + 333
+    rng = np.random.default_rng(23)
+    r, cs = random_pair(rng, dt, n, 5)
+    code = {"f32": kb.KB_F32, "bf16": kb.KB_BF16}[dt]
+    atol, rtol = (1e-5, 1e-5) if dt == "f32" else (1e-3, 1e-3)
+    ref = to_dev(r, dt, dev)
+    for picks in ([2], [1, 2, 3, 4]):
+        K = len(picks)
+        plan = kb.kb_screen_launch(K, n, code)
+        S = (plan["blocks_per_group"] + 15) // 16
+        say("one group", dt, "K", K, plan, "super-groups", S)
+        assert plan["n_groups"] == 1 and S > 48, plan
+        cands = [to_dev(cs[i], dt, dev) for i in picks]
+        for flags in (0, kb.KB_EQUAL_NAN):
+            run_case(ref, cands, atol, rtol, flags, "%s one group K=%d flags=%d" % (dt, K, flags))
+        del cands
+
+
 @pytest.mark.parametrize("name,scale,K", SCALED)
 def test_workloads_scaled(dev, name, scale, K):
     say("workload", name, "scale", scale)
