@@ -11,9 +11,10 @@
 // A wave scans its chunks in increasing index order and stops looking for a
 // position as soon as one of its lanes has found it: every later chunk of
 // the wave holds larger indices.  On a failing candidate the first mismatch
-// is usually in a wave's first chunk.  Per element a cheap pass only ORs
-// three wave ballots (mismatch, d == max abs, the max-rel filter) into
-// scalar masks; a chunk whose masks show a hit is evaluated again from the
+// is usually in a wave's first chunk.  Each wave keeps two chunks' loads in
+// flight.  Per element a cheap, branch-free pass only ORs wave ballots (the
+// mismatch filter, d == max abs, the max-rel filter) into scalar masks; a
+// chunk whose masks show a hit is evaluated again from the
 // definitions into 8-bit lane masks, and its index formed (the lane's lowest
 // set bit, then a wave minimum by DPP).  The wave's finds are merged into
 // the output with a 64-bit atomic minimum ("none" is all-ones, which reads
@@ -60,18 +61,21 @@ struct LaneChunk {
 
 // One lane's part of chunk `chunk` of a tensor: base is wave-uniform (scalar
 // registers), off = 16 * lane, so a load is a scalar base plus the lane's
-// 32-bit offset.
-template <int DT>
+// 32-bit offset.  NT marks the loads nontemporal: each candidate byte is
+// read once, while the reference chunk is re-read by the work-groups of the
+// stripe's other candidates, which run on the same XCD, and should stay in
+// its L2.
+template <int DT, bool NT = true>
 __device__ __forceinline__ LaneChunk<DT> load_lane(const char* base, uint64_t chunk, uint32_t off) {
     LaneChunk<DT> x;
     typedef const __attribute__((address_space(1))) char* gbytes;
     const gbytes c = (gbytes)base + chunk * (DT == DT_F32 ? 2048u : 1024u);
     uint32_t o = off;
     asm volatile("" : "+v"(o));
-    const v4u32 a = __builtin_nontemporal_load((gvec)(c + o));
+    const v4u32 a = NT ? __builtin_nontemporal_load((gvec)(c + o)) : *(gvec)(c + o);
     x.w[0] = a.x; x.w[1] = a.y; x.w[2] = a.z; x.w[3] = a.w;
     if constexpr (DT == DT_F32) {
-        const v4u32 b = __builtin_nontemporal_load((gvec)(c + o + 1024u));
+        const v4u32 b = NT ? __builtin_nontemporal_load((gvec)(c + o + 1024u)) : *(gvec)(c + o + 1024u);
         x.w[4] = b.x; x.w[5] = b.y; x.w[6] = b.z; x.w[7] = b.w;
     }
     return x;
@@ -147,22 +151,29 @@ enum { REL_NONE = 0, REL_INF = 1, REL_ALL = 2, REL_FMA = 3 };
 template <int RM>
 __device__ __forceinline__ bool rel_candidate(float d, float a, float T) {
     if constexpr (RM == REL_NONE) return false;
-    else if constexpr (RM == REL_INF) return a == 0.f || d == __builtin_inff() || d >= a * 0x1p100f;
+    else if constexpr (RM == REL_INF) return (a == 0.f) | (d == __builtin_inff()) | (d >= a * 0x1p100f);
     else if constexpr (RM == REL_ALL) return true;
     else return fmaf(-T, a, d) >= 0.f;
 }
 
 // One chunk's cheap pass: per element only the wave ballots of the
-// mismatch predicate (M: still looked for), of d == max_abs and of the
+// mismatch filter (M: still looked for), of d == max_abs and of the
 // max-rel filter, OR-ed over the lane's elements (scalar masks, no per-lane
 // state).  A nonzero mask sends the wave to the exact pass.
+//
+// The mismatch filter is d > tol, or a reference that is not finite (class
+// test).  For a finite reference it is the predicate itself: c == r gives
+// d = 0 <= tol, and a NaN candidate gives a NaN d, which fails d <= tol; an
+// infinite or NaN reference always goes to the exact pass, which applies
+// the definition (tol = -1, and the equal_nan clause).  Written with
+// bitwise ORs of ballots, so that no element needs a branch.
 struct AnyHits {
     uint64_t m, a, r;
 };
 
 template <int DT, bool M, int RM>
 __device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const LaneChunk<DT>& cc, float atol,
-                                              float rtol, bool equal_nan, float max_abs, float T) {
+                                              float rtol, float max_abs, float T) {
     AnyHits h{0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -171,9 +182,9 @@ __device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const Lan
         const float d = fabsf(c - r);
         const float a = fabsf(r);
         if constexpr (M) {
-            const float tol = __builtin_isfinite(r) ? __fadd_rn(atol, __fmul_rn(rtol, a)) : -1.0f;
-            const bool match = (c == r) || (d <= tol) || (equal_nan && __builtin_isnan(c) && __builtin_isnan(r));
-            h.m |= ballot(!match);
+            const float tol = __fadd_rn(atol, __fmul_rn(rtol, a));
+            // class mask: signaling NaN, quiet NaN, -inf, +inf
+            h.m |= ballot(!(d <= tol)) | ballot(__builtin_amdgcn_classf(r, 0x207));
         }
         h.a |= ballot(d == max_abs);
         if constexpr (RM != REL_NONE) h.r |= ballot(rel_candidate<RM>(d, a, T));
@@ -183,11 +194,11 @@ __device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const Lan
 
 template <int DT, bool M>
 __device__ __forceinline__ AnyHits cheap_pass_rm(int rm, const LaneChunk<DT>& rc, const LaneChunk<DT>& cc,
-                                                 float atol, float rtol, bool equal_nan, float max_abs, float T) {
-    if (rm == REL_FMA) return cheap_pass<DT, M, REL_FMA>(rc, cc, atol, rtol, equal_nan, max_abs, T);
-    if (rm == REL_NONE) return cheap_pass<DT, M, REL_NONE>(rc, cc, atol, rtol, equal_nan, max_abs, T);
-    if (rm == REL_INF) return cheap_pass<DT, M, REL_INF>(rc, cc, atol, rtol, equal_nan, max_abs, T);
-    return cheap_pass<DT, M, REL_ALL>(rc, cc, atol, rtol, equal_nan, max_abs, T);
+                                                 float atol, float rtol, float max_abs, float T) {
+    if (rm == REL_FMA) return cheap_pass<DT, M, REL_FMA>(rc, cc, atol, rtol, max_abs, T);
+    if (rm == REL_NONE) return cheap_pass<DT, M, REL_NONE>(rc, cc, atol, rtol, max_abs, T);
+    if (rm == REL_INF) return cheap_pass<DT, M, REL_INF>(rc, cc, atol, rtol, max_abs, T);
+    return cheap_pass<DT, M, REL_ALL>(rc, cc, atol, rtol, max_abs, T);
 }
 
 // A pointer made explicitly wave-uniform (held in scalar registers), so that
@@ -233,17 +244,15 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
     const uint64_t n_chunks = p.numel / kChunk;
     const uint64_t wstride = (uint64_t)p.stripes * kWaves;
     const uint32_t off = 16u * (uint32_t)lane;
-    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave;
-         chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += wstride) {
-        const LaneChunk<DT> rc = load_lane<DT>(ref, chunk, off);
-        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, off);
+    // One chunk: the cheap pass, and the exact pass when a ballot is set.
+    auto scan = [&](uint64_t chunk, const LaneChunk<DT>& rc, const LaneChunk<DT>& cc) {
         // (readfirstlane: the choice of variant is a scalar branch)
         const int rm = __builtin_amdgcn_readfirstlane(need_rel ? rel_mode : REL_NONE);
         const AnyHits h = __builtin_amdgcn_readfirstlane(need_mism ? 1 : 0)
-                              ? cheap_pass_rm<DT, true>(rm, rc, cc, p.atol, p.rtol, equal_nan, max_abs, T)
-                              : cheap_pass_rm<DT, false>(rm, rc, cc, p.atol, p.rtol, equal_nan, max_abs, T);
+                              ? cheap_pass_rm<DT, true>(rm, rc, cc, p.atol, p.rtol, max_abs, T)
+                              : cheap_pass_rm<DT, false>(rm, rc, cc, p.atol, p.rtol, max_abs, T);
         const uint64_t any_m = h.m, any_a = need_abs ? h.a : 0u, any_r = h.r;
-        if ((any_m | any_a | any_r) == 0) continue;
+        if ((any_m | any_a | any_r) == 0) return;
         // Exact pass (rare): the definitions, element by element, into 8-bit
         // lane masks (bit i: element i of this lane qualifies); a position
         // found anywhere in this chunk is below everything later.
@@ -257,7 +266,9 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
             mr |= (uint32_t)h.rel << i;
         }
         const uint64_t base = chunk * kChunk;
-        if (any_m != 0) {
+        // (the mismatch and max-rel filters let through elements that the
+        // definitions then reject: a position only if a lane confirmed one)
+        if (any_m != 0 && ballot(mm != 0u)) {
             f_mism = base + wave_min_u32(first_in_lane<DT>(mm, lane));
             need_mism = false;
         }
@@ -269,6 +280,23 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
             f_rel = base + wave_min_u32(first_in_lane<DT>(mr, lane));
             need_rel = false;
         }
+    };
+    // Two chunks of the wave's range in flight: both are loaded before the
+    // first is scanned, and the second is scanned after it, so the scan
+    // order (and the early exit) is the wave's chunk order.
+    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave;
+         chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += 2 * wstride) {
+        const uint64_t next = chunk + wstride;
+        const bool two = next < n_chunks;
+        const LaneChunk<DT> rc = load_lane<DT, false>(ref, chunk, off);
+        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, off);
+        LaneChunk<DT> rn, cn;
+        if (two) {
+            rn = load_lane<DT, false>(ref, next, off);
+            cn = load_lane<DT>(cand, next, off);
+        }
+        scan(chunk, rc, cc);
+        if (two && (need_mism || need_abs || need_rel)) scan(next, rn, cn);
     }
     // Ragged tail (numel mod 512 elements): stripe 0, one element per thread.
     if (stripe == 0) {

@@ -121,6 +121,34 @@ def test_max_rel_filter_near_misses(dev):
     assert locs[0] == {"first_mismatch": -1, "max_abs_index": hit, "max_rel_index": hit}, locs
 
 
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_non_finite_references(dev, dt):
+    """References with +-inf and NaN scattered through many chunks.  The
+    cheap pass sends every such element to the exact pass, which applies the
+    definition (a non-finite reference matches only an equal candidate, or a
+    NaN one under KB_EQUAL_NAN)."""
+    n = 512 * 40 + 5
+    rng = np.random.default_rng(41)
+    r32 = rng.uniform(-2.0, 2.0, n).astype(np.float32)
+    special = rng.choice(n, size=n // 30, replace=False)
+    r32[special] = rng.choice(np.array([np.inf, -np.inf, np.nan], np.float32), size=special.size)
+    cands = [r32.copy() for _ in range(5)]
+    # 1: an infinity of the reference replaced by a finite value, late
+    late_inf = [i for i in special if np.isinf(r32[i]) and i > n // 2]
+    cands[1][late_inf[0]] = 1.0
+    # 2: in-tolerance noise on the finite elements only
+    fin = np.isfinite(r32)
+    cands[2][fin] = r32[fin] * (1 + rng.uniform(-1e-4, 1e-4, int(fin.sum()))).astype(np.float32)
+    # 3: an infinity of the opposite sign
+    cands[3][late_inf[-1]] = -r32[late_inf[-1]]
+    # 4: every NaN of the reference replaced by 0
+    cands[4][np.isnan(r32)] = 0.0
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cd = [to_dev(CONV[dt](c), dt, dev) for c in cands]
+    for flags in (0, kb.KB_EQUAL_NAN):
+        check(ref, cd, 1e-2, 1e-2, flags, "%s non-finite flags=%d" % (dt, flags))
+
+
 def test_rejected_and_identical(dev):
     r = torch.randn(5000, device=dev)
     cands = [r.clone(), None, r.to(torch.float16), r.clone()]
