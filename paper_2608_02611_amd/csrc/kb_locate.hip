@@ -11,8 +11,8 @@
 // A wave scans its chunks in increasing index order and stops looking for a
 // position as soon as one of its lanes has found it: every later chunk of
 // the wave holds larger indices.  On a failing candidate the first mismatch
-// is usually in a wave's first chunk.  Each wave keeps two chunks' loads in
-// flight.  Per element a cheap, branch-free pass only ORs wave ballots (the
+// is usually in a wave's first chunk.  Each wave loads two chunks ahead of
+// the two it scans.  Per element a cheap, branch-free pass only ORs wave ballots (the
 // mismatch filter, d == max abs, the max-rel filter) into scalar masks; a
 // chunk whose masks show a hit is evaluated again from the
 // definitions into 8-bit lane masks, and its index formed (the lane's lowest
@@ -281,22 +281,32 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
             need_rel = false;
         }
     };
-    // Two chunks of the wave's range in flight: both are loaded before the
-    // first is scanned, and the second is scanned after it, so the scan
-    // order (and the early exit) is the wave's chunk order.
-    for (uint64_t chunk = (uint64_t)stripe * kWaves + wave;
-         chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += 2 * wstride) {
-        const uint64_t next = chunk + wstride;
-        const bool two = next < n_chunks;
-        const LaneChunk<DT> rc = load_lane<DT, false>(ref, chunk, off);
-        const LaneChunk<DT> cc = load_lane<DT>(cand, chunk, off);
-        LaneChunk<DT> rn, cn;
-        if (two) {
-            rn = load_lane<DT, false>(ref, next, off);
-            cn = load_lane<DT>(cand, next, off);
+    // Software pipeline, two chunks deep: the next two chunks of the wave's
+    // range are loaded before the current two are scanned, so the scan
+    // order (and the early exit) is the wave's chunk order.  A load past the
+    // wave's last chunk is redirected to a chunk the wave reads anyway (every
+    // index stays inside the tensor), and its data is not scanned.
+    uint64_t chunk = (uint64_t)stripe * kWaves + wave;
+    if (chunk < n_chunks) {
+        const uint64_t c1 = chunk + wstride < n_chunks ? chunk + wstride : chunk;
+        LaneChunk<DT> ra = load_lane<DT, false>(ref, chunk, off);
+        LaneChunk<DT> ca = load_lane<DT>(cand, chunk, off);
+        LaneChunk<DT> rb = load_lane<DT, false>(ref, c1, off);
+        LaneChunk<DT> cb = load_lane<DT>(cand, c1, off);
+        for (; chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += 2 * wstride) {
+            const uint64_t n0 = chunk + 2 * wstride, n1 = chunk + 3 * wstride;
+            const uint64_t l0 = n0 < n_chunks ? n0 : chunk, l1 = n1 < n_chunks ? n1 : chunk;
+            const LaneChunk<DT> rn0 = load_lane<DT, false>(ref, l0, off);
+            const LaneChunk<DT> cn0 = load_lane<DT>(cand, l0, off);
+            const LaneChunk<DT> rn1 = load_lane<DT, false>(ref, l1, off);
+            const LaneChunk<DT> cn1 = load_lane<DT>(cand, l1, off);
+            scan(chunk, ra, ca);
+            if (chunk + wstride < n_chunks && (need_mism || need_abs || need_rel)) scan(chunk + wstride, rb, cb);
+            ra = rn0;
+            ca = cn0;
+            rb = rn1;
+            cb = cn1;
         }
-        scan(chunk, rc, cc);
-        if (two && (need_mism || need_abs || need_rel)) scan(next, rn, cn);
     }
     // Ragged tail (numel mod 512 elements): stripe 0, one element per thread.
     if (stripe == 0) {

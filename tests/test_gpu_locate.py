@@ -149,6 +149,17 @@ def test_non_finite_references(dev, dt):
         check(ref, cd, 1e-2, 1e-2, flags, "%s non-finite flags=%d" % (dt, flags))
 
 
+def test_workload_c2_full_size(dev):
+    """The 16-candidate 4096 x 4096 bf16 workload at its full size, the
+    position search bench.py times."""
+    w = synth.build("c2", dev, seed=0)
+    torch.cuda.synchronize()
+    locs = check(w.ref, w.cands, w.atol, w.rtol, 0, "c2 full")
+    assert sum(l["first_mismatch"] >= 0 for l in locs) > 0 and all(l["max_abs_index"] >= 0 for l in locs)
+    del w
+    torch.cuda.empty_cache()
+
+
 def test_rejected_and_identical(dev):
     r = torch.randn(5000, device=dev)
     cands = [r.clone(), None, r.to(torch.float16), r.clone()]
