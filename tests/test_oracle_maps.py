@@ -163,6 +163,45 @@ def test_f32_to_bf16_all_inputs():
         assert all(ex.map(check, _chunks(1 << 32, 1 << 24)))
 
 
+def _conversion_sample():
+    """About 3 M binary32 bit patterns: a prime stride over all of them, every
+    pattern whose value rounds into or near the binary16 subnormals or near
+    the binary16 overflow threshold (sampled with a small stride), the exact
+    halfway cases of both narrowings under random upper bits, and NaNs whose
+    payload sits only in the low bits."""
+    rng = np.random.default_rng(2024)
+    parts = [np.arange(0, 1 << 32, 2039, dtype=np.uint64)]
+    for e_lo, e_hi in ((96, 114), (140, 144)):  # exponent fields: f16 subnormal targets, near 65520
+        parts.append(np.arange(e_lo << 23, e_hi << 23, 61, dtype=np.uint64))
+    hi = rng.integers(0, 1 << 19, 1 << 16, dtype=np.uint64)
+    parts.append((hi << 13) | 0x1000)            # f16 halfway (13 dropped bits)
+    parts.append(((hi << 16) & 0xFFFF0000) | 0x8000)  # bf16 halfway (16 dropped bits)
+    parts.append(np.array([0x7F800001, 0xFF800001, 0x7F80FFFF, 0x7FC00000, 0x477FEFFF, 0x477FF000,
+                           0x477FE000, 0x33000000, 0x33000001, 0x337FFFFF, 0x387FC000, 0x387FE000],
+                          dtype=np.uint64))
+    x = np.concatenate(parts) & 0xFFFFFFFF
+    x = np.concatenate([x, x ^ (1 << 31)])  # both signs
+    return x.astype(np.uint32).view(np.float32)
+
+
+def test_conversions_sampled():
+    """The two narrowings on a sample that reaches every branch of the
+    definition (numpy's binary16 and torch's bfloat16 as references); the
+    exhaustive tests below cover every input."""
+    import torch
+    x = _conversion_sample()
+    nan = np.isnan(x)
+    got = oracle.f32_to_f16_n(x)
+    with np.errstate(over="ignore", invalid="ignore"):
+        want = x.astype(np.float16).view(np.uint16)
+    assert np.array_equal(got[~nan], want[~nan])
+    assert np.all((got[nan] & 0x7FFF) == 0x7E00)
+    got = oracle.f32_to_bf16_n(x)
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got[~nan], want[~nan])
+    assert np.all((got[nan] & 0x7FFF) == 0x7FC0)
+
+
 def test_widenings_all_inputs():
     import torch
     h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)

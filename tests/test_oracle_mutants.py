@@ -21,7 +21,8 @@ from oracle import build as oracle_build  # noqa: E402
 
 SCREEN = ["tests/test_oracle_screen.py"]
 PHILOX = ["tests/test_oracle_philox.py"]
-MAPS = ["tests/test_oracle_maps.py", "-k", "not all_inputs"]
+# (the two exhaustive narrowing tests take a minute; the sampled one stands in for them)
+MAPS = ["tests/test_oracle_maps.py", "-k", "not f32_to_f16_all_inputs and not f32_to_bf16_all_inputs"]
 RUNG = ["tests/test_oracle_rung.py"]
 LOCATE = ["tests/test_oracle_locate.py"]
 
@@ -72,6 +73,32 @@ MUTANTS = [
     ("locate_first_mismatch_last", "kbo.c",
      "if (out->first_mismatch < 0 && !kbo_match(c, r, atol, rtol, flags))",
      "if (!kbo_match(c, r, atol, rtol, flags))", LOCATE),
+    ("locate_max_abs_last", "kbo.c", "if (out->max_abs_index < 0 && max_abs > 0.0f && d == max_abs)",
+     "if (max_abs > 0.0f && d == max_abs)", LOCATE),
+    ("locate_max_rel_of_candidate", "kbo.c", "float q = d / fabsf(r);\n        if (out->first_mismatch",
+     "float q = d / fabsf(c);\n        if (out->first_mismatch", LOCATE),
+    # the promotion decision and the survival table
+    ("promote_ties_to_higher_index", "kbo_rung.c", "return key[j] > key[i] || (key[j] == key[i] && j < i);",
+     "return key[j] > key[i] || (key[j] == key[i] && j > i);", RUNG),
+    ("promote_keep_rounded_down", "kbo_rung.c", "((long long)n_eligible * num + den - 1) / den",
+     "((long long)n_eligible * num) / den", RUNG),
+    ("promote_invalid_baseline", "kbo_rung.c", "p = valid[i] != 0;", "p = 1;", RUNG),
+    ("promote_baseline_counted_eligible", "kbo_rung.c", "n_eligible += valid[i] && i != base;",
+     "n_eligible += valid[i];", RUNG),
+    ("promote_invalid_ranked_by_score", "kbo_rung.c",
+     "key[i] = valid[i] && !isnan(score[i]) ? score[i] : -INFINITY;",
+     "key[i] = !isnan(score[i]) ? score[i] : -INFINITY;", RUNG),
+    ("survival_fail_over_original", "kbo_rung.c",
+     "100.0 * (double)failed[r] / (double)entering[r]", "100.0 * (double)failed[r] / (double)original", RUNG),
+    # binary32 -> binary16 / bfloat16 rounding and back
+    ("rounding_ties_away", "kbo.c", "if (rem > half || (rem == half && (q & 1))) q++;",
+     "if (rem >= half) q++;", MAPS),
+    ("f16_overflow_saturates", "kbo.c", "mag = enc >= 0x7c00u ? 0x7c00u : (uint32_t)enc;",
+     "mag = enc >= 0x7c00u ? 0x7bffu : (uint32_t)enc;", MAPS),
+    ("f16_subnormal_scale", "kbo.c", "q = shift_rne(m, -e - 1);", "q = shift_rne(m, -e);", MAPS),
+    ("bf16_nan_truncated", "kbo.c", "if (mag > 0x7f800000u) return (uint16_t)(sign | 0x7fc0u);",
+     "if (mag > 0x7f800000u) return (uint16_t)(sign | (mag >> 16));", MAPS),
+    ("f16_widen_subnormal_scale", "kbo.c", "ldexpf((float)man, -24)", "ldexpf((float)man, -25)", MAPS),
 ]
 
 
