@@ -62,6 +62,9 @@ __device__ __forceinline__ uint16_t f32_to_f16_bits(float f) {
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
     uint32_t u = __float_as_uint(f);
+    // NaN: the quiet NaN with the sign kept (rounding the bits would turn a
+    // NaN whose payload lies in the dropped half into infinity)
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)(((u >> 16) & 0x8000u) | 0x7FC0u);
     u += 0x7FFFu + ((u >> 16) & 1u);  // ties to even on the dropped half
     return (uint16_t)(u >> 16);
 }

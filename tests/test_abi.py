@@ -191,6 +191,31 @@ def test_summarize_on_host(L):
     assert kb.lib().kb_summarize(None, 3, None) == kb.KB_ERR_INVALID_ARG
 
 
+def test_summarize_matches_the_verdict_rule(L):
+    """The verdict: a candidate passes iff the gate accepted it and it has no
+    mismatch (one is enough to fail, and counts past 2^32 are counts);
+    first_failed is the first candidate that did not pass."""
+    import numpy as np
+    rng = np.random.default_rng(3)
+    statuses = [kb.KB_STATUS_OK] * 4 + [kb.KB_REJECT_NULL, kb.KB_REJECT_DTYPE, kb.KB_REJECT_SHAPE,
+                                        kb.KB_REJECT_LAYOUT]
+    for trial in range(200):
+        n = int(rng.integers(1, 40))
+        recs = []
+        for _ in range(n):
+            r = {name: 0 for name, _ in kb.KbStats._fields_}
+            r["status"] = statuses[int(rng.integers(0, len(statuses)))]
+            r["mismatches"] = int(rng.choice([0, 0, 1, 2, 1 << 32, (1 << 40) + 1]))
+            recs.append(r)
+        ok = [r["status"] == kb.KB_STATUS_OK and r["mismatches"] == 0 for r in recs]
+        rej = [r["status"] != kb.KB_STATUS_OK for r in recs]
+        want = {"n_candidates": n, "n_passed": sum(ok), "n_rejected": sum(rej),
+                "n_failed": n - sum(ok) - sum(rej),
+                "first_passed": ok.index(True) if any(ok) else -1,
+                "first_failed": ok.index(False) if not all(ok) else -1}
+        assert kb.kb_summarize(recs) == want, (trial, recs)
+
+
 def test_workspace_init_argument_errors(L):
     f = kb.lib().kb_screen_workspace_init
     assert f(None, 256, None) == kb.KB_ERR_WORKSPACE
