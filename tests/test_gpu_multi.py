@@ -134,6 +134,34 @@ def test_many_candidates(dev, flags):
     compare(refs, cands, atol, rtol, flags, "many flags=%d" % flags)
 
 
+def test_attention_pair_full_size(dev):
+    """The output pair the benchmark screens, at its size: out fp16
+    [4, 32, 2048, 128] and lse fp32 [4, 32, 2048], 16 candidates with
+    in-tolerance noise, two of them wrong in one output.  Every record
+    against the oracle's (host threads over chunks of the outputs)."""
+    from tests.helpers import oracle_records
+    g = torch.Generator(device=dev).manual_seed(3)
+    out = torch.randn(4, 32, 2048, 128, generator=g, device=dev).to(torch.float16)
+    lse = torch.randn(4, 32, 2048, generator=g, device=dev) + 8.0
+    refs = [out, lse]
+    atol, rtol = [1e-2, 1e-4], [1e-2, 1e-4]
+    cands = []
+    for k in range(16):
+        gk = torch.Generator(device=dev).manual_seed(100 + k)
+        o = (out.float() * (1 + 1e-3 * torch.randn(out.shape, generator=gk, device=dev))).to(torch.float16)
+        l = lse + 1e-6 * torch.randn(lse.shape, generator=gk, device=dev)
+        cands.append([o, l])
+    cands[3][1][1, 7, 1000] += 1.0
+    cands[9][0][2, 3, 17, 5] = float("nan")
+    say("attention pair full size")
+    g_recs, g_summ, g_passed = kb.screen_multi(refs, cands, atol, rtol, 0)
+    for o in range(2):
+        want = oracle_records(refs[o], [c[o] for c in cands], atol[o], rtol[o], 0)
+        assert_records_match(g_recs[o], want, "attention pair output %d" % o)
+    assert g_passed == [int(k not in (3, 9)) for k in range(16)], g_passed
+    assert g_summ["n_passed"] == 14
+
+
 def test_single_output_equals_kb_screen(dev):
     ref = torch.randn(70001, device=dev)
     cands = [ref + 1e-6 * torch.randn(70001, device=dev) for _ in range(5)]
