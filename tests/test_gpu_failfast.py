@@ -233,6 +233,27 @@ def test_one_group_many_super_groups(dev, dt):
             check_partial(g, o, "one group %s cand %d" % (dt, k))
 
 
+def test_workload_c2_full_size(dev):
+    """The fail-fast screen bench.py times: the 16-candidate 4096 x 4096
+    bf16 workload at its full size."""
+    import synth
+    w = synth.build("c2", dev, seed=0)
+    torch.cuda.synchronize()
+    say("fail-fast c2 full size")
+    full, fsum = kb.screen(w.ref, w.cands, w.atol, w.rtol, 0)
+    fast, ssum = kb.screen(w.ref, w.cands, w.atol, w.rtol, FF)
+    orc = oracle_records(w.ref, w.cands, w.atol, w.rtol, 0)
+    assert_records_match(full, orc, "c2 full")
+    assert ssum == fsum and fsum["n_failed"] > 0 and fsum["n_passed"] > 0, (ssum, fsum)
+    for k, (g, f, o) in enumerate(zip(fast, full, orc)):
+        if o["mismatches"] == 0:
+            assert same_bits(g, f), (k, g, f)
+        else:
+            check_partial(g, o, "c2 full cand %d" % k)
+    del w
+    torch.cuda.empty_cache()
+
+
 def test_workspace_left_clean(dev):
     """Fail, then pass, on one workspace and one record buffer: the second
     call must read the (now passing) candidates in full."""
