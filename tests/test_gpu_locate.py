@@ -43,6 +43,10 @@ def oracle_positions(ref, cands, atol, rtol, flags=0):
     return out
 
 
+def say(*a):
+    print(*a, flush=True)
+
+
 def check(ref, cands, atol, rtol, flags=0, label=""):
     recs, locs = kb.locate(ref, cands, atol, rtol, flags)
     want = oracle_positions(ref, cands, atol, rtol, flags)
@@ -157,6 +161,36 @@ def test_workload_c2_full_size(dev):
     locs = check(w.ref, w.cands, w.atol, w.rtol, 0, "c2 full")
     assert sum(l["first_mismatch"] >= 0 for l in locs) > 0 and all(l["max_abs_index"] >= 0 for l in locs)
     del w
+    torch.cuda.empty_cache()
+
+
+def test_indices_beyond_32_bits(dev):
+    """2^32 + 777 bf16 elements (8.6 GB per tensor): element indices and
+    counts past 32 bits in the screen and the position search.  The
+    candidate is the reference except at three planted elements, so the
+    expected record and positions follow from the construction (the oracle
+    would take minutes over 4 G elements): a difference of 4 below 2^32,
+    and a tie of the largest difference 8 (relative error 8) at 2^32 + 5,
+    in the last whole chunk, and in the ragged tail."""
+    n = (1 << 32) + 777
+    ref = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    kb.kb_gen_inputs(ref, kb.KB_DIST_NORMAL, 0.0, 1.0, seed=5, stream_id=0x3232)
+    cand = ref.clone()
+    low, high, tail = 3 << 30, (1 << 32) + 5, n - 3
+    assert high < (n // 512) * 512 <= tail
+    for i, c in ((low, 5.0), (high, 9.0), (tail, 9.0)):
+        ref[i] = 1.0
+        cand[i] = c
+    torch.cuda.synchronize()
+    say("indices beyond 32 bits")
+    recs, locs = kb.locate(ref, [cand], 1e-2, 1e-2)
+    r = recs[0]
+    assert r["numel"] == n and r["mismatches"] == 3 and r["nan_count"] == 0, r
+    assert r["max_abs_err"] == 8.0 and r["max_rel_err"] == 8.0 and r["bitwise_equal"] == 0, r
+    assert r["sum_sq_diff"] == 16.0 + 64.0 + 64.0, r
+    assert 0.99 * n < r["sum_sq_ref"] < 1.01 * n, r
+    assert locs[0] == {"first_mismatch": low, "max_abs_index": high, "max_rel_index": high}, locs
+    del ref, cand
     torch.cuda.empty_cache()
 
 
