@@ -190,7 +190,15 @@ def test_indices_beyond_32_bits(dev):
     assert r["sum_sq_diff"] == 16.0 + 64.0 + 64.0, r
     assert 0.99 * n < r["sum_sq_ref"] < 1.01 * n, r
     assert locs[0] == {"first_mismatch": low, "max_abs_index": high, "max_rel_index": high}, locs
-    del ref, cand
+    # fail-fast: a passing copy is read in full (its element count, summed
+    # over work-groups, is past 2^32) and its record is the plain one
+    same = ref.clone()
+    full, _ = kb.screen(ref, [cand, same], 1e-2, 1e-2, 0)
+    fast, summ = kb.screen(ref, [cand, same], 1e-2, 1e-2, kb.KB_FAIL_FAST)
+    assert summ["n_failed"] == 1 and summ["n_passed"] == 1, summ
+    assert fast[1] == full[1] and full[1]["numel"] == n and full[1]["bitwise_equal"] == 1, (fast[1], full[1])
+    assert 1 <= fast[0]["mismatches"] <= 3 and fast[0]["numel"] <= n, fast[0]
+    del ref, cand, same
     torch.cuda.empty_cache()
 
 
