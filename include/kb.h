@@ -37,8 +37,12 @@
  *   - kb_gen_inputs and kb_screen are asynchronous and stream-ordered on the
  *     given hipStream_t (NULL = the default stream).  kb_screen_stats
  *     synchronizes that stream.
- *   - The library allocates no device memory.  It keeps one small pinned
- *     host staging ring per process for the launch tables it uploads.
+ *   - The library allocates no device memory and keeps no mutable state
+ *     beyond the calling thread's error text and a per-process cache of
+ *     kernel occupancy queries (and, for kb_screen_noalloc, the address of
+ *     its fixed device scratch on each device).  A call with more than
+ *     KB_INLINE_CANDS candidates is given a launch-table buffer of the
+ *     caller's pinned host memory (kb_screen_ex, kb_screen_multi).
  *   - Device buffers must be 16-byte aligned (hipMalloc and torch
  *     allocations are); element counts may be anything, including 0.
  *   - A "data pointer" of a tensor points at element 0; strides are in
@@ -103,7 +107,8 @@ typedef struct kb_tensor {
 } kb_tensor;
 
 /* Per-candidate screening record, 80 bytes, written to device memory by
- * kb_screen.  For a candidate that passed the policy gate:
+ * kb_screen (kb_summarize and kb_screen_stats give each record's pass/fail
+ * verdict K(p)).  For a candidate that passed the policy gate:
  *   numel          elements compared (= reference numel);
  *   mismatches     elements with NOT match, where match means c == r
  *                  (IEEE equality: +0 == -0, equal infinities), or
@@ -124,7 +129,8 @@ typedef struct kb_tensor {
  *   max_rel_err    max over elements of |c - r| / |r| (binary32 division),
  *                  NaN quotients (0/0, inf/inf) ignored, 0 if none;
  *   bitwise_equal  1 iff every stored element is bit-identical;
- *   status         KB_STATUS_OK.
+ *   status         KB_STATUS_OK (KB_ERR_WORKSPACE, every other field zero,
+ *                  when the call found its workspace not clean).
  * Counts, flags and maxima are exact; the two sums are binary64 sums in a
  * fixed order (deterministic from call to call, within 1e-6 relative of the
  * exact sums).  A rejected candidate has status = KB_REJECT_* and every
@@ -135,8 +141,11 @@ typedef struct kb_tensor {
  * being their count (<= the reference numel) and every other field the
  * definition above restricted to them (sum_sq_ref included); mismatches is
  * still >= 1, so the verdict is the same.  Which elements were compared
- * depends on timing.  A candidate without mismatch is always read in full
- * and its record is bit-identical to the one written without the flag. */
+ * depends on timing.  A candidate without mismatch is always read in full:
+ * its counts, flags and maxima equal those written without the flag, and its
+ * two sums (and rel_l2) agree with them within 1e-6 relative -- the same
+ * definition, summed over another split of the work, so not always the same
+ * bits. */
 typedef struct kb_stats {
     uint64_t numel;
     uint64_t mismatches;
@@ -207,12 +216,17 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype);
 
 /* Zero-fill a workspace (a fill kernel, stream-ordered; no memset node, so
- * it may be captured in a graph).  A workspace must be initialised this way
- * (or zero-filled otherwise) after it is allocated, and again before it is
- * used for a call with different (n_cands, numel, dtype) or after anything
- * else wrote to it: kb_screen keeps cross-work-group counters in it and
- * leaves them zero when the call completes, so consecutive calls with the
- * same sizes need no re-initialisation.
+ * it may be captured in a graph).  A workspace must be zero-filled this way
+ * (or otherwise) once after it is allocated, and again before it is used for
+ * a call with other (n_cands, numel, dtype) or after anything else wrote to
+ * it.  kb_screen keeps cross-work-group counters in it and leaves them zero
+ * when the call completes, so consecutive calls with the same sizes need
+ * nothing.  A call that finds a counter that did not begin at zero (the
+ * contract broken, or a call cut short) does not trust it: the records of
+ * the affected candidates get status KB_ERR_WORKSPACE, and kb_screen_stats,
+ * kb_summarize and kb_summarize_multi then return KB_ERR_WORKSPACE, so a
+ * dirty workspace gives an error, never wrong records (up to a 2^-32 chance
+ * per counter that a leftover value passes the check).
  *   workspace: device, 16-byte aligned; workspace_bytes: multiple of 16.
  * Errors: KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
 int kb_screen_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
@@ -238,30 +252,69 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out);
  *                failed stop reading the reference too;
  *   workspace    device scratch of workspace_bytes >=
  *                kb_screen_workspace_bytes(n_cands, numel, dtype),
- *                initialised by kb_screen_workspace_init (see there); one
+ *                zero-filled as kb_screen_workspace_init describes; one
  *                workspace must not be used by two calls that can run
  *                concurrently;
  *   d_stats      n_cands kb_stats written by the kernel: device memory, or
  *                pinned host memory mapped for the device (hipHostMalloc),
  *                which lets a pipelined caller read the records without a
  *                copy once the stream has passed the call.
- * Candidate k's record goes to d_stats[k].  Returns KB_OK once the work is
- * enqueued.  Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_DTYPE,
- * KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT (reference, accepted candidate,
- * workspace or d_stats not 16-byte aligned), KB_ERR_HIP. */
+ * Candidate k's record goes to d_stats[k].  At most KB_INLINE_CANDS
+ * candidates: the launch table travels in the kernel arguments; more need
+ * kb_screen_ex with a host table.  Returns KB_OK once the work is enqueued.
+ * Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_DTYPE,
+ * KB_ERR_WORKSPACE (workspace too small, or more than KB_INLINE_CANDS
+ * candidates), KB_ERR_ALIGNMENT (reference, accepted candidate, workspace or
+ * d_stats not 16-byte aligned), KB_ERR_HIP. */
 int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
               float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
               kb_stats* d_stats, hipStream_t stream);
 
-/* Verdict summary of n_cands records already in host memory (host only). */
-int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary);
+/* Candidates whose launch table (16 bytes per candidate) travels in the
+ * kernel arguments. */
+#define KB_INLINE_CANDS 128
+
+/* Options of kb_screen_ex (all-zero = none). */
+typedef struct kb_screen_opts {
+    /* Launch table of a call with more than KB_INLINE_CANDS candidates:
+     * pinned host memory (hipHostMalloc, or a pinned torch tensor) owned by
+     * the caller, 16-byte aligned, of host_table_bytes >=
+     * kb_screen_host_table_bytes(n_cands).  The library writes the table
+     * there during the call and the kernels read it from there, so the caller
+     * leaves it untouched until the stream has passed the call (reusing it
+     * earlier, e.g. for the next call, races).  Ignored for smaller calls. */
+    void* host_table;
+    size_t host_table_bytes;
+} kb_screen_opts;
+
+/* Bytes of pinned host memory kb_screen_ex needs for n_cands candidates:
+ * 0 for n_cands <= KB_INLINE_CANDS (and for n_cands < 1). */
+size_t kb_screen_host_table_bytes(int n_cands);
+
+/* kb_screen with options (opts may be NULL: then exactly kb_screen).
+ * Errors as for kb_screen; KB_ERR_WORKSPACE also when a host table is needed
+ * and missing or short, KB_ERR_ALIGNMENT when it is misaligned. */
+int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+                 float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
+                 kb_stats* d_stats, const kb_screen_opts* opts, hipStream_t stream);
+
+/* The verdict of each of n_cands records already in host memory (host only):
+ * candidate k passes -- K(p) = 1 for its output -- iff status is
+ * KB_STATUS_OK and mismatches is 0 (Section 3.1's correctness indicator;
+ * Algorithm 1 rejects a candidate that fails the policy check or the
+ * Verifier's test).  passed: optional host array of n_cands flags (1 =
+ * passed); summary: optional counts.  Errors: KB_ERR_INVALID_ARG,
+ * KB_ERR_WORKSPACE (a record has that status: see kb_screen_workspace_init). */
+int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary, int32_t* passed);
 
 /* Copy n_cands records from device d_stats to host h_stats (may be NULL),
- * synchronize `stream`, and fill *summary (may be NULL).  This is the
- * readback and verdict step of Algorithm 1's reject-on-failure gates.
- * Errors: KB_ERR_INVALID_ARG, KB_ERR_HIP. */
+ * synchronize `stream`, and give the verdicts of kb_summarize in *summary
+ * and passed[] (each may be NULL).  This is the readback and verdict step of
+ * Algorithm 1's reject-on-failure gates.  Errors: KB_ERR_INVALID_ARG,
+ * KB_ERR_HIP, KB_ERR_WORKSPACE (the call that wrote the records found its
+ * workspace not clean; see kb_screen_workspace_init). */
 int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats,
-                    kb_summary* summary, hipStream_t stream);
+                    kb_summary* summary, int32_t* passed, hipStream_t stream);
 
 /* Positions of the first mismatch and of the maxima of each candidate: the
  * element-level detail that the feedback about a failed candidate carries
@@ -292,9 +345,12 @@ int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, 
 
 /* Bytes of device workspace kb_screen_multi needs (0 on invalid arguments):
  * the sum, over outputs, of kb_screen_workspace_bytes for that output's
- * reference, each rounded up to 256.  Initialise it with
- * kb_screen_workspace_init (same contract as for kb_screen). */
+ * reference, each rounded up to 256.  Zero-filled as for kb_screen. */
 size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int n_cands);
+
+/* Bytes of pinned host table kb_screen_multi needs: n_outputs times
+ * kb_screen_host_table_bytes(n_cands) (each output has its own table). */
+size_t kb_screen_multi_host_table_bytes(int n_outputs, int n_cands);
 
 /* Screen candidates whose output is a tuple of n_outputs tensors against a
  * tuple of references (a kernel returning several tensors: the
@@ -307,7 +363,9 @@ size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int
  *   atol, rtol  host arrays of n_outputs tolerances;
  *   flags       as for kb_screen, applied to every output;
  *   d_stats     n_outputs * n_cands records, output-major: output o of
- *               candidate k at d_stats[o * n_cands + k].
+ *               candidate k at d_stats[o * n_cands + k];
+ *   opts        as for kb_screen_ex (may be NULL); a host table must hold
+ *               kb_screen_multi_host_table_bytes(n_outputs, n_cands).
  * One gate over all outputs: candidate k is accepted only if every output
  * passes kb_policy_check against its reference; otherwise no output of it
  * is read and every one of its records has status = the first failing check
@@ -316,7 +374,8 @@ size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int
  * another on `stream`.  Errors (nothing launched) as for kb_screen. */
 int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands, int n_cands,
                     const float* atol, const float* rtol, uint32_t flags, void* workspace,
-                    size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream);
+                    size_t workspace_bytes, kb_stats* d_stats, const kb_screen_opts* opts,
+                    hipStream_t stream);
 
 /* Verdict over multi-output records in host memory (output-major, as
  * kb_screen_multi writes them): a candidate passes iff every output has
@@ -401,8 +460,8 @@ int kb_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, 
  *             ceil(n_eligible frac_num / frac_den) valid non-baseline
  *             candidates in rank order (n_eligible = their count, computed
  *             in integers) and for a valid baseline, which is always
- *             carried to the next rung (Fig. 4: "6 candidates + baseline");
- *             0 for the pruned.
+ *             carried to the next rung (Fig. 4 shows the baseline promoted
+ *             beside the top candidates at every rung); 0 for the pruned.
  * All arrays 4-byte aligned (scores 8).  n_cands <= KB_PROMOTE_MAX.
  * Errors (nothing launched): KB_ERR_INVALID_ARG, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
 #define KB_PROMOTE_MAX 65536

@@ -42,8 +42,8 @@
  *           last, in index order;
  *   promote of the valid candidates other than the baseline, the first
  *           ceil(n_eligible num / den) in rank order (integer arithmetic),
- *           and the baseline itself when it is valid -- Fig. 4 promotes
- *           "6 candidates + baseline" and "2 candidates + baseline".  The
+ *           and the baseline itself when it is valid -- Fig. 4 carries the
+ *           baseline beside six, then two, promoted candidates.  The
  *           paper does not print its fraction; with 2/5 this rule yields
  *           Fig. 4's counts (15 successful candidates -> 6, then 4 -> 2).
  *   survival per rung (Table A.1): Fail% = failed / entering, Promotion% =

@@ -8,7 +8,9 @@ current stream.  The names mirror the C interface in include/kb.h:
     kb_screen_stats, kb_gen_inputs, kb_last_error, kb_version
 
 plus `screen(...)`, which chains the gate, the kernel and the readback for the
-common case.  Loading fails loudly (KbError) when libkb.so has not been built;
+common case.  The pass/fail verdict of each record comes from the library
+(kb_summarize / kb_screen_stats); this module only copies it into the record
+dicts.  Loading fails loudly (KbError) when libkb.so has not been built;
 there is no fallback implementation.
 """
 import ctypes
@@ -51,9 +53,12 @@ class KbStats(ctypes.Structure):
                 ("max_abs_err", ctypes.c_float), ("max_rel_err", ctypes.c_float),
                 ("bitwise_equal", ctypes.c_int32), ("status", ctypes.c_int32)]
 
-    def as_dict(self):
+    def as_dict(self, passed=None):
+        """The record's fields; `passed`, the library's verdict for it (from
+        kb_summarize or kb_screen_stats), is added when given."""
         d = {name: getattr(self, name) for name, _ in self._fields_}
-        d["passed"] = int(d["status"] == KB_STATUS_OK and d["mismatches"] == 0)
+        if passed is not None:
+            d["passed"] = int(passed)
         return d
 
 
@@ -64,6 +69,13 @@ class KbSummary(ctypes.Structure):
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class KbScreenOpts(ctypes.Structure):
+    _fields_ = [("host_table", ctypes.c_void_p), ("host_table_bytes", ctypes.c_size_t)]
+
+
+KB_INLINE_CANDS = 128
 
 
 class KbLaunch(ctypes.Structure):
@@ -111,9 +123,11 @@ assert ctypes.sizeof(KbLocate) == 32
 assert ctypes.sizeof(KbTensor) == 144
 
 EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
-           "kb_screen_launch", "kb_screen", "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
+           "kb_screen_launch", "kb_screen", "kb_screen_ex", "kb_screen_host_table_bytes",
+           "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
            "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_screen_multi",
-           "kb_screen_multi_workspace_bytes", "kb_summarize_multi", "kb_last_error", "kb_version")
+           "kb_screen_multi_workspace_bytes", "kb_screen_multi_host_table_bytes", "kb_summarize_multi",
+           "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -134,15 +148,21 @@ def lib():
         L.kb_screen_workspace_bytes.restype = ctypes.c_size_t
         L.kb_screen_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
         L.kb_screen_workspace_init.restype = i32
-        L.kb_summarize.argtypes = [ctypes.POINTER(KbStats), i32, ctypes.POINTER(KbSummary)]
+        L.kb_summarize.argtypes = [ctypes.POINTER(KbStats), i32, ctypes.POINTER(KbSummary),
+                                   ctypes.POINTER(ctypes.c_int32)]
         L.kb_summarize.restype = i32
         L.kb_screen_launch.argtypes = [i32, u64, i32, ctypes.POINTER(KbLaunch)]
         L.kb_screen_launch.restype = i32
         L.kb_screen.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
                                 u32, vp, ctypes.c_size_t, vp, vp]
         L.kb_screen.restype = i32
+        L.kb_screen_ex.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
+                                   u32, vp, ctypes.c_size_t, vp, ctypes.POINTER(KbScreenOpts), vp]
+        L.kb_screen_ex.restype = i32
+        L.kb_screen_host_table_bytes.argtypes = [i32]
+        L.kb_screen_host_table_bytes.restype = ctypes.c_size_t
         L.kb_screen_stats.argtypes = [vp, i32, ctypes.POINTER(KbStats), ctypes.POINTER(KbSummary),
-                                      vp]
+                                      ctypes.POINTER(ctypes.c_int32), vp]
         L.kb_screen_stats.restype = i32
         L.kb_screen_locate.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32,
                                        f32, u32, vp, vp, vp]
@@ -158,8 +178,10 @@ def lib():
         L.kb_screen_multi_workspace_bytes.restype = ctypes.c_size_t
         L.kb_screen_multi.argtypes = [ctypes.POINTER(KbTensor), i32, ctypes.POINTER(KbTensor), i32,
                                       ctypes.POINTER(f32), ctypes.POINTER(f32), u32, vp,
-                                      ctypes.c_size_t, vp, vp]
+                                      ctypes.c_size_t, vp, ctypes.POINTER(KbScreenOpts), vp]
         L.kb_screen_multi.restype = i32
+        L.kb_screen_multi_host_table_bytes.argtypes = [i32, i32]
+        L.kb_screen_multi_host_table_bytes.restype = ctypes.c_size_t
         L.kb_summarize_multi.argtypes = [ctypes.POINTER(KbStats), i32, i32, ctypes.POINTER(KbSummary),
                                          ctypes.POINTER(ctypes.c_int32)]
         L.kb_summarize_multi.restype = i32
@@ -259,7 +281,7 @@ def kb_screen_workspace_init(workspace, stream=None):
 
 
 def alloc_workspace(n_cands, numel, dtype, device, stream=None):
-    """A workspace for these sizes, initialised (zero-filled) by the library."""
+    """A workspace for these sizes, zero-filled by the library."""
     torch = _torch()
     nbytes = kb_screen_workspace_bytes(n_cands, numel, dtype)
     if nbytes == 0:
@@ -273,11 +295,68 @@ def alloc_stats(n_cands, device):
     return torch.empty(n_cands * ctypes.sizeof(KbStats), dtype=torch.uint8, device=device)
 
 
+class HostTables:
+    """The caller-owned pinned launch tables of calls with more than
+    KB_INLINE_CANDS candidates: a ring of `count` pinned host buffers of
+    `nbytes` each.  A buffer is handed out again only once the stream has
+    passed the call that last used it (an event recorded after each call),
+    because the kernels read their table from it."""
+
+    def __init__(self, nbytes, count=2):
+        torch = _torch()
+        self.nbytes = int(nbytes)
+        self.bufs = [torch.empty(max(1, self.nbytes), dtype=torch.uint8, pin_memory=True)
+                     for _ in range(count)]
+        self.events = [None] * count
+        self.opts = [KbScreenOpts(t.data_ptr(), self.nbytes) for t in self.bufs]
+        self.next = 0
+
+    def acquire(self):
+        """(index, opts) of the next buffer, after its previous call has passed."""
+        i = self.next
+        self.next = (i + 1) % len(self.bufs)
+        if self.events[i] is not None:
+            self.events[i].synchronize()
+            self.events[i] = None
+        return i, self.opts[i]
+
+    def release(self, i, stream=None):
+        """Record that the call just enqueued on `stream` reads buffer i."""
+        torch = _torch()
+        e = torch.cuda.Event()
+        e.record(torch.cuda.current_stream() if stream is None else stream)
+        self.events[i] = e
+
+
+# Host tables of function-style calls, kept alive until their calls have passed.
+_pending_tables = []
+
+
+def _one_off_opts(nbytes, stream):
+    """(opts, keep) for one call that needs a host table, or (None, None)."""
+    global _pending_tables
+    if nbytes == 0:
+        return None, None
+    _pending_tables = [(t, e) for t, e in _pending_tables if not e.query()]
+    tables = HostTables(nbytes, count=1)
+    i, opts = tables.acquire()
+    return opts, (tables, i)
+
+
+def _after_one_off(keep, stream):
+    if keep is not None:
+        tables, i = keep
+        tables.release(i, stream)
+        _pending_tables.append((tables, tables.events[i]))
+
+
 def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, stream=None):
     """Enqueue the screen of `cands` (torch tensors or None) against `ref`.
 
     Returns (d_stats, workspace) device buffers; read the records with
-    kb_screen_stats.
+    kb_screen_stats.  More than KB_INLINE_CANDS candidates go through
+    kb_screen_ex with a pinned host table, kept alive here until the call
+    has passed.
     """
     n = len(cands)
     r = describe(ref)
@@ -287,19 +366,24 @@ def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, str
                                     ref.device, stream)
     if d_stats is None:
         d_stats = alloc_stats(max(1, n), ref.device)
-    _check(lib().kb_screen(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
-                           ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
-                           ctypes.c_void_p(d_stats.data_ptr()), _stream_handle(stream)))
+    opts, keep = _one_off_opts(lib().kb_screen_host_table_bytes(n), stream)
+    _check(lib().kb_screen_ex(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
+                              ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                              ctypes.c_void_p(d_stats.data_ptr()),
+                              ctypes.byref(opts) if opts is not None else None, _stream_handle(stream)))
+    _after_one_off(keep, stream)
     return d_stats, workspace
 
 
 def kb_screen_stats(d_stats, n_cands, stream=None):
-    """Read back n_cands records (synchronizes the stream): (list of dicts, summary dict)."""
+    """Read back n_cands records (synchronizes the stream): (list of dicts
+    with the library's verdict as "passed", summary dict)."""
     host = (KbStats * max(1, n_cands))()
     summ = KbSummary()
+    passed = (ctypes.c_int32 * max(1, n_cands))()
     _check(lib().kb_screen_stats(ctypes.c_void_p(d_stats.data_ptr()), n_cands, host,
-                                 ctypes.byref(summ), _stream_handle(stream)))
-    return [host[k].as_dict() for k in range(n_cands)], summ.as_dict()
+                                 ctypes.byref(summ), passed, _stream_handle(stream)))
+    return [host[k].as_dict(passed[k]) for k in range(n_cands)], summ.as_dict()
 
 
 def kb_screen_locate(ref, cands, atol, rtol, d_stats, flags=0, stream=None):
@@ -454,9 +538,12 @@ def kb_screen_multi(refs, cands, atol, rtol, flags=0, workspace=None, d_stats=No
         d_stats = alloc_stats(max(1, n * n_out), refs[0].device)
     A = (ctypes.c_float * max(1, n_out))(*[float(x) for x in atol])
     T = (ctypes.c_float * max(1, n_out))(*[float(x) for x in rtol])
+    opts, keep = _one_off_opts(lib().kb_screen_multi_host_table_bytes(n_out, max(1, n)), stream)
     _check(lib().kb_screen_multi(R, n_out, C, n, A, T, int(flags),
                                  ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
-                                 ctypes.c_void_p(d_stats.data_ptr()), _stream_handle(stream)))
+                                 ctypes.c_void_p(d_stats.data_ptr()),
+                                 ctypes.byref(opts) if opts is not None else None, _stream_handle(stream)))
+    _after_one_off(keep, stream)
     return d_stats, workspace
 
 
@@ -489,10 +576,16 @@ class MultiScreener:
         self._st = ctypes.c_void_p(self.d_stats.data_ptr())
         self._stream = _stream_handle(stream)
         self.stream = stream
+        tb = self._L.kb_screen_multi_host_table_bytes(self.n_out, max(1, self.n))
+        self._tables = HostTables(tb, count=4) if tb > 0 else None
 
     def launch(self):
+        i, opts = self._tables.acquire() if self._tables else (None, None)
         _check(self._L.kb_screen_multi(self._R, self.n_out, self._C, self.n, self._A, self._T, self.flags,
-                                       self._ws, self.workspace.numel(), self._st, self._stream))
+                                       self._ws, self.workspace.numel(), self._st,
+                                       ctypes.byref(opts) if opts is not None else None, self._stream))
+        if self._tables:
+            self._tables.release(i, self.stream)
 
     def records(self):
         """All n_out * n_cands records, output-major (synchronizes the stream)."""
@@ -537,7 +630,7 @@ def kb_summarize(records):
     else:
         arr, n = records, len(records)
     summ = KbSummary()
-    _check(lib().kb_summarize(arr, n, ctypes.byref(summ)))
+    _check(lib().kb_summarize(arr, n, ctypes.byref(summ), None))
     return summ.as_dict()
 
 
@@ -580,32 +673,49 @@ class Screener:
             self._views = None
         self._slot_ptr = [ctypes.c_void_p(t.data_ptr()) for t in self.slots]
         self._host = (KbStats * max(1, self.n))()
+        self._passed = (ctypes.c_int32 * max(1, self.n))()
         self._summary = KbSummary()
         self._L = lib()
+        # more than KB_INLINE_CANDS candidates: a ring of pinned launch
+        # tables, one per record slot (at least two)
+        tb = self._L.kb_screen_host_table_bytes(max(1, self.n))
+        self._tables = HostTables(tb, count=max(2, len(self.slots))) if tb > 0 else None
 
     @property
     def d_stats(self):
         return self.slots[0]
 
     def launch(self, slot=0):
-        _check(self._L.kb_screen(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
-                                 self.flags, self._ws, self.workspace.numel(),
-                                 self._slot_ptr[slot], self._stream))
+        i, opts = self._tables.acquire() if self._tables else (None, None)
+        _check(self._L.kb_screen_ex(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
+                                    self.flags, self._ws, self.workspace.numel(),
+                                    self._slot_ptr[slot], ctypes.byref(opts) if opts is not None else None,
+                                    self._stream))
+        if self._tables:
+            self._tables.release(i, self.stream)
 
     def read(self, slot=0):
-        """Copy the records back (synchronizes the stream); returns the summary."""
+        """Copy the records back (synchronizes the stream); returns the
+        summary (the verdicts are kept for records())."""
         _check(self._L.kb_screen_stats(self._slot_ptr[slot], self.n, self._host,
-                                       ctypes.byref(self._summary), self._stream))
+                                       ctypes.byref(self._summary), self._passed, self._stream))
         return self._summary
 
     def summarize(self, slot):
         """Summary of a pinned host slot; the caller has synchronized past the launch."""
-        _check(self._L.kb_summarize(self._views[slot], self.n, ctypes.byref(self._summary)))
+        _check(self._L.kb_summarize(self._views[slot], self.n, ctypes.byref(self._summary),
+                                    self._passed))
         return self._summary
 
     def records(self, slot=None):
-        src = self._host if slot is None else self._views[slot]
-        return [src[k].as_dict() for k in range(self.n)]
+        """Record dicts of the last read() (slot None) or of a pinned slot,
+        each with the library's verdict as "passed"."""
+        if slot is None:
+            src = self._host
+        else:
+            src = self._views[slot]
+            _check(self._L.kb_summarize(src, self.n, None, self._passed))
+        return [src[k].as_dict(self._passed[k]) for k in range(self.n)]
 
     def launch_plan(self):
         return kb_screen_launch(max(1, self.n), self.ref.numel(), self._ref.dtype)

@@ -1,15 +1,13 @@
 // kb_api.hip -- host side of the C interface (include/kb.h): argument
-// validation, the policy gate, launch planning, the launch-table upload and
-// the statistics readback.
+// validation, the policy gate, launch planning and the statistics readback.
 #include <hip/hip_runtime.h>
 
+#include <chrono>
 #include <cmath>
 #include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <mutex>
-#include <string>
 #include <vector>
 
 #include "kb_device.hpp"
@@ -19,17 +17,19 @@
 namespace kb {
 namespace {
 
-thread_local std::string g_error;
+// The last error of the calling thread, a fixed buffer (setting it allocates
+// nothing).
+thread_local char g_error[512];
 
-void clear_error() { g_error.clear(); }
+void clear_error() { g_error[0] = '\0'; }
 
 int fail(int code, const char* fmt, ...) {
-    char buf[512];
+    char buf[sizeof g_error];
     va_list ap;
     va_start(ap, fmt);
     std::vsnprintf(buf, sizeof buf, fmt, ap);
     va_end(ap);
-    g_error = buf;
+    std::memcpy(g_error, buf, sizeof g_error);
     return code;
 }
 
@@ -81,85 +81,57 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Launch tuning override for measurement sweeps: KB_SCREEN_TUNE="kg=16,blocks=1024"
 // caps the candidates per group (1, 2, 4, 8 or 16) and sets the target total
-// number of work-groups.  Unset, the built-in choice applies.
-void tuning_override(int* kg_cap, int* blocks_total, int* ff_round = nullptr) {
-    const char* s = std::getenv("KB_SCREEN_TUNE");
-    if (s == nullptr) return;
-    int v;
-    const char* k = std::strstr(s, "kg=");
-    if (k && std::sscanf(k + 3, "%d", &v) == 1 && (v == 1 || v == 2 || v == 4 || v == 8 || v == 16))
-        *kg_cap = v;
-    const char* b = std::strstr(s, "blocks=");  // 0 or absent: occupancy-based
-    if (b && std::sscanf(b + 7, "%d", &v) == 1 && v >= 8 && v <= (1 << 20)) *blocks_total = v;
-    const char* f = std::strstr(s, "ffround=");  // fail-fast groups per round
-    if (ff_round && f && std::sscanf(f + 8, "%d", &v) == 1 && v >= 1) *ff_round = v;
-}
-
-// ---------------------------------------------------------------------------
-// Pinned host staging ring for launch-table uploads.  A slot is reused only
-// after the copy that last read it has completed (its event), so callers may
-// return immediately and the copies stay asynchronous.
-// ---------------------------------------------------------------------------
-class Staging {
-public:
-    // Fill a pinned slot of `bytes` bytes with fill(host) and enqueue its copy
-    // to device dst on `stream`.
-    template <class Fill>
-    int upload(size_t bytes, Fill fill, void* dst, hipStream_t stream) {
-        std::lock_guard<std::mutex> lock(mu_);
-        Slot& sl = slots_[next_];
-        next_ = (next_ + 1) % kSlots;
-        int dev = 0;
-        hipError_t e = hipGetDevice(&dev);
-        if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
-        if (sl.ev != nullptr) {
-            e = hipEventSynchronize(sl.ev);
-            if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize(staging)");
-            if (sl.dev != dev) {
-                (void)hipEventDestroy(sl.ev);
-                sl.ev = nullptr;
-            }
-        }
-        if (sl.ev == nullptr) {
-            e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
-            if (e != hipSuccess) return fail_hip(e, "hipEventCreateWithFlags");
-            sl.dev = dev;
-        }
-        if (sl.cap < bytes) {
-            if (sl.host) (void)hipHostFree(sl.host);
-            sl.host = nullptr;
-            sl.cap = 0;
-            const size_t cap = align_up(bytes < 65536 ? 65536 : bytes, 4096);
-            e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
-            if (e != hipSuccess) return fail_hip(e, "hipHostMalloc(staging)");
-            sl.cap = cap;
-        }
-        fill(sl.host);
-        e = hipMemcpyAsync(dst, sl.host, bytes, hipMemcpyHostToDevice, stream);
-        if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync(launch table)");
-        e = hipEventRecord(sl.ev, stream);
-        if (e != hipSuccess) return fail_hip(e, "hipEventRecord(staging)");
-        return KB_OK;
-    }
-
-private:
-    static constexpr int kSlots = 8;
-    struct Slot {
-        void* host = nullptr;
-        size_t cap = 0;
-        hipEvent_t ev = nullptr;
-        int dev = -1;
-    };
-    std::mutex mu_;
-    Slot slots_[kSlots];
-    int next_ = 0;
+// number of work-groups; "ffround=N" sets the fail-fast groups per round.
+// Read once per process; unset (the normal case), the built-in choice
+// applies.
+struct Tuning {
+    int kg_cap = 0, blocks_total = 0, ff_round = 0;  // 0 = not overridden
 };
 
-// Intentionally leaked: pinned memory and events must not be released from a
-// static destructor after the HIP runtime has shut down.
-Staging& staging() {
-    static Staging* s = new Staging();
-    return *s;
+const Tuning& tuning() {
+    static const Tuning t = [] {
+        Tuning r;
+        const char* s = std::getenv("KB_SCREEN_TUNE");
+        if (s == nullptr) return r;
+        int v;
+        const char* k = std::strstr(s, "kg=");
+        if (k && std::sscanf(k + 3, "%d", &v) == 1 && (v == 1 || v == 2 || v == 4 || v == 8 || v == 16))
+            r.kg_cap = v;
+        const char* b = std::strstr(s, "blocks=");
+        if (b && std::sscanf(b + 7, "%d", &v) == 1 && v >= 8 && v <= (1 << 20)) r.blocks_total = v;
+        const char* f = std::strstr(s, "ffround=");
+        if (f && std::sscanf(f + 8, "%d", &v) == 1 && v >= 1) r.ff_round = v;
+        return r;
+    }();
+    return t;
+}
+
+// A tag for one screening call: odd (the self-checking tickets need it), and
+// in practice different from any value a workspace word holds unless this
+// call wrote it (the kernel marks its tickets and fail-fast words with it; see
+// the kernel).  Derived from the monotonic clock, so the library keeps no
+// state for it.
+uint32_t call_tag() {
+    uint64_t x = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+    // MurmurHash3's 64-bit finalizer: every input bit reaches every output bit
+    x ^= x >> 33;
+    x *= 0xFF51AFD7ED558CCDull;
+    x ^= x >> 33;
+    x *= 0xC4CEB9FE1A85EC53ull;
+    x ^= x >> 33;
+    return ((uint32_t)x ^ (uint32_t)(x >> 32)) | 1u;
+}
+
+// A record that a kernel wrote with status KB_ERR_WORKSPACE: the call found
+// a ticket word of its workspace that did not begin at zero.
+int dirty_workspace_error(const kb_stats* st, int n) {
+    for (int k = 0; k < n; ++k)
+        if (st[k].status == KB_ERR_WORKSPACE)
+            return fail(KB_ERR_WORKSPACE,
+                        "candidate %d: the screening call found its workspace not clean (zero-fill it "
+                        "with kb_screen_workspace_init after allocating it and before using it for other "
+                        "sizes); the records of that call are not valid", k);
+    return KB_OK;
 }
 
 }  // namespace
@@ -182,8 +154,8 @@ int plan_group_size(int n_cands, int dtype) {
     // Measured on the five screening workloads: groups of 4 for fp32 and
     // for short candidate lists, 8 for long lists of 16-bit tensors (the
     // reference is then re-read by fewer groups).
-    int kg_cap = (dtype != DT_F32 && n_cands >= 32) ? 8 : 4, blocks_total = 0;
-    tuning_override(&kg_cap, &blocks_total);
+    int kg_cap = (dtype != DT_F32 && n_cands >= 32) ? 8 : 4;
+    if (tuning().kg_cap > 0) kg_cap = tuning().kg_cap;
     int kg = 1;
     while (kg < n_cands && kg < kg_cap) kg *= 2;
     return kg;
@@ -234,8 +206,8 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     const uint64_t c_plain = clamp_c(align_up((4096 + groups_max - 1) / groups_max, 8));
     const uint64_t c_ws = clamp_c(c_plain > 2048 ? c_plain : 2048);
     if (c_ws > (1u << 20)) return false;
-    int kg_cap = 8, blocks_total = 0, ff_round = kFailFastRound;
-    tuning_override(&kg_cap, &blocks_total, &ff_round);
+    int blocks_total = tuning().blocks_total;
+    const int ff_round = tuning().ff_round > 0 ? tuning().ff_round : kFailFastRound;
     if (blocks_total <= 0) blocks_total = resident_blocks > 0 ? resident_blocks : 2048;
     const int groups = P.n_groups > 0 ? P.n_groups : 1;
     P.ff_round = ff_round < groups ? ff_round : groups;
@@ -251,20 +223,19 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     if (C < 8) C = 8;
     P.blocks_per_group = (int)C;
     const uint64_t Cw = c_ws;  // layout stride bound
-    // Workspace layout, sized for the group count of n_cands.  The tickets
-    // (zero between calls) come first.
+    // Workspace layout, sized for the group count of n_cands.  The tagged
+    // tickets (8 bytes each) come first, then the fail-fast words (one
+    // 128-byte line each).
     P.n_super = (int)((C + 15) / 16);
     const int super_ws = (int)((Cw + 15) / 16);
     size_t off = 0;
     P.off_tickets2 = off;
-    off += (size_t)groups_max * 4;
+    off += (size_t)groups_max * 8;
     P.off_tickets1 = off;
-    off += (size_t)groups_max * super_ws * 4;
+    off += (size_t)groups_max * super_ws * 8;
     off = align_up(off, 256);
-    P.off_ff_flags = off;  // fail-fast words (128-byte lines), zero between calls like the tickets
+    P.off_ff_flags = off;
     off = align_up(off + (size_t)groups_max * P.kg * (size_t)(1 + super_ws) * 128, 256);
-    P.off_table = off;
-    off = align_up(off + (size_t)(n_cands + P.kg) * sizeof(CandEntry), 256);
     P.off_part_u32 = off;
     off = align_up(off + (size_t)kPartPlanes * n_cands * Cw * 4, 256);
     P.off_part_ssd = off;
@@ -286,17 +257,26 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
 
 namespace kb {
 
+// Host memory a call must be given for its launch table: none when the table
+// (one entry per candidate) travels in the kernel arguments.
+size_t host_table_bytes(int n_cands) {
+    return n_cands <= kInlineCands ? 0 : align_up((size_t)n_cands * sizeof(CandEntry), 256);
+}
+
 // The screen of n_cands candidates whose gate statuses are already known
 // (status[k] == KB_STATUS_OK: read and compared; otherwise a record of
-// that status, not read).  Shared by kb_screen and kb_screen_multi; `who`
-// names the caller in error messages.  The caller has validated ref,
-// cands, n_cands, atol, rtol and flags.
+// that status, not read).  Shared by kb_screen, kb_screen_ex, kb_screen_multi
+// and kb_screen_noalloc; `who` names the caller in error messages.  The
+// caller has validated ref, cands, n_cands, atol, rtol and flags.
+// host_table: caller-owned pinned host memory of at least
+// host_table_bytes(n_cands) bytes when the table does not fit the kernel
+// arguments (the kernels then read it there), else ignored.
 int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* cands, int n_cands,
                        const int32_t* status, float atol, float rtol, uint32_t flags, void* workspace,
-                       size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream) {
-    int rc = KB_OK;
+                       size_t workspace_bytes, void* host_table, size_t host_table_size,
+                       kb_stats* d_stats, hipStream_t stream) {
     const bool fail_fast = (flags & KB_FAIL_FAST) != 0;
-    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "reference is not contiguous");
+    if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "%s: reference is not contiguous", who);
     const uint64_t numel = tensor_numel(*ref);
     const int dtype = ref->dtype;
     int n_acc = 0;
@@ -317,39 +297,35 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
         if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
             return fail(KB_ERR_ALIGNMENT, "%s: candidate %d data not 16-byte aligned", who, k);
 
-    // Launch table: accepted candidates in call order padded to whole groups
-    // (padding points at the reference and writes no record), then rejected
-    // ones.  Up to kInlineCands entries travel in the kernel arguments; a
-    // larger table is uploaded to the workspace through the pinned staging
-    // ring.
-    const int n_groups = P.n_groups;
-    const int rej_start = n_groups * P.kg;
-    const int n_table = rej_start + (n_cands - n_acc);
+    // Launch table: the accepted candidates in call order, then the rejected
+    // ones (one entry per candidate).  Up to kInlineCands entries travel in
+    // the kernel arguments; a longer table is written to the caller's pinned
+    // host memory, which the kernels read directly.
+    const int n_table = n_cands;
     const bool table_inline = n_table <= kInlineCands;
+    const size_t need = host_table_bytes(n_cands);
+    if (!table_inline && (host_table == nullptr || host_table_size < need))
+        return fail(KB_ERR_WORKSPACE,
+                    "%s: %d candidates need a pinned host table of %zu bytes (kb_screen_ex), %zu given",
+                    who, n_cands, need, host_table == nullptr ? (size_t)0 : host_table_size);
+    if (!table_inline && !aligned16(host_table))
+        return fail(KB_ERR_ALIGNMENT, "%s: host table not 16-byte aligned", who);
     InlineTable tab;
-    auto fill = [&](CandEntry* t) {
+    CandEntry* t = table_inline ? tab.e : (CandEntry*)host_table;
+    {
         int w = 0;
         for (int k = 0; k < n_cands; ++k)
             if (status[k] == KB_STATUS_OK) t[w++] = CandEntry{cands[k].data, k, KB_STATUS_OK};
-        while (w < rej_start) t[w++] = CandEntry{ref->data, -1, KB_STATUS_OK};
         for (int k = 0; k < n_cands; ++k)
             if (status[k] != KB_STATUS_OK) t[w++] = CandEntry{nullptr, k, status[k]};
-    };
+    }
+    const CandEntry* d_table = table_inline ? nullptr : (const CandEntry*)host_table;
     char* ws = (char*)workspace;
     P.wide = wide ? 1 : 0;
-    const CandEntry* d_table = (const CandEntry*)(ws + P.off_table);
-    if (table_inline) {
-        fill(tab.e);
-    } else {
-        rc = staging().upload(
-            (size_t)n_table * sizeof(CandEntry), [&](void* host) { fill((CandEntry*)host); },
-            ws + P.off_table, stream);
-        if (rc != KB_OK) return rc;
-    }
     hipError_t e;
     if (n_acc == 0 || numel == 0) {
         e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, stream);
-        if (e != hipSuccess) return fail_hip(e, (std::string(who) + ": records launch").c_str());
+        if (e != hipSuccess) return fail(KB_ERR_HIP, "%s: records launch: %s", who, hipGetErrorString(e));
         return KB_OK;
     }
     ScreenParams p{};
@@ -363,14 +339,15 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     p.n_acc = n_acc;
     p.n_cands = n_cands;
     p.n_table = n_table;
-    p.rej_start = rej_start;
+    p.rej_start = n_acc;
     p.table_inline = table_inline ? 1 : 0;
     p.n_groups = P.n_groups;
     p.blocks_per_group = P.blocks_per_group;
     p.n_super = P.n_super;
     p.ff_round = P.ff_round;
-    p.tickets1 = (uint32_t*)(ws + P.off_tickets1);
-    p.tickets2 = (uint32_t*)(ws + P.off_tickets2);
+    p.tag = call_tag();
+    p.tickets1 = (uint64_t*)(ws + P.off_tickets1);
+    p.tickets2 = (uint64_t*)(ws + P.off_tickets2);
     p.ff_flags = (uint32_t*)(ws + P.off_ff_flags);
     p.part_u32 = (uint32_t*)(ws + P.off_part_u32);
     p.part_ssd = (double*)(ws + P.off_part_ssd);
@@ -380,7 +357,7 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     p.part2_ssr = (double*)(ws + P.off_part2_ssr);
     p.stats = d_stats;
     e = launch_screen(P, p, tab, fail_fast, stream);
-    if (e != hipSuccess) return fail_hip(e, (std::string(who) + ": kernel launch").c_str());
+    if (e != hipSuccess) return fail(KB_ERR_HIP, "%s: kernel launch: %s", who, hipGetErrorString(e));
     return KB_OK;
 }
 
@@ -390,9 +367,9 @@ using namespace kb;
 
 extern "C" {
 
-const char* kb_last_error(void) { return g_error.c_str(); }
+const char* kb_last_error(void) { return g_error; }
 
-int kb_version(void) { return 100; }
+int kb_version(void) { return 20000; }
 
 int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands, int32_t* status) {
     clear_error();
@@ -431,22 +408,40 @@ int kb_screen_launch(int n_cands, uint64_t numel, int dtype, kb_launch* out) {
     return KB_OK;
 }
 
+// Checks shared by the screening entry points (no device work).
+static int check_screen_args(const char* who, const kb_tensor* ref, const kb_tensor* cands, int n_cands,
+                             float atol, float rtol, uint32_t flags, const kb_stats* d_stats) {
+    if (ref == nullptr || cands == nullptr || d_stats == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "%s: null ref, cands or d_stats", who);
+    if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "%s: n_cands = %d < 1", who, n_cands);
+    if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
+        return fail(KB_ERR_INVALID_ARG, "%s: atol and rtol must be finite and >= 0", who);
+    if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
+        return fail(KB_ERR_INVALID_ARG, "%s: unknown flags 0x%x", who, flags);
+    return KB_OK;
+}
+
+size_t kb_screen_host_table_bytes(int n_cands) { return n_cands < 1 ? 0 : host_table_bytes(n_cands); }
+
+int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
+                 uint32_t flags, void* workspace, size_t workspace_bytes, kb_stats* d_stats,
+                 const kb_screen_opts* opts, hipStream_t stream) {
+    clear_error();
+    int rc = check_screen_args("kb_screen", ref, cands, n_cands, atol, rtol, flags, d_stats);
+    if (rc != KB_OK) return rc;
+    std::vector<int32_t> status((size_t)n_cands);
+    rc = kb_policy_check(ref, cands, n_cands, status.data());
+    if (rc != KB_OK) return rc;
+    return screen_with_status("kb_screen", ref, cands, n_cands, status.data(), atol, rtol, flags,
+                              workspace, workspace_bytes, opts ? opts->host_table : nullptr,
+                              opts ? opts->host_table_bytes : 0, d_stats, stream);
+}
+
 int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
               uint32_t flags, void* workspace, size_t workspace_bytes, kb_stats* d_stats,
               hipStream_t stream) {
-    clear_error();
-    if (ref == nullptr || cands == nullptr || d_stats == nullptr)
-        return fail(KB_ERR_INVALID_ARG, "kb_screen: null ref, cands or d_stats");
-    if (n_cands < 1) return fail(KB_ERR_INVALID_ARG, "kb_screen: n_cands = %d < 1", n_cands);
-    if (!std::isfinite(atol) || !std::isfinite(rtol) || atol < 0.f || rtol < 0.f)
-        return fail(KB_ERR_INVALID_ARG, "kb_screen: atol and rtol must be finite and >= 0");
-    if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
-        return fail(KB_ERR_INVALID_ARG, "kb_screen: unknown flags 0x%x", flags);
-    std::vector<int32_t> status((size_t)n_cands);
-    int rc = kb_policy_check(ref, cands, n_cands, status.data());
-    if (rc != KB_OK) return rc;
-    return screen_with_status("kb_screen", ref, cands, n_cands, status.data(), atol, rtol, flags,
-                              workspace, workspace_bytes, d_stats, stream);
+    return kb_screen_ex(ref, cands, n_cands, atol, rtol, flags, workspace, workspace_bytes, d_stats,
+                        nullptr, stream);
 }
 
 // Multi-output candidates: the workspace of output o starts at the sum of
@@ -471,9 +466,15 @@ size_t kb_screen_multi_workspace_bytes(const kb_tensor* refs, int n_outputs, int
     return multi_layout(refs, n_outputs, n_cands, nullptr, &total) ? total : 0;
 }
 
+size_t kb_screen_multi_host_table_bytes(int n_outputs, int n_cands) {
+    if (n_outputs < 1 || n_outputs > KB_MAX_OUTPUTS || n_cands < 1) return 0;
+    return (size_t)n_outputs * host_table_bytes(n_cands);
+}
+
 int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands, int n_cands,
                     const float* atol, const float* rtol, uint32_t flags, void* workspace,
-                    size_t workspace_bytes, kb_stats* d_stats, hipStream_t stream) {
+                    size_t workspace_bytes, kb_stats* d_stats, const kb_screen_opts* opts,
+                    hipStream_t stream) {
     clear_error();
     if (refs == nullptr || cands == nullptr || atol == nullptr || rtol == nullptr || d_stats == nullptr)
         return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: null refs, cands, atol, rtol or d_stats");
@@ -494,7 +495,11 @@ int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands
     for (int o = 0; o < n_outputs; ++o) {
         for (int k = 0; k < n_cands; ++k) col[k] = cands[(size_t)k * n_outputs + o];
         const int rc = kb_policy_check(&refs[o], col.data(), n_cands, st.data());
-        if (rc != KB_OK) return fail(rc, "kb_screen_multi: reference %d: %s", o, g_error.c_str());
+        if (rc != KB_OK) {
+            char why[sizeof g_error];
+            std::memcpy(why, g_error, sizeof why);
+            return fail(rc, "kb_screen_multi: reference %d: %s", o, why);
+        }
         if (!is_contiguous(refs[o]))
             return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: reference %d is not contiguous", o);
         for (int k = 0; k < n_cands; ++k)
@@ -518,12 +523,20 @@ int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands
                 return fail(KB_ERR_ALIGNMENT, "kb_screen_multi: candidate %d output %d not 16-byte aligned",
                             k, o);
     }
+    // Each output's launch table gets its own region of the host table (the
+    // outputs' kernels are in flight together).
+    const size_t tab_bytes = host_table_bytes(n_cands);
+    char* htab = opts ? (char*)opts->host_table : nullptr;
+    if (tab_bytes > 0 && (htab == nullptr || opts->host_table_bytes < (size_t)n_outputs * tab_bytes))
+        return fail(KB_ERR_WORKSPACE, "kb_screen_multi: %d candidates need a pinned host table of %zu bytes",
+                    n_cands, (size_t)n_outputs * tab_bytes);
     char* ws = (char*)workspace;
     for (int o = 0; o < n_outputs; ++o) {
         for (int k = 0; k < n_cands; ++k) col[k] = cands[(size_t)k * n_outputs + o];
         const size_t bytes = (o + 1 < n_outputs ? offs[o + 1] : total) - offs[o];
         const int rc = screen_with_status("kb_screen_multi", &refs[o], col.data(), n_cands, combined.data(),
                                           atol[o], rtol[o], flags, ws + offs[o], bytes,
+                                          htab ? htab + (size_t)o * tab_bytes : nullptr, tab_bytes,
                                           d_stats + (size_t)o * n_cands, stream);
         if (rc != KB_OK) return rc;
     }
@@ -535,6 +548,8 @@ int kb_summarize_multi(const kb_stats* h_stats, int n_outputs, int n_cands, kb_s
     clear_error();
     if (h_stats == nullptr || summary == nullptr || n_outputs < 1 || n_cands < 0)
         return fail(KB_ERR_INVALID_ARG, "kb_summarize_multi: null argument or bad count");
+    const int dirty = dirty_workspace_error(h_stats, n_outputs * n_cands);
+    if (dirty != KB_OK) return dirty;
     kb_summary s{n_cands, 0, 0, 0, -1, -1};
     for (int k = 0; k < n_cands; ++k) {
         bool rejected = false, failed = false;
@@ -631,48 +646,51 @@ int kb_screen_workspace_init(void* workspace, size_t workspace_bytes, hipStream_
     return KB_OK;
 }
 
-int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary) {
+int kb_summarize(const kb_stats* h_stats, int n_cands, kb_summary* summary, int32_t* passed) {
     clear_error();
-    if (h_stats == nullptr || summary == nullptr || n_cands < 0)
-        return fail(KB_ERR_INVALID_ARG, "kb_summarize: null argument or negative count");
+    if (h_stats == nullptr || n_cands < 0)
+        return fail(KB_ERR_INVALID_ARG, "kb_summarize: null records or negative count");
+    const int dirty = dirty_workspace_error(h_stats, n_cands);
+    if (dirty != KB_OK) return dirty;
     kb_summary s{n_cands, 0, 0, 0, -1, -1};
     for (int k = 0; k < n_cands; ++k) {
         const kb_stats& st = h_stats[k];
-        if (st.status != KB_STATUS_OK) {
-            s.n_rejected++;
-        } else if (st.mismatches == 0) {
+        // K(p) for one output: accepted by the gate and no mismatching element
+        const bool ok = st.status == KB_STATUS_OK && st.mismatches == 0;
+        if (passed) passed[k] = ok ? 1 : 0;
+        if (ok) {
             s.n_passed++;
             if (s.first_passed < 0) s.first_passed = k;
             continue;
-        } else {
-            s.n_failed++;
         }
+        if (st.status != KB_STATUS_OK) s.n_rejected++;
+        else s.n_failed++;
         if (s.first_failed < 0) s.first_failed = k;
     }
-    *summary = s;
+    if (summary) *summary = s;
     return KB_OK;
 }
 
 int kb_screen_stats(const kb_stats* d_stats, int n_cands, kb_stats* h_stats, kb_summary* summary,
-                    hipStream_t stream) {
+                    int32_t* passed, hipStream_t stream) {
     clear_error();
     if (d_stats == nullptr || n_cands < 0)
         return fail(KB_ERR_INVALID_ARG, "kb_screen_stats: null d_stats or negative count");
     std::vector<kb_stats> tmp;
     kb_stats* dst = h_stats;
-    if (dst == nullptr) {
+    if (dst == nullptr && (summary != nullptr || passed != nullptr)) {
         tmp.resize((size_t)n_cands);
         dst = tmp.data();
     }
-    if (n_cands > 0) {
+    if (n_cands > 0 && dst != nullptr) {
         hipError_t e = hipMemcpyAsync(dst, d_stats, (size_t)n_cands * sizeof(kb_stats),
                                       hipMemcpyDeviceToHost, stream);
         if (e != hipSuccess) return fail_hip(e, "kb_screen_stats: hipMemcpyAsync");
     }
     hipError_t e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen_stats: hipStreamSynchronize");
-    if (summary) return kb_summarize(dst, n_cands, summary);
-    return KB_OK;
+    if (dst != nullptr) return kb_summarize(dst, n_cands, summary, passed);
+    return KB_OK;  // (without a host copy there is nothing to check)
 }
 
 int kb_screen_locate(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,

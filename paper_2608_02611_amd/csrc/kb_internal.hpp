@@ -11,9 +11,9 @@
 namespace kb {
 
 // One entry of the launch table.  The table holds the accepted candidates
-// in call order, padded to whole candidate groups with entries that point
-// at the reference (index -1; the kernel compares them but writes no
-// record), then the rejected candidates.
+// in call order, then the rejected candidates: one entry per candidate.  (The
+// last candidate group is padded inside the kernel with the reference, which
+// it compares but writes no record for.)
 struct CandEntry {
     const void* data;  // device pointer (NULL for rejected entries)
     int32_t index;     // position in the caller's candidate array, -1 for padding
@@ -94,7 +94,7 @@ int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide = false);
 constexpr int kFailFastRound = 2;
 
 // Launch tables of up to this many candidates travel in the kernel
-// arguments (no upload); larger ones are uploaded to the workspace.
+// arguments; larger ones are read from the caller's pinned host memory.
 constexpr int kInlineCands = 128;
 
 struct InlineTable {
@@ -112,15 +112,16 @@ struct ScreenParams {
     uint32_t flags;
     int n_acc;
     int n_cands;
-    int n_table;         // table entries: n_groups * KG padded accepted + rejected
-    int rej_start;       // first rejected entry (n_groups * KG)
-    int table_inline;    // 1: the table is the kernel argument, 0: p.table
+    int n_table;         // table entries: the accepted, then the rejected candidates
+    int rej_start;       // first rejected entry (n_acc)
+    int table_inline;    // 1: the table is the kernel argument, 0: p.table (host memory)
     int n_groups;
     int blocks_per_group;
     int n_super;
     int ff_round;        // fail-fast: candidate groups per round of the grid
-    uint32_t* tickets1;  // [n_groups][n_super]
-    uint32_t* tickets2;  // [n_groups]
+    uint32_t tag;        // this call's tag (nonzero): marks its tickets and fail-fast words
+    uint64_t* tickets1;  // [n_groups][n_super] tagged tickets: (tag << 32) | arrivals
+    uint64_t* tickets2;  // [n_groups]
     uint32_t* ff_flags;  // fail-fast words: [n_groups * KG][1 + n_super] lines of 32 words
     uint32_t* part_u32;  // [kPartPlanes][n_acc][blocks_per_group]
     double* part_ssd;    // [n_acc][blocks_per_group]

@@ -152,16 +152,34 @@ __device__ __forceinline__ uint32_t count_within(float s, float tol) {
 // L2, which is what a device-scope fence costs here and which would also
 // evict the lines other work-groups on the XCD are streaming.
 __device__ __forceinline__ void complete_stores() { __builtin_amdgcn_s_waitcnt(0); }
-__device__ __forceinline__ uint32_t ticket(uint32_t* t) {
-    return __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 template <class T>
 __device__ __forceinline__ T ld_coherent(const T* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ double ld_coherent(const double* p) {
-    return __builtin_bit_cast(double, ld_coherent((const uint64_t*)p));
+
+// Self-checking tickets.  Every arrival adds D = (tag << 32) | 1 to its
+// 64-bit ticket word, the call's tag being odd.  A word that was zero when
+// the call began (as every completed call leaves its words) holds j D after
+// j arrivals, so its high half is always its low half times the tag (mod
+// 2^32).  A word that began with anything else -- a value left by a call cut
+// short, the partials of a call with other sizes laid out over it, or
+// whatever the memory held -- fails that test: with the tag odd, an old
+// value (h, l) passes only if h = l tag mod 2^32, which a nonzero leftover
+// meets by chance with probability 2^-32.  So a leftover ticket cannot make
+// a work-group that is not the last finish the group; a work-group that
+// finds a failed test reports the workspace instead (the caller's readback
+// then returns an error).  Arrivals stay single atomic adds, which the
+// memory-side atomic unit serves back to back: claiming the word with a
+// compare-exchange, per arrival or per work-group start, was measured to
+// cost 7-15 us on the 16 x 4096^2 bf16 screen.  Returns the arrival number
+// (1-based), or 0 when the word did not begin at zero.
+__device__ __forceinline__ uint32_t ticket_arrive(uint64_t* t, uint32_t tag) {
+    const uint64_t old =
+        __hip_atomic_fetch_add(t, ((uint64_t)tag << 32) | 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t n = (uint32_t)old;
+    return (uint32_t)(old >> 32) == n * tag ? n + 1u : 0u;
 }
+
 template <class T>
 __device__ __forceinline__ void st_coherent(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -317,6 +335,32 @@ __device__ __forceinline__ void write_record(kb_stats* dst, uint64_t numel, uint
     *dst = st;
 }
 
+// The launch table: the kernel argument, or the caller's pinned host copy.
+__device__ __forceinline__ const CandEntry* table_of(const ScreenParams& p, const InlineTable& tab) {
+    return p.table_inline ? tab.e : p.table;
+}
+
+// A work-group found a ticket word that did not begin at zero: the group
+// cannot be finished reliably, so its candidates' records say so (status
+// KB_ERR_WORKSPACE, every other field zero; the readback reports the error),
+// and group 0 also writes the rejected candidates' records.  Every
+// work-group of the group that finds it writes the same bytes.
+__device__ __forceinline__ void report_dirty(const ScreenParams& p, const CandEntry* table, int g, int j0,
+                                             int kg) {
+    for (int j = threadIdx.x; j < kg; j += kThreads) {
+        kb_stats st = {};
+        st.status = KB_ERR_WORKSPACE;
+        p.stats[table[j0 + j].index] = st;
+    }
+    if (g == 0) {
+        for (int k = p.rej_start + (int)threadIdx.x; k < p.n_table; k += kThreads) {
+            kb_stats st = {};
+            st.status = table[k].status;
+            p.stats[table[k].index] = st;
+        }
+    }
+}
+
 // Records of the rejected candidates (written by group 0's finisher).
 __device__ __forceinline__ void write_rejected(const ScreenParams& p, const CandEntry* table) {
     for (int k = p.rej_start + (int)threadIdx.x; k < p.n_table; k += kThreads) {
@@ -345,7 +389,9 @@ constexpr int min_waves(int dt, int kg) { return kg <= 4 || (kg == 8 && dt != DT
 // sees at most 16 or n_super writers.  (Stores to one word from every
 // work-group that fails at the same moment -- all of them, for a candidate
 // that is wrong everywhere -- serialize at the memory and were measured to
-// cost more than the whole pass.)  Every word lives on its own line.
+// cost more than the whole pass.)  Every word lives on its own line.  A word
+// means "failed" only when it holds this call's tag (p.tag), so a value left
+// in the workspace by another call is never taken for a failure of this one.
 __device__ __forceinline__ uint32_t* ff_word(const ScreenParams& p, int slot, int line) {
     return p.ff_flags + ((size_t)slot * (size_t)(1 + p.n_super) + (size_t)line) * 32u;
 }
@@ -378,7 +424,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     __shared__ double s_ssr[kWaves];
     __shared__ NonFinite s_nf[kWaves][KG];
     __shared__ uint32_t s_rel[KG];  // work-group max-rel values (binary32 bits)
-    __shared__ uint32_t s_is_last;
+    __shared__ uint32_t s_arrival;  // this work-group's ticket (0: the workspace was not clean)
     __shared__ double s_sr1;        // single-level finish: the group's sum of r^2
     // fail-fast: per wave and candidate, elements compared and their sum of r^2
     __shared__ uint32_t s_nread[FF ? kWaves : 1][FF ? KG : 1];
@@ -393,12 +439,14 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
     const float atol = p.atol, rtol = p.rtol;
 
-    // The accepted part of the table is padded to whole groups with the
-    // reference, so all KG slots hold a readable tensor.
+    // Slots past the accepted candidates (the last group's padding) read the
+    // reference, so all KG slots hold a readable tensor; they write no record.
     gbytes cand[KG];
 #pragma unroll
-    for (int j = 0; j < KG; ++j)
-        cand[j] = uniform_ptr(p.table_inline ? tab.e[j0 + j].data : p.table[j0 + j].data);
+    for (int j = 0; j < KG; ++j) {
+        const int slot = j0 + j;
+        cand[j] = uniform_ptr(slot < p.n_acc ? (p.table_inline ? tab.e[slot].data : p.table[slot].data) : p.ref);
+    }
     const gbytes ref = uniform_ptr(p.ref);
 
     uint32_t mism[KG];  // wave-uniform mismatch counts
@@ -423,7 +471,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         // candidates that failed before this work-group started are not read
         // at all (work-groups of a group whose candidates have all failed
         // then leave at once, freeing their CU for the others)
-        const uint32_t early = (uint32_t)ballot(ld_coherent(ff_word(p, j0 + (lane & (KG - 1)), 0)) != 0u) & alive;
+        const uint32_t early = (uint32_t)ballot(ld_coherent(ff_word(p, j0 + (lane & (KG - 1)), 0)) == p.tag) & alive;
         if (early != 0u && lane == 0) {
 #pragma unroll
             for (int j = 0; j < KG; ++j) {
@@ -608,7 +656,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             failed &= alive;
             // known failed: by the poll, or by another wave of this work-group
             const uint32_t told = s_told[lane & (KG - 1)];
-            const uint32_t seen = (uint32_t)ballot(polled != 0u || told != 0u) & alive;
+            const uint32_t seen = (uint32_t)ballot(polled == p.tag || told != 0u) & alive;
             // uniform as far as the compiler can tell too, so that the exit
             // below is a scalar branch and the loop stays uniform
             const uint32_t stop = __builtin_amdgcn_readfirstlane(failed | seen);
@@ -618,9 +666,9 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 const uint32_t tell = failed & ~seen;
                 if (lane < KG && ((tell >> lane) & 1u)) {
                     if (atomicOr(&s_told[lane], 1u) == 0u &&
-                        __hip_atomic_exchange(ff_word(p, j0 + lane, 1 + (stripe >> 4)), 1u, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT) == 0u)
-                        st_coherent(ff_word(p, j0 + lane, 0), 1u);
+                        __hip_atomic_exchange(ff_word(p, j0 + lane, 1 + (stripe >> 4)), p.tag, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT) != p.tag)
+                        st_coherent(ff_word(p, j0 + lane, 0), p.tag);
                 }
                 const double sr = wave_sum_f64(ssr);
                 if (lane == 0) {
@@ -718,14 +766,16 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
 
     const int C = p.blocks_per_group;
     const size_t plane = (size_t)p.n_acc * C;
+    const int S = p.n_super;
+    const int m = stripe >> 4;
     if (threadIdx.x < kg) {
         const int j = threadIdx.x;
-        uint32_t m = 0, na = 0, pi = 0, ni = 0, ma = 0, mr = 0, bd = 0;
+        uint32_t mi = 0, na = 0, pi = 0, ni = 0, ma = 0, mr = 0, bd = 0;
         double sd = 0.0;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) {
             const WaveOut& o = s_out[w][j];
-            m += o.u[PF_MISM];
+            mi += o.u[PF_MISM];
             na += o.u[PF_NAN];
             pi += o.u[PF_PINF];
             ni += o.u[PF_NINF];
@@ -746,7 +796,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             st_coherent(&p.part_u32[PF_NREAD * plane + row], nr);
             st_coherent(&p.part_ssrc[row], src);
         }
-        st_coherent(&p.part_u32[PF_MISM * plane + row], m);
+        st_coherent(&p.part_u32[PF_MISM * plane + row], mi);
         st_coherent(&p.part_u32[PF_NAN * plane + row], na);
         st_coherent(&p.part_u32[PF_PINF * plane + row], pi);
         st_coherent(&p.part_u32[PF_NINF * plane + row], ni);
@@ -771,14 +821,15 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     // has one super-group, whose combiner writes the records directly.
     // Fixed orders throughout, so the binary64 sums are the same bits on
     // every call.
-    const int S = p.n_super;
-    const int m = stripe >> 4;
     const int msize = min(16, C - 16 * m);
     complete_stores();
     __syncthreads();
-    if (threadIdx.x == 0) s_is_last = ticket(&p.tickets1[(size_t)g * S + m]) == (uint32_t)msize - 1u;
+    if (threadIdx.x == 0) s_arrival = ticket_arrive(&p.tickets1[(size_t)g * S + m], p.tag);
     __syncthreads();
-    if (!s_is_last) return;
+    if (s_arrival != (uint32_t)msize) {
+        if (s_arrival == 0u) report_dirty(p, table_of(p, tab), g, j0, kg);
+        return;
+    }
 
     const int jj = threadIdx.x >> 4;
     const int sl = threadIdx.x & 15;
@@ -856,18 +907,21 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                                  sd, s_sr1);
             }
             if (g == 0) write_rejected(p, table);
-            if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
+            if (threadIdx.x == 0) st_coherent(&p.tickets1[(size_t)g * S + m], (uint64_t)0);
             if constexpr (FF) clear_ff_words(p, j0, KG);
             return;
         }
     }
-    if (threadIdx.x == 0) p.tickets1[(size_t)g * S + m] = 0u;
+    if (threadIdx.x == 0) st_coherent(&p.tickets1[(size_t)g * S + m], (uint64_t)0);
 
     complete_stores();
     __syncthreads();
-    if (threadIdx.x == 0) s_is_last = ticket(&p.tickets2[g]) == (uint32_t)S - 1u;
+    if (threadIdx.x == 0) s_arrival = ticket_arrive(&p.tickets2[g], p.tag);
     __syncthreads();
-    if (!s_is_last) return;
+    if (s_arrival != (uint32_t)S) {
+        if (s_arrival == 0u) report_dirty(p, table, g, j0, kg);
+        return;
+    }
 
     if (jj < kg) {
         uint64_t mi = 0, na = 0, pi = 0, ni = 0, nr = 0;
@@ -936,9 +990,10 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     }
     // Group 0's finisher also writes the rejected candidates' records.
     if (g == 0) write_rejected(p, table);
-    // Leave the ticket and the failed words at zero for the next call on
-    // this workspace (every work-group of the group has finished reading).
-    if (threadIdx.x == 0) p.tickets2[g] = 0u;
+    // Leave the ticket and the failed words at zero (every work-group of the
+    // group has finished reading them): the next call on this workspace then
+    // finds them clean even if its tag happens to equal this call's.
+    if (threadIdx.x == 0) st_coherent(&p.tickets2[g], (uint64_t)0);
     if constexpr (FF) clear_ff_words(p, j0, KG);
 }
 

@@ -32,7 +32,7 @@ def test_every_declared_function_is_exported(L):
 
 
 def test_version(L):
-    assert kb.kb_version() == 100
+    assert kb.kb_version() == 20000
 
 
 def desc(data, dtype, shape, strides=None):
@@ -168,8 +168,45 @@ def test_gen_argument_errors(L):
 
 
 def test_stats_argument_errors(L):
-    assert kb.lib().kb_screen_stats(None, 4, None, None, None) == kb.KB_ERR_INVALID_ARG
-    assert kb.lib().kb_screen_stats(0x1000, -1, None, None, None) == kb.KB_ERR_INVALID_ARG
+    assert kb.lib().kb_screen_stats(None, 4, None, None, None, None) == kb.KB_ERR_INVALID_ARG
+    assert kb.lib().kb_screen_stats(0x1000, -1, None, None, None, None) == kb.KB_ERR_INVALID_ARG
+
+
+def test_large_calls_need_a_host_table(L):
+    """More than KB_INLINE_CANDS candidates: the launch table lives in the
+    caller's pinned host memory, so kb_screen (no options) refuses, and
+    kb_screen_ex refuses a missing, short or misaligned table -- all before
+    any device work."""
+    assert kb.lib().kb_screen_host_table_bytes(1) == 0
+    assert kb.lib().kb_screen_host_table_bytes(kb.KB_INLINE_CANDS) == 0
+    assert kb.lib().kb_screen_host_table_bytes(0) == 0
+    need = kb.lib().kb_screen_host_table_bytes(kb.KB_INLINE_CANDS + 1)
+    assert need >= 16 * (kb.KB_INLINE_CANDS + 1) and need % 256 == 0
+    assert kb.lib().kb_screen_host_table_bytes(1024) >= 16 * 1024
+    assert kb.lib().kb_screen_multi_host_table_bytes(3, 1024) == 3 * kb.lib().kb_screen_host_table_bytes(1024)
+    assert kb.lib().kb_screen_multi_host_table_bytes(3, 100) == 0
+    n = 300
+    ref = desc(0x10000, kb.KB_F32, (64,))
+    cands = [desc(0x20000 + 256 * k, kb.KB_F32, (64,)) for k in range(n)]
+    assert screen_rc(ref, cands) == kb.KB_ERR_WORKSPACE
+    assert "host table" in kb.kb_last_error()
+    arr = (kb.KbTensor * n)(*cands)
+    buf = (ctypes.c_uint8 * (kb.lib().kb_screen_host_table_bytes(n) + 32))()
+    base = ctypes.addressof(buf)
+    aligned = (base + 15) // 16 * 16
+
+    def ex(ptr, nbytes):
+        opts = kb.KbScreenOpts(ptr, nbytes)
+        return kb.lib().kb_screen_ex(ctypes.byref(ref), arr, n, 1e-5, 1e-5, 0, 0x100000, 1 << 30,
+                                     0x200000, ctypes.byref(opts), None)
+
+    assert ex(None, 1 << 20) == kb.KB_ERR_WORKSPACE
+    assert ex(aligned, 256) == kb.KB_ERR_WORKSPACE
+    assert ex(aligned + 8, kb.lib().kb_screen_host_table_bytes(n)) == kb.KB_ERR_ALIGNMENT
+    # a 2-candidate call ignores the options entirely (inline table)
+    assert kb.lib().kb_screen_ex(ctypes.byref(ref), arr, 2, 1e-5, 1e-5, 0, 0x100000, 16, 0x200000,
+                                 ctypes.byref(kb.KbScreenOpts(None, 0)), None) == kb.KB_ERR_WORKSPACE
+    assert "workspace of 16 bytes" in kb.kb_last_error()
 
 
 def test_missing_library_fails_loudly(monkeypatch):
@@ -188,7 +225,21 @@ def test_summarize_on_host(L):
     assert kb.kb_summarize(recs) == {"n_candidates": 5, "n_passed": 2, "n_rejected": 2,
                                      "n_failed": 1, "first_passed": 0, "first_failed": 1}
     assert kb.kb_summarize([])["n_candidates"] == 0
-    assert kb.lib().kb_summarize(None, 3, None) == kb.KB_ERR_INVALID_ARG
+    assert kb.lib().kb_summarize(None, 3, None, None) == kb.KB_ERR_INVALID_ARG
+    # the per-candidate verdicts come from the library
+    arr = (kb.KbStats * 5)()
+    for k, r in enumerate(recs):
+        for name, _ in kb.KbStats._fields_:
+            setattr(arr[k], name, r[name])
+    passed = (ctypes.c_int32 * 5)(*([7] * 5))
+    assert kb.lib().kb_summarize(arr, 5, None, passed) == kb.KB_OK
+    assert list(passed) == [1, 0, 0, 1, 0]
+    # a record written by a call that found its workspace not clean makes the
+    # verdict an error, not a rejection
+    arr[3].status = kb.KB_ERR_WORKSPACE
+    assert kb.lib().kb_summarize(arr, 5, None, passed) == kb.KB_ERR_WORKSPACE
+    assert "not clean" in kb.kb_last_error()
+    assert kb.lib().kb_summarize_multi(arr, 1, 5, ctypes.byref(kb.KbSummary()), None) == kb.KB_ERR_WORKSPACE
 
 
 def test_summarize_matches_the_verdict_rule(L):
@@ -214,6 +265,13 @@ def test_summarize_matches_the_verdict_rule(L):
                 "first_passed": ok.index(True) if any(ok) else -1,
                 "first_failed": ok.index(False) if not all(ok) else -1}
         assert kb.kb_summarize(recs) == want, (trial, recs)
+        arr = (kb.KbStats * n)()
+        for k, r in enumerate(recs):
+            for name, _ in kb.KbStats._fields_:
+                setattr(arr[k], name, r[name])
+        passed = (ctypes.c_int32 * n)()
+        assert kb.lib().kb_summarize(arr, n, None, passed) == kb.KB_OK
+        assert [bool(x) for x in passed] == ok, (trial, recs)
 
 
 def test_workspace_init_argument_errors(L):

@@ -342,19 +342,55 @@ def test_determinism_and_workspace_reuse(dev):
     assert_records_match(first, oracle_records(w.ref, w.cands, w.atol, w.rtol), "c2 1/16")
 
 
-def test_workspace_reinit_between_sizes(dev):
-    say("workspace reuse across sizes")
+@pytest.mark.parametrize("flags", [0, kb.KB_FAIL_FAST])
+def test_dirty_workspace_is_reported(dev, flags):
+    """Workspaces that break the zero-fill contract: filled with 0xFF bytes,
+    with random bytes, and used for other sizes without a new zero-fill
+    (the partials of one call then lie where the next call's counters are).
+    Every call's readback must either be the oracle's records or raise
+    KB_ERR_WORKSPACE -- never wrong records -- and the garbage fills must be
+    caught.  After kb_screen_workspace_init every call is exact again."""
     big = synth.build("c4", dev, seed=2, scale=1 / 256, K=40)
     small = synth.build("c1", dev, seed=2)
+    plan = kb.kb_screen_launch(40, big.numel, kb.KB_F16)
+    say("dirty workspace", flags, plan)
+    assert plan["n_groups"] > 1 and plan["blocks_per_group"] > 16, plan  # two-level finish
     nbytes = max(kb.kb_screen_workspace_bytes(40, big.numel, kb.KB_F16),
                  kb.kb_screen_workspace_bytes(4, small.numel, kb.KB_F32))
     ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    for w, code in ((big, kb.KB_F16), (small, kb.KB_F32), (big, kb.KB_F16)):
-        kb.kb_screen_workspace_init(ws)
+    orcs = {w.name: oracle_records(w.ref, w.cands, w.atol, w.rtol) for w in (big, small)}
+    g = torch.Generator(device=dev).manual_seed(99)
+
+    def run(w):
         st = kb.alloc_stats(len(w.cands), dev)
-        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, 0, ws, st)
-        recs, _ = kb.kb_screen_stats(st, len(w.cands))
-        assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), w.name)
+        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, flags, ws, st)
+        try:
+            recs, _ = kb.kb_screen_stats(st, len(w.cands))
+        except kb.KbError as e:
+            assert e.code == kb.KB_ERR_WORKSPACE, e
+            return None
+        orc = orcs[w.name]
+        if flags == 0:
+            assert_records_match(recs, orc, w.name)
+        else:
+            assert [r["passed"] for r in recs] == [o["passed"] for o in orc], w.name
+            assert_records_match([r for r, o in zip(recs, orc) if o["passed"]],
+                                 [o for o in orc if o["passed"]], w.name)
+        return recs
+
+    ws.fill_(0xFF)
+    assert run(big) is None, "0xFF workspace not reported"
+    ws.copy_(torch.randint(0, 256, (nbytes,), generator=g, device=dev, dtype=torch.uint8))
+    assert run(big) is None, "random workspace not reported"
+    kb.kb_screen_workspace_init(ws)
+    assert run(big) is not None
+    assert run(big) is not None  # consecutive calls of one size need nothing
+    run(small)  # other sizes without a new zero-fill: exact, or reported
+    run(big)
+    kb.kb_screen_workspace_init(ws)
+    assert run(small) is not None
+    kb.kb_screen_workspace_init(ws)
+    assert run(big) is not None
 
 
 def test_pinned_host_records_pipeline(dev):

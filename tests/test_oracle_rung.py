@@ -143,8 +143,9 @@ def test_survival_reproduces_table_a1_matvec():
 def test_promotion_rule_reproduces_fig4_counts():
     """With the fraction 2/5 of the successful non-baseline candidates (and
     the baseline carried), the rule promotes Fig. 4's numbers: 16 successes
-    at rung 0 (15 candidates + baseline) -> 6 candidates + baseline; 5 at
-    rung 1 (4 + baseline) -> 2 + baseline -- whatever the scores."""
+    at rung 0 (15 and the baseline) -> six promoted plus the baseline; 5 at
+    rung 1 (4 and the baseline) -> two plus the baseline -- whatever the
+    scores."""
     rng = np.random.default_rng(44)
     for trial in range(50):
         s0 = rng.uniform(100, 1000, 21)
