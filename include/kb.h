@@ -298,6 +298,34 @@ int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, floa
                  float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
                  kb_stats* d_stats, const kb_screen_opts* opts, hipStream_t stream);
 
+/* Bytes of the fixed device scratch of kb_screen_noalloc (enough for any call
+ * with at most KB_INLINE_CANDS candidates). */
+#define KB_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* kb_screen for callers that cannot allocate device memory -- code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  The
+ * same screen and records as kb_screen (the same kernels and launch), with
+ * the workspace replaced by a fixed scratch array in the library: this call
+ * allocates nothing (no hipMalloc, no hipFree, no allocating library routine)
+ * and needs no workspace argument.
+ *   ref, cands, n_cands, atol, rtol, flags, d_stats, stream   as for kb_screen;
+ *   n_cands <= KB_INLINE_CANDS, and the call's workspace size
+ *   (kb_screen_workspace_bytes) at most KB_NOALLOC_SCRATCH_BYTES, which holds
+ *   for every such call.
+ * Scratch: KB_NOALLOC_SCRATCH_BYTES of device memory per device, held from
+ * the first call on that device until the process ends; its address is
+ * looked up on that first call (with the device current).  Every call on a
+ * device shares that device's scratch and leaves its contents there; each
+ * call first zero-fills the part that must begin at zero (one small fill
+ * kernel on `stream`).  So two calls that can overlap on one device -- on
+ * two streams, or from two threads -- race and give wrong records; calls on
+ * different devices do not interfere.
+ * Errors (nothing launched): as for kb_screen, KB_ERR_INVALID_ARG for more
+ * than KB_INLINE_CANDS candidates or a device index beyond 63, KB_ERR_WORKSPACE
+ * when the call would need more scratch, KB_ERR_HIP. */
+int kb_screen_noalloc(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+                      float rtol, uint32_t flags, kb_stats* d_stats, hipStream_t stream);
+
 /* The verdict of each of n_cands records already in host memory (host only):
  * candidate k passes -- K(p) = 1 for its output -- iff status is
  * KB_STATUS_OK and mismatches is 0 (Section 3.1's correctness indicator;

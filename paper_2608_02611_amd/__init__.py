@@ -127,7 +127,7 @@ EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_
            "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
            "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_screen_multi",
            "kb_screen_multi_workspace_bytes", "kb_screen_multi_host_table_bytes", "kb_summarize_multi",
-           "kb_last_error", "kb_version")
+           "kb_screen_noalloc", "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -159,6 +159,9 @@ def lib():
         L.kb_screen_ex.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
                                    u32, vp, ctypes.c_size_t, vp, ctypes.POINTER(KbScreenOpts), vp]
         L.kb_screen_ex.restype = i32
+        L.kb_screen_noalloc.argtypes = [ctypes.POINTER(KbTensor), ctypes.POINTER(KbTensor), i32, f32, f32,
+                                        u32, vp, vp]
+        L.kb_screen_noalloc.restype = i32
         L.kb_screen_host_table_bytes.argtypes = [i32]
         L.kb_screen_host_table_bytes.restype = ctypes.c_size_t
         L.kb_screen_stats.argtypes = [vp, i32, ctypes.POINTER(KbStats), ctypes.POINTER(KbSummary),
@@ -373,6 +376,23 @@ def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, str
                               ctypes.byref(opts) if opts is not None else None, _stream_handle(stream)))
     _after_one_off(keep, stream)
     return d_stats, workspace
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def kb_screen_noalloc(ref, cands, atol, rtol, flags=0, d_stats=None, stream=None):
+    """Enqueue kb_screen_noalloc (the library's fixed scratch instead of a
+    workspace; at most KB_INLINE_CANDS candidates).  Returns d_stats; read
+    the records with kb_screen_stats."""
+    n = len(cands)
+    r = describe(ref)
+    arr = (KbTensor * max(1, n))(*[describe(c) for c in cands])
+    if d_stats is None:
+        d_stats = alloc_stats(max(1, n), ref.device)
+    _check(lib().kb_screen_noalloc(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
+                                   ctypes.c_void_p(d_stats.data_ptr()), _stream_handle(stream)))
+    return d_stats
 
 
 def kb_screen_stats(d_stats, n_cands, stream=None):

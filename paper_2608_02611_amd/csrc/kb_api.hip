@@ -2,6 +2,7 @@
 // validation, the policy gate, launch planning and the statistics readback.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <cstdlib>
@@ -13,6 +14,12 @@
 #include "kb_device.hpp"
 #include "kb_internal.hpp"
 #include "kb_rung.hpp"
+
+// Fixed device scratch of kb_screen_noalloc: a workspace for callers that
+// cannot allocate.  Each device that runs the library holds its own copy
+// until the process ends.  Host code never uses this name as an address:
+// kb::noalloc_scratch() asks the runtime for the copy on the current device.
+static __device__ __align__(256) unsigned char scratch[KB_NOALLOC_SCRATCH_BYTES];
 
 namespace kb {
 namespace {
@@ -120,6 +127,29 @@ uint32_t call_tag() {
     x *= 0xC4CEB9FE1A85EC53ull;
     x ^= x >> 33;
     return ((uint32_t)x ^ (uint32_t)(x >> 32)) | 1u;
+}
+
+// Address of `scratch` on each device, looked up once per device (with that
+// device current) and kept for the process.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
+// The scratch's address on device `dev` (the current device), in *out;
+// KB_OK or an error code.
+int noalloc_scratch(int dev, void** out) {
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_noalloc: device %d beyond the %d the library tracks",
+                    dev, kMaxDevices);
+    void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr)
+            return fail(KB_ERR_HIP, "kb_screen_noalloc: hipGetSymbolAddress(scratch): %s",
+                        hipGetErrorString(e));
+        g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return KB_OK;
 }
 
 // A record that a kernel wrote with status KB_ERR_WORKSPACE: the call found
@@ -422,6 +452,40 @@ static int check_screen_args(const char* who, const kb_tensor* ref, const kb_ten
 }
 
 size_t kb_screen_host_table_bytes(int n_cands) { return n_cands < 1 ? 0 : host_table_bytes(n_cands); }
+
+int kb_screen_noalloc(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
+                      float rtol, uint32_t flags, kb_stats* d_stats, hipStream_t stream) {
+    clear_error();
+    int rc = check_screen_args("kb_screen_noalloc", ref, cands, n_cands, atol, rtol, flags, d_stats);
+    if (rc != KB_OK) return rc;
+    if (n_cands > KB_INLINE_CANDS)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_noalloc: %d candidates, at most %d", n_cands,
+                    KB_INLINE_CANDS);
+    int32_t status[KB_INLINE_CANDS];  // on the stack: nothing is allocated
+    rc = kb_policy_check(ref, cands, n_cands, status);
+    if (rc != KB_OK) return rc;
+    ScreenPlan P;
+    const uint64_t numel = tensor_numel(*ref);
+    if (!make_plan(n_cands, n_cands, numel, ref->dtype, 0, false, &P))
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_noalloc: no launch plan (numel=%llu)",
+                    (unsigned long long)numel);
+    if (P.total > (size_t)KB_NOALLOC_SCRATCH_BYTES)
+        return fail(KB_ERR_WORKSPACE, "kb_screen_noalloc: the call needs %zu bytes of scratch, the fixed "
+                    "scratch holds %zu", P.total, (size_t)KB_NOALLOC_SCRATCH_BYTES);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen_noalloc: hipGetDevice");
+    void* ws = nullptr;
+    rc = noalloc_scratch(dev, &ws);
+    if (rc != KB_OK) return rc;
+    // The scratch holds what the last call on this device left, laid out for
+    // that call's sizes: zero this call's counters and fail-fast words (the
+    // words that must begin at zero) with the fill kernel, stream-ordered.
+    e = launch_zero_fill(ws, P.off_part_u32, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_screen_noalloc: fill launch");
+    return screen_with_status("kb_screen_noalloc", ref, cands, n_cands, status, atol, rtol, flags, ws,
+                              (size_t)KB_NOALLOC_SCRATCH_BYTES, nullptr, 0, d_stats, stream);
+}
 
 int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
                  uint32_t flags, void* workspace, size_t workspace_bytes, kb_stats* d_stats,

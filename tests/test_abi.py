@@ -167,6 +167,27 @@ def test_gen_argument_errors(L):
     assert g(None, kb.KB_F32, 0, kb.KB_DIST_NORMAL, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_OK
 
 
+def test_noalloc_argument_errors(L):
+    """kb_screen_noalloc refuses, before any device work, what kb_screen
+    refuses, and more than KB_INLINE_CANDS candidates."""
+    ref = desc(0x10000, kb.KB_F32, (64,))
+    f = kb.lib().kb_screen_noalloc
+
+    def call(cands, atol=1e-5, stats=0x200000, flags=0):
+        arr = (kb.KbTensor * max(1, len(cands)))(*cands)
+        return f(ctypes.byref(ref), arr, len(cands), atol, 1e-5, flags, stats, None)
+
+    good = [desc(0x20000, kb.KB_F32, (64,))]
+    assert call([]) == kb.KB_ERR_INVALID_ARG
+    assert call(good, atol=-1.0) == kb.KB_ERR_INVALID_ARG
+    assert call(good, stats=None) == kb.KB_ERR_INVALID_ARG
+    assert call(good, flags=8) == kb.KB_ERR_INVALID_ARG
+    assert call(good * (kb.KB_INLINE_CANDS + 1)) == kb.KB_ERR_INVALID_ARG
+    assert "at most" in kb.kb_last_error()
+    assert kb.NOALLOC_SCRATCH_BYTES >= max(kb.kb_screen_workspace_bytes(kb.KB_INLINE_CANDS, 1 << 32, dt)
+                                           for dt in (kb.KB_F32, kb.KB_F16, kb.KB_BF16))
+
+
 def test_stats_argument_errors(L):
     assert kb.lib().kb_screen_stats(None, 4, None, None, None, None) == kb.KB_ERR_INVALID_ARG
     assert kb.lib().kb_screen_stats(0x1000, -1, None, None, None, None) == kb.KB_ERR_INVALID_ARG
