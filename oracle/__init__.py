@@ -16,7 +16,10 @@ import numpy as np
 from . import build as _build
 
 F32, F16, BF16, U32 = 0, 1, 2, 3
-DIST_U32, DIST_UNIFORM, DIST_NORMAL = 0, 1, 2
+DIST_U32, DIST_UNIFORM, DIST_NORMAL, DIST_STUDENT_T3 = 0, 1, 2, 3
+(PERTURB_ADD_UNIFORM, PERTURB_REL_UNIFORM, PERTURB_ADD_NORMAL, PERTURB_SCALE_WHERE,
+ PERTURB_FLIP_LSB_WHERE, PERTURB_SPECIALS, PERTURB_ZERO_SUBNORMAL_REL) = range(1, 8)
+SCATTER_NAN, SCATTER_INF_SIGN_OF_REF = 1, 2
 EQUAL_NAN = 1
 DTYPES = {"f32": F32, "f16": F16, "bf16": BF16, "u32": U32}
 NP_STORAGE = {F32: np.float32, F16: np.uint16, BF16: np.uint16, U32: np.uint32}
@@ -97,6 +100,21 @@ def lib():
         L.kbo_bf16_to_f32.restype = f32
         L.kbo_gen.argtypes = [vp, ctypes.c_int, u64, ctypes.c_int, f32, f32, u64, u32, u32, u64]
         L.kbo_gen.restype = ctypes.c_int
+        L.kbo_box_muller64.argtypes = [u32, u32, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double)]
+        L.kbo_student_t3_64.argtypes = [ctypes.POINTER(u32)]
+        L.kbo_student_t3_64.restype = ctypes.c_double
+        L.kbo_student_t3.argtypes = [ctypes.POINTER(u32)]
+        L.kbo_student_t3.restype = f32
+        L.kbo_softmax_row.argtypes = [vp, u64, vp]
+        L.kbo_gen_softmax_rows.argtypes = [vp, u64, u64, u64, f32, u64, u32, u32]
+        L.kbo_gen_softmax_rows.restype = ctypes.c_int
+        L.kbo_gen_indices.argtypes = [vp, u32, u64, u64, u32, u32]
+        L.kbo_gen_indices.restype = ctypes.c_int
+        L.kbo_perturb.argtypes = [vp, vp, ctypes.c_int, u64, ctypes.c_int, f32, f32, f32, u64, u32, u32, u64]
+        L.kbo_perturb.restype = ctypes.c_int
+        L.kbo_scatter.argtypes = [vp, vp, ctypes.c_int, u64, vp, u32, ctypes.c_int]
+        L.kbo_scatter.restype = ctypes.c_int
         L.kbo_partial_init.argtypes = [ctypes.POINTER(Partial)]
         L.kbo_screen_range.argtypes = [ctypes.c_int, vp, vp, u64, u64, f32, f32, u32,
                                        ctypes.POINTER(Partial)]
@@ -170,6 +188,67 @@ def gen(dtype, n, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=0):
     if rc != 0:
         raise ValueError("invalid (dtype, dist) pair")
     return out
+
+
+def box_muller64(xa, xb):
+    """(cosine, sine) branches in binary64, unrounded."""
+    c, s_ = ctypes.c_double(), ctypes.c_double()
+    lib().kbo_box_muller64(xa, xb, ctypes.byref(c), ctypes.byref(s_))
+    return c.value, s_.value
+
+
+def student_t3(words, exact=False):
+    """Student-t (3) of one block's four words: binary32, or binary64 with exact=True."""
+    w = (ctypes.c_uint32 * 4)(*words)
+    return lib().kbo_student_t3_64(w) if exact else lib().kbo_student_t3(w)
+
+
+def softmax_row(x):
+    """Softmax of one row of binary32 logits (binary64 inside, rounded once)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty_like(x)
+    lib().kbo_softmax_row(x.ctypes.data, x.size, out.ctypes.data)
+    return out
+
+
+def gen_softmax_rows(rows, cols, sigma, seed=0, stream_id=0, sub=0, row0=0):
+    """Rows row0..row0+rows-1 of the softmax tensor of NORMAL(0, sigma) logits, float32 [rows, cols]."""
+    out = np.empty((rows, cols), dtype=np.float32)
+    if lib().kbo_gen_softmax_rows(out.ctypes.data, row0, rows, cols, sigma, seed, stream_id, sub) != 0:
+        raise ValueError("cols must be >= 1")
+    return out
+
+
+def gen_indices(m, n, seed=0, stream_id=0, sub=0):
+    """m distinct indices in [0, n) in draw order (uint64 array)."""
+    out = np.empty(max(1, m), dtype=np.uint64)
+    if lib().kbo_gen_indices(out.ctypes.data, m, n, seed, stream_id, sub) != 0:
+        raise ValueError("need 1 <= n and m <= n")
+    return out[:m]
+
+
+def perturb(src, dtype, op, a=0.0, b=0.0, p=0.0, seed=0, stream_id=0, sub=0, offset=0):
+    """A new storage array: the planted change `op` applied to storage array src."""
+    code = _code(dtype)
+    src = _storage(src, code)
+    out = np.empty_like(src)
+    rc = lib().kbo_perturb(out.ctypes.data, src.ctypes.data, code, src.size, op, a, b, p, seed, stream_id,
+                           sub, offset)
+    if rc != 0:
+        raise ValueError("op %d not defined for dtype code %d" % (op, code))
+    return out
+
+
+def scatter(dst, ref, dtype, idx, mode):
+    """In place: dst[idx] = NaN (mode 1) or the infinity with ref's sign (mode 2)."""
+    code = _code(dtype)
+    dst = _storage(dst, code)
+    ref = _storage(ref, code)
+    idx = np.ascontiguousarray(idx, dtype=np.uint64)
+    if lib().kbo_scatter(dst.ctypes.data, ref.ctypes.data, code, dst.size, idx.ctypes.data, idx.size,
+                         mode) != 0:
+        raise ValueError("bad mode or dtype")
+    return dst
 
 
 def _storage(a, code):

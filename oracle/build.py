@@ -9,7 +9,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libkbo.so")
-SOURCES = [os.path.join(HERE, "kbo.c"), os.path.join(HERE, "kbo_rung.c")]
+SOURCES = [os.path.join(HERE, "kbo.c"), os.path.join(HERE, "kbo_rung.c"), os.path.join(HERE, "kbo_derived.c")]
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra"]
 

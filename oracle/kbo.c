@@ -111,13 +111,19 @@ float kbo_uniform(uint32_t x, float a, float b) {
 /* 2*pi rounded to the nearest binary64. */
 #define KBO_TWO_PI 6.283185307179586476925286766559
 
-float kbo_normal01(uint32_t xa, uint32_t xb, int odd) {
+void kbo_box_muller64(uint32_t xa, uint32_t xb, double* zc, double* zs) {
     double u1 = ((double)xa + 1.0) * 0x1p-32; /* (0, 1], exact */
     double u2 = (double)xb * 0x1p-32;         /* [0, 1), exact */
     double rho = sqrt(-2.0 * log(u1));
     double theta = KBO_TWO_PI * u2;
-    double z = odd ? rho * sin(theta) : rho * cos(theta);
-    return (float)z;
+    *zc = rho * cos(theta);
+    *zs = rho * sin(theta);
+}
+
+float kbo_normal01(uint32_t xa, uint32_t xb, int odd) {
+    double zc, zs;
+    kbo_box_muller64(xa, xb, &zc, &zs);
+    return (float)(odd ? zs : zc);
 }
 
 /* ---------------------------------------------------------------------------
@@ -189,17 +195,26 @@ float kbo_bf16_to_f32(uint16_t h) { return bits_f32((uint32_t)h << 16); }
 /* ---------------------------------------------------------------------------
  * Generator: element g = offset + j comes from word (g mod 4) of block g / 4;
  * a normal takes the word pair of its half-block, the cosine branch for even
- * g and the sine branch for odd g.
+ * g and the sine branch for odd g.  A Student-t value takes all of block g.
  * ------------------------------------------------------------------------- */
 int kbo_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
             uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset) {
     if (dist == KBO_DIST_U32 && dtype != KBO_U32) return -1;
     if (dist != KBO_DIST_U32 && dtype == KBO_U32) return -1;
-    if (dist < 0 || dist > 2 || dtype < 0 || dtype > 3) return -1;
+    if (dist < 0 || dist > 3 || dtype < 0 || dtype > 3) return -1;
     fpenv_guard env = fpenv_enter();
     for (uint64_t j = 0; j < n; ++j) {
         uint64_t g = offset + j;
         uint32_t w[4];
+        if (dist == KBO_DIST_STUDENT_T3) {
+            /* one whole block per element */
+            kbo_stream_block(seed, stream_id, sub, g, w);
+            float v = fmaf(kbo_student_t3(w), p1, p0);
+            if (dtype == KBO_F32) ((float*)dst)[j] = v;
+            else if (dtype == KBO_F16) ((uint16_t*)dst)[j] = kbo_f32_to_f16(v);
+            else ((uint16_t*)dst)[j] = kbo_f32_to_bf16(v);
+            continue;
+        }
         kbo_stream_block(seed, stream_id, sub, g >> 2, w);
         unsigned word = (unsigned)(g & 3u);
         if (dist == KBO_DIST_U32) {

@@ -34,7 +34,7 @@ extern "C" {
 #endif
 
 enum { KBO_F32 = 0, KBO_F16 = 1, KBO_BF16 = 2, KBO_U32 = 3 };
-enum { KBO_DIST_U32 = 0, KBO_DIST_UNIFORM = 1, KBO_DIST_NORMAL = 2 };
+enum { KBO_DIST_U32 = 0, KBO_DIST_UNIFORM = 1, KBO_DIST_NORMAL = 2, KBO_DIST_STUDENT_T3 = 3 };
 enum { KBO_EQUAL_NAN = 1u };
 
 /* Philox4x32-10 block function (SC'11, Section 4 "Philox"): ten rounds of
@@ -51,6 +51,10 @@ void kbo_stream_block(uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t 
 float kbo_u01(uint32_t x);
 /* U(a, b) value: fmaf(u, fl32(b - a), a), one rounding. */
 float kbo_uniform(uint32_t x, float a, float b);
+/* Box-Muller on one word pair in binary64: u1 = (xa + 1) 2^-32, u2 = xb 2^-32,
+ * rho = sqrt(-2 ln u1), theta = 2 pi u2 (2 pi rounded to binary64); the
+ * cosine and sine branches rho cos(theta), rho sin(theta), unrounded. */
+void kbo_box_muller64(uint32_t xa, uint32_t xb, double* zc, double* zs);
 /* Standard normal from one word pair by the Box-Muller transform, in
  * binary64 then rounded once to binary32.  odd = 0 takes the cosine branch,
  * odd = 1 the sine branch. */
@@ -64,10 +68,81 @@ float kbo_bf16_to_f32(uint16_t h);
 
 /* Fill dst[0..n) with elements offset..offset+n-1 of the stream.
  * dist U32 needs dtype U32; UNIFORM takes [p0, p1); NORMAL takes mean p0,
- * standard deviation p1.  16-bit dtypes round the binary32 value to nearest
- * even.  Returns 0, or -1 for an invalid (dtype, dist) pair. */
+ * standard deviation p1; STUDENT_T3 takes location p0 and scale p1, element g
+ * being kbo_student_t3 of block g.  16-bit dtypes round the binary32 value
+ * to nearest even.  Returns 0, or -1 for an invalid (dtype, dist) pair. */
 int kbo_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
             uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset);
+
+/* ---- derived inputs (kbo_derived.c) ---- */
+
+/* Student-t with 3 degrees of freedom from one block's four words: the four
+ * binary64 normals z0, z1 (Box-Muller on words 0, 1) and z2, z3 (words 2, 3),
+ * t = z0 / sqrt(((z1^2 + z2^2) + z3^2) / 3) in binary64 (the ratio of a
+ * normal to the root of an independent chi-square over its 3 degrees of
+ * freedom), then rounded once to binary32. */
+double kbo_student_t3_64(const uint32_t w[4]);
+float kbo_student_t3(const uint32_t w[4]);
+
+/* Softmax of one row of binary32 logits x[0..n), n >= 1, in binary64:
+ * m = max x, e_j = exp(x_j - m), s = e_0 + e_1 + ... (left to right),
+ * out_j = e_j / s rounded once to binary32. */
+void kbo_softmax_row(const float* x, uint64_t n, float* out);
+/* Rows row0 .. row0 + rows - 1 of a [*][cols] softmax tensor whose logits are
+ * the NORMAL stream (mean 0, standard deviation sigma): logit (i, j) is
+ * element i cols + j of kbo_gen(F32, NORMAL, 0, sigma).  dst holds
+ * rows * cols binary32 values.  Returns 0, or -1 for cols = 0. */
+int kbo_gen_softmax_rows(float* dst, uint64_t row0, uint64_t rows, uint64_t cols, float sigma,
+                         uint64_t seed, uint32_t stream_id, uint32_t sub);
+
+/* m distinct indices in [0, n), in draw order: draw j = 0, 1, 2, ... is
+ * ((w1 << 32) | w0) mod n of block j of the stream; a draw equal to an
+ * earlier accepted index is skipped.  Returns 0, or -1 unless 1 <= n and
+ * m <= n. */
+int kbo_gen_indices(uint64_t* out, uint32_t m, uint64_t n, uint64_t seed, uint32_t stream_id,
+                    uint32_t sub);
+
+/* Planted changes of a seeded candidate (dst[j] from src[j], element g =
+ * offset + j; dst may be src).  x is src widened to binary32, and "narrow"
+ * rounds a binary32 value to the dtype (nearest even).  u(g) is the uniform
+ * [0, 1) value of word g mod 4 of block g / 4 (as kbo_gen UNIFORM with
+ * [0, 1)), U(g) the one with [a, b), and N(g) the NORMAL element g with mean
+ * 0 and standard deviation a; ops 6 and 7 use the four words w0..w3 of
+ * block g and take only F32.
+ *   1 ADD_UNIFORM         narrow(x + U(g))
+ *   2 REL_UNIFORM         narrow(fmaf(x, U(g), x))
+ *   3 ADD_NORMAL          narrow(x + N(g))
+ *   4 SCALE_WHERE         u(g) < p ? narrow(x * a) : src
+ *   5 FLIP_LSB_WHERE      u(g) < p ? storage bits ^ 1 : src
+ *   6 SPECIALS            with v = u01(w0), the sign s = w1 >> 31 and the
+ *                         mantissa (w2 & 0x7FFFFF) | 1: v < a: the subnormal
+ *                         of that sign and mantissa; else v < b: zero of
+ *                         sign s; else v < p: infinity of sign s; else src
+ *                         (a <= b <= p are cumulative thresholds)
+ *   7 ZERO_SUBNORMAL_REL  with v = u01(w0) and d = the [a, b) value of w1:
+ *                         v < p: a zero changes sign, a subnormal becomes
+ *                         the zero of its sign, a finite normal becomes
+ *                         fmaf(x, d, x), an infinity or NaN is kept; else src
+ * Returns 0, or -1 for an unknown op or an op/dtype pair not defined. */
+enum {
+    KBO_PERTURB_ADD_UNIFORM = 1,
+    KBO_PERTURB_REL_UNIFORM = 2,
+    KBO_PERTURB_ADD_NORMAL = 3,
+    KBO_PERTURB_SCALE_WHERE = 4,
+    KBO_PERTURB_FLIP_LSB_WHERE = 5,
+    KBO_PERTURB_SPECIALS = 6,
+    KBO_PERTURB_ZERO_SUBNORMAL_REL = 7
+};
+int kbo_perturb(void* dst, const void* src, int dtype, uint64_t n, int op, float a, float b, float p,
+                uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset);
+
+/* Set dst[idx[i]] for i < m (indices >= n are skipped): mode 1 the quiet
+ * NaN of the dtype (f32 0x7FC00000, f16 0x7E00, bf16 0x7FC0); mode 2 the
+ * infinity with the sign bit of ref[idx[i]].  Returns 0, or -1 for an
+ * unknown mode or dtype. */
+enum { KBO_SCATTER_NAN = 1, KBO_SCATTER_INF_SIGN_OF_REF = 2 };
+int kbo_scatter(void* dst, const void* ref, int dtype, uint64_t n, const uint64_t* idx, uint32_t m,
+                int mode);
 
 /* Mergeable per-candidate screening state over a range of elements.  Sums are
  * Neumaier-compensated binary64 (value = sum + comp). */

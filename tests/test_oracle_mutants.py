@@ -25,6 +25,7 @@ PHILOX = ["tests/test_oracle_philox.py"]
 MAPS = ["tests/test_oracle_maps.py", "-k", "not f32_to_f16_all_inputs and not f32_to_bf16_all_inputs"]
 RUNG = ["tests/test_oracle_rung.py"]
 LOCATE = ["tests/test_oracle_locate.py"]
+DERIVED = ["tests/test_oracle_derived.py"]
 
 # (name, source file, text, replacement, pins)
 MUTANTS = [
@@ -56,8 +57,8 @@ MUTANTS = [
      "uint32_t ctr[4] = {(uint32_t)b, (uint32_t)(b >> 32), stream_id, sub};", PHILOX),
     ("uniform_wrong_bits", "kbo.c", "return (float)(x >> 8) * 0x1p-24f;", "return (float)(x >> 9) * 0x1p-23f;",
      MAPS),
-    ("normal_sin_cos_swapped", "kbo.c", "double z = odd ? rho * sin(theta) : rho * cos(theta);",
-     "double z = odd ? rho * cos(theta) : rho * sin(theta);", MAPS),
+    ("normal_sin_cos_swapped", "kbo.c", "*zc = rho * cos(theta);\n    *zs = rho * sin(theta);",
+     "*zc = rho * sin(theta);\n    *zs = rho * cos(theta);", MAPS),
     ("normal_u1_without_offset", "kbo.c", "double u1 = ((double)xa + 1.0) * 0x1p-32;",
      "double u1 = ((double)xa + 0.5) * 0x1p-32;", MAPS),
     ("quantile_position", "kbo_rung.c", "const double h = (double)(n - 1) * p;",
@@ -99,6 +100,40 @@ MUTANTS = [
     ("bf16_nan_truncated", "kbo.c", "if (mag > 0x7f800000u) return (uint16_t)(sign | 0x7fc0u);",
      "if (mag > 0x7f800000u) return (uint16_t)(sign | (mag >> 16));", MAPS),
     ("f16_widen_subnormal_scale", "kbo.c", "ldexpf((float)man, -24)", "ldexpf((float)man, -25)", MAPS),
+    # derived inputs: Student-t, softmax rows, index draws, planted changes
+    ("t3_numerator_from_sine", "kbo_derived.c", "return z0 / sqrt(chi2 / 3.0);",
+     "return z1 / sqrt(chi2 / 3.0);", DERIVED),
+    ("t3_two_degrees_of_freedom", "kbo_derived.c", "double chi2 = (z1 * z1 + z2 * z2) + z3 * z3;",
+     "double chi2 = (z1 * z1 + z2 * z2);", DERIVED),
+    ("t3_not_divided_by_3", "kbo_derived.c", "return z0 / sqrt(chi2 / 3.0);", "return z0 / sqrt(chi2);",
+     DERIVED),
+    ("t3_numerator_in_chi_square", "kbo_derived.c", "double chi2 = (z1 * z1 + z2 * z2) + z3 * z3;",
+     "double chi2 = (z0 * z0 + z2 * z2) + z3 * z3;", DERIVED),
+    ("softmax_max_not_taken", "kbo_derived.c", "if (x[j] > m) m = x[j];", "if (0) m = x[j];", DERIVED),
+    ("softmax_sum_in_binary32", "kbo_derived.c", "double s = 0.0;", "float s = 0.0f;", DERIVED),
+    ("softmax_row_offset_dropped", "kbo_derived.c", "(row0 + i) * cols);", "i * cols);", DERIVED),
+    ("indices_words_swapped", "kbo_derived.c", "(((uint64_t)w[1] << 32) | w[0])",
+     "(((uint64_t)w[0] << 32) | w[1])", DERIVED),
+    ("indices_repeats_kept", "kbo_derived.c", "if (!seen) out[have++] = x;", "out[have++] = x;", DERIVED),
+    ("indices_block_shifted", "kbo_derived.c", "kbo_stream_block(seed, stream_id, sub, j, w);",
+     "kbo_stream_block(seed, stream_id, sub, j + 1, w);", DERIVED),
+    ("perturb_word_of_local_index", "kbo_derived.c", "const uint32_t word = w[g & 3u];",
+     "const uint32_t word = w[j & 3u];", DERIVED),
+    ("perturb_rel_not_fused", "kbo_derived.c", "store(dtype, dst, j, fmaf(x, kbo_uniform(word, a, b), x));",
+     "store(dtype, dst, j, x * kbo_uniform(word, a, b) + x);", DERIVED),
+    ("perturb_mask_inverted", "kbo_derived.c", "if (kbo_u01(word) < p) store(dtype, dst, j, x * a);",
+     "if (kbo_u01(word) >= p) store(dtype, dst, j, x * a);", DERIVED),
+    ("specials_sign_from_word0", "kbo_derived.c", "const uint32_t sign = w[1] & 0x80000000u;",
+     "const uint32_t sign = w[0] & 0x80000000u;", DERIVED),
+    ("specials_thresholds_not_cumulative", "kbo_derived.c", "else if (v < b) out = sign;",
+     "else if (v < b - a) out = sign;", DERIVED),
+    ("specials_mantissa_may_be_even", "kbo_derived.c", "(w[2] & 0x7FFFFFu) | 1u;", "(w[2] & 0x7FFFFFu);",
+     DERIVED),
+    ("flush_keeps_subnormal", "kbo_derived.c", "else if (mag < 0x00800000u) out = bits & 0x80000000u;",
+     "else if (mag < 0x00800000u) out = bits;", DERIVED),
+    ("relative_change_from_word0", "kbo_derived.c", "fmaf(x, kbo_uniform(w[1], a, b), x)",
+     "fmaf(x, kbo_uniform(w[0], a, b), x)", DERIVED),
+    ("scatter_infinity_unsigned", "kbo_derived.c", "(sign | 0x7F800000u)", "0x7F800000u", DERIVED),
 ]
 
 
