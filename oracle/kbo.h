@@ -104,7 +104,8 @@ int kbo_gen_indices(uint64_t* out, uint32_t m, uint64_t n, uint64_t seed, uint32
 
 /* Planted changes of a seeded candidate (dst[j] from src[j], element g =
  * offset + j; dst may be src).  x is src widened to binary32, and "narrow"
- * rounds a binary32 value to the dtype (nearest even).  u(g) is the uniform
+ * rounds a binary32 value to the dtype (nearest even), a NaN result becoming
+ * the dtype's positive quiet NaN (f32 0x7FC00000, f16 0x7E00, bf16 0x7FC0).  u(g) is the uniform
  * [0, 1) value of word g mod 4 of block g / 4 (as kbo_gen UNIFORM with
  * [0, 1)), U(g) the one with [a, b), and N(g) the NORMAL element g with mean
  * 0 and standard deviation a; ops 6 and 7 use the four words w0..w3 of

@@ -127,7 +127,15 @@ static float widen(int dtype, const void* src, uint64_t j) {
     return dtype == KBO_F16 ? kbo_f16_to_f32(h) : kbo_bf16_to_f32(h);
 }
 
+/* An arithmetic result, rounded to the dtype; a NaN result is stored as the
+ * dtype's positive quiet NaN (IEEE 754 leaves the sign and payload of a NaN
+ * an operation creates to the platform). */
 static void store(int dtype, void* dst, uint64_t j, float v) {
+    if (isnan(v)) {
+        if (dtype == KBO_F32) ((uint32_t*)dst)[j] = 0x7FC00000u;
+        else ((uint16_t*)dst)[j] = dtype == KBO_F16 ? 0x7E00u : 0x7FC0u;
+        return;
+    }
     if (dtype == KBO_F32) ((float*)dst)[j] = v;
     else if (dtype == KBO_F16) ((uint16_t*)dst)[j] = kbo_f32_to_f16(v);
     else ((uint16_t*)dst)[j] = kbo_f32_to_bf16(v);

@@ -380,6 +380,26 @@ def test_zero_subnormal_rel():
     assert abs(hit.mean() - 0.5) < 0.05
 
 
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_nan_results_are_canonical(dt):
+    """A NaN that the arithmetic creates (inf * e + inf with e < 0) or passes
+    on (a NaN input) is stored as the dtype's positive quiet NaN; a masked-out
+    NaN is copied bit for bit."""
+    qnan = {"f32": 0x7FC00000, "f16": 0x7E00, "bf16": 0x7FC0}[dt]
+    ui = np.uint32 if dt == "f32" else np.uint16
+    neg_nan = {"f32": 0xFFC00001, "f16": 0xFE01, "bf16": 0xFFC1}[dt]
+    src = NARROW[dt](np.full(64, np.inf, np.float32))
+    got = oracle.perturb(src, dt, oracle.PERTURB_REL_UNIFORM, -0.5, -0.25, 0.0, seed=0, stream_id=1)
+    assert np.all(got.view(ui) == qnan)
+    src = np.full(64, neg_nan, ui)
+    if dt == "f32":
+        src = src.view(np.float32)
+    got = oracle.perturb(src, dt, oracle.PERTURB_ADD_UNIFORM, 0.0, 1.0, 0.0, seed=0, stream_id=1)
+    assert np.all(got.view(ui) == qnan)
+    got = oracle.perturb(src, dt, oracle.PERTURB_SCALE_WHERE, 2.0, 0.0, 0.0, seed=0, stream_id=1)
+    assert np.all(got.view(ui) == neg_nan)
+
+
 def test_perturb_refuses_undefined_pairs():
     with pytest.raises(ValueError):
         oracle.perturb(np.zeros(4, np.uint16), "f16", oracle.PERTURB_SPECIALS)

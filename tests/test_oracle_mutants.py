@@ -134,6 +134,8 @@ MUTANTS = [
     ("relative_change_from_word0", "kbo_derived.c", "fmaf(x, kbo_uniform(w[1], a, b), x)",
      "fmaf(x, kbo_uniform(w[0], a, b), x)", DERIVED),
     ("scatter_infinity_unsigned", "kbo_derived.c", "(sign | 0x7F800000u)", "0x7F800000u", DERIVED),
+    ("created_nan_not_canonical", "kbo_derived.c", "    if (isnan(v)) {\n        if (dtype == KBO_F32)",
+     "    if (0) {\n        if (dtype == KBO_F32)", DERIVED),
 ]
 
 
