@@ -66,7 +66,12 @@ extern "C" {
 typedef enum kb_dtype { KB_F32 = 0, KB_F16 = 1, KB_BF16 = 2, KB_U32 = 3 } kb_dtype;
 
 /* Generator distributions. */
-typedef enum kb_dist { KB_DIST_U32 = 0, KB_DIST_UNIFORM = 1, KB_DIST_NORMAL = 2 } kb_dist;
+typedef enum kb_dist {
+    KB_DIST_U32 = 0,
+    KB_DIST_UNIFORM = 1,
+    KB_DIST_NORMAL = 2,
+    KB_DIST_STUDENT_T3 = 3
+} kb_dist;
 
 /* Call-level status codes (function return values). */
 enum {
@@ -520,7 +525,13 @@ int kb_rung_survival(const int32_t* entering, const int32_t* failed, const int32
  *                    or 2,3): u1 = (x_a + 1) 2^-32, u2 = x_b 2^-32,
  *                    z = sqrt(-2 ln u1) * (cos or sin)(2 pi u2) in binary64
  *                    (cosine for even g, sine for odd g), rounded to
- *                    binary32; value fmaf(z, p1, p0) (mean p0, std dev p1).
+ *                    binary32; value fmaf(z, p1, p0) (mean p0, std dev p1);
+ *   KB_DIST_STUDENT_T3  Student's t with 3 degrees of freedom from all four
+ *                    words of block g (not g / 4): the binary64 normals z0,
+ *                    z1 of words 0, 1 and z2, z3 of words 2, 3 (as above,
+ *                    unrounded), t = z0 / sqrt(((z1^2 + z2^2) + z3^2) / 3) in
+ *                    binary64, rounded to binary32; value fmaf(t, p1, p0).
+ *                    A heavy-tailed output (its fourth moment is infinite).
  *   F16 / BF16 dtypes round the binary32 value to nearest even.
  * dst: device, 16-byte aligned.  Errors: KB_ERR_INVALID_ARG (null dst with
  * n > 0, non-finite p0/p1), KB_ERR_DTYPE (U32 with a float distribution or
@@ -528,6 +539,81 @@ int kb_rung_survival(const int32_t* entering, const int32_t* failed, const int32
 int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
                   uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
                   hipStream_t stream);
+
+/* ------------------------------------------------- derived seeded inputs --
+ * The synthetic outputs a screen is measured on, built from the same stream:
+ * a reference and candidates with planted differences (the Verifier checks
+ * a candidate's output against the reference's on seeded inputs, Sections
+ * 3.1 and 3.4).  All stream-ordered on `stream`, device buffers 16-byte
+ * aligned, nothing launched on error. */
+
+/* Rows of softmax probabilities: dst is a [rows][cols] binary32 tensor (dtype
+ * KB_F32 only); its logits are the NORMAL stream with mean 0 and standard
+ * deviation sigma (logit (i, j) is element i cols + j of kb_gen_inputs(F32,
+ * NORMAL, 0, sigma)), and each row is, in binary64, m = max x,
+ * p_j = exp(x_j - m) / sum_k exp(x_k - m), rounded once to binary32.  The
+ * binary64 row sum is a fixed tree (the same bits on every call; within
+ * rounding of a left-to-right sum).  Every p_j > 0 unless it underflows.
+ * Errors: KB_ERR_INVALID_ARG (cols = 0 with rows > 0, null dst, sigma not
+ * finite), KB_ERR_DTYPE, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_gen_softmax_rows(void* dst, int dtype, uint64_t rows, uint64_t cols, float sigma,
+                        uint64_t seed, uint32_t stream_id, uint32_t sub, hipStream_t stream);
+
+/* Most indices kb_gen_indices draws. */
+#define KB_MAX_INDICES 4096
+
+/* m distinct element indices in [0, n), in draw order, to device dst[0..m)
+ * (uint64): draw j = 0, 1, 2, ... is ((w1 << 32) | w0) mod n of block j of
+ * the stream (seed, stream_id, sub); a draw equal to an earlier one is
+ * skipped.  Requires 1 <= m <= KB_MAX_INDICES and 2 m <= n (each draw is then
+ * new with probability at least 1/2; a draw count cap of 2^20, never reached
+ * in practice, bounds the kernel, and entries it did not fill would be
+ * UINT64_MAX).  Errors: KB_ERR_INVALID_ARG, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_gen_indices(uint64_t* dst, uint32_t m, uint64_t n, uint64_t seed, uint32_t stream_id,
+                   uint32_t sub, hipStream_t stream);
+
+/* Planted changes (kb_gen_perturb ops).  x is src[j] widened to binary32 and
+ * "narrow" rounds a binary32 value to the dtype (nearest even); a NaN result
+ * is stored as the dtype's positive quiet NaN (0x7FC00000, 0x7E00, 0x7FC0),
+ * whatever NaN the arithmetic produced.  For element g = offset + j: u(g) is
+ * kb_gen_inputs(UNIFORM, 0, 1) element g, U(g) the UNIFORM [a, b) element g,
+ * N(g) the NORMAL element g with mean 0 and standard deviation a; ops 6 and 7
+ * take the four words w0..w3 of block g and the dtype KB_F32 only, and
+ * u01(w) = (w >> 8) 2^-24. */
+enum {
+    KB_PERTURB_ADD_UNIFORM = 1,      /* narrow(x + U(g)) */
+    KB_PERTURB_REL_UNIFORM = 2,      /* narrow(fmaf(x, U(g), x)): relative noise, one rounding */
+    KB_PERTURB_ADD_NORMAL = 3,       /* narrow(x + N(g)) */
+    KB_PERTURB_SCALE_WHERE = 4,      /* u(g) < p ? narrow(x * a) : src[j] */
+    KB_PERTURB_FLIP_LSB_WHERE = 5,   /* u(g) < p ? storage bits ^ 1 : src[j] */
+    KB_PERTURB_SPECIALS = 6,         /* v = u01(w0), sign = top bit of w1: v < a: the subnormal
+                                        with mantissa (w2 & 0x7FFFFF) | 1; else v < b: zero; else
+                                        v < p: infinity; else src[j] (a <= b <= p cumulative) */
+    KB_PERTURB_ZERO_SUBNORMAL_REL = 7 /* v = u01(w0), d = the [a, b) value of w1: v < p: a zero
+                                         flips its sign, a subnormal becomes the zero of its sign,
+                                         a finite normal x becomes fmaf(x, d, x), an infinity or
+                                         NaN stays; else src[j] */
+};
+
+/* dst[j] = op(src[j]) for j < n (dst may equal src; dtype F32, F16 or BF16).
+ * Errors: KB_ERR_INVALID_ARG (unknown op, a, b or p not finite, null
+ * pointers with n > 0, offset + n overflowing), KB_ERR_DTYPE (ops 6-7 on a
+ * 16-bit dtype), KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_gen_perturb(void* dst, const void* src, int dtype, uint64_t n, int op, float a, float b,
+                   float p, uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
+                   hipStream_t stream);
+
+/* Scatter modes. */
+enum {
+    KB_SCATTER_NAN = 1,             /* the dtype's quiet NaN: 0x7FC00000, 0x7E00 (f16), 0x7FC0 (bf16) */
+    KB_SCATTER_INF_SIGN_OF_REF = 2  /* the infinity with the sign bit of ref[idx] */
+};
+
+/* For i < m: dst[idx[i]] = the mode's value (an index >= n is skipped).
+ * dst, ref: device tensors of n elements of dtype; idx: device uint64[m].
+ * Errors: KB_ERR_INVALID_ARG, KB_ERR_DTYPE, KB_ERR_ALIGNMENT, KB_ERR_HIP. */
+int kb_gen_scatter(void* dst, const void* ref, int dtype, uint64_t n, const uint64_t* idx, uint32_t m,
+                   int mode, hipStream_t stream);
 
 /* ----------------------------------------------------------------- misc -- */
 

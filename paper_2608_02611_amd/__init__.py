@@ -21,7 +21,11 @@ LIB_PATH = os.path.join(HERE, "libkb.so")
 
 # Codes shared with include/kb.h.
 KB_F32, KB_F16, KB_BF16, KB_U32 = 0, 1, 2, 3
-KB_DIST_U32, KB_DIST_UNIFORM, KB_DIST_NORMAL = 0, 1, 2
+KB_DIST_U32, KB_DIST_UNIFORM, KB_DIST_NORMAL, KB_DIST_STUDENT_T3 = 0, 1, 2, 3
+(KB_PERTURB_ADD_UNIFORM, KB_PERTURB_REL_UNIFORM, KB_PERTURB_ADD_NORMAL, KB_PERTURB_SCALE_WHERE,
+ KB_PERTURB_FLIP_LSB_WHERE, KB_PERTURB_SPECIALS, KB_PERTURB_ZERO_SUBNORMAL_REL) = range(1, 8)
+KB_SCATTER_NAN, KB_SCATTER_INF_SIGN_OF_REF = 1, 2
+KB_MAX_INDICES = 4096
 KB_OK = 0
 KB_ERR_INVALID_ARG, KB_ERR_DTYPE, KB_ERR_WORKSPACE, KB_ERR_ALIGNMENT, KB_ERR_HIP = -1, -2, -3, -4, -5
 KB_STATUS_OK, KB_REJECT_NULL, KB_REJECT_DTYPE, KB_REJECT_SHAPE, KB_REJECT_LAYOUT = 0, 1, 2, 3, 4
@@ -127,7 +131,8 @@ EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_
            "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
            "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_screen_multi",
            "kb_screen_multi_workspace_bytes", "kb_screen_multi_host_table_bytes", "kb_summarize_multi",
-           "kb_screen_noalloc", "kb_last_error", "kb_version")
+           "kb_screen_noalloc", "kb_gen_softmax_rows", "kb_gen_indices", "kb_gen_perturb", "kb_gen_scatter",
+           "kb_last_error", "kb_version")
 
 _lib = None
 
@@ -190,6 +195,14 @@ def lib():
         L.kb_summarize_multi.restype = i32
         L.kb_gen_inputs.argtypes = [vp, i32, u64, i32, f32, f32, u64, u32, u32, u64, vp]
         L.kb_gen_inputs.restype = i32
+        L.kb_gen_softmax_rows.argtypes = [vp, i32, u64, u64, f32, u64, u32, u32, vp]
+        L.kb_gen_softmax_rows.restype = i32
+        L.kb_gen_indices.argtypes = [vp, u32, u64, u64, u32, u32, vp]
+        L.kb_gen_indices.restype = i32
+        L.kb_gen_perturb.argtypes = [vp, vp, i32, u64, i32, f32, f32, f32, u64, u32, u32, u64, vp]
+        L.kb_gen_perturb.restype = i32
+        L.kb_gen_scatter.argtypes = [vp, vp, i32, u64, vp, u32, i32, vp]
+        L.kb_gen_scatter.restype = i32
         L.kb_last_error.argtypes = []
         L.kb_last_error.restype = ctypes.c_char_p
         L.kb_version.argtypes = []
@@ -636,6 +649,49 @@ def kb_gen_inputs(dst, dist, p0=0.0, p1=1.0, seed=0, stream_id=0, sub=0, offset=
     _check(lib().kb_gen_inputs(ctypes.c_void_p(dst.data_ptr()), dtype_code(dst), dst.numel(),
                                int(dist), float(p0), float(p1), int(seed), int(stream_id),
                                int(sub), int(offset), _stream_handle(stream)))
+    return dst
+
+
+def kb_gen_softmax_rows(dst, sigma, seed=0, stream_id=0, sub=0, stream=None):
+    """Fill a contiguous float32 [rows, cols] tensor with softmax rows of NORMAL(0, sigma) logits."""
+    if not dst.is_contiguous() or dst.dim() != 2:
+        raise ValueError("dst must be a contiguous 2-d tensor")
+    _check(lib().kb_gen_softmax_rows(ctypes.c_void_p(dst.data_ptr()), dtype_code(dst), dst.shape[0],
+                                     dst.shape[1], float(sigma), int(seed), int(stream_id), int(sub),
+                                     _stream_handle(stream)))
+    return dst
+
+
+def kb_gen_indices(m, n, device, seed=0, stream_id=0, sub=0, stream=None):
+    """m distinct indices in [0, n), in draw order: a device int64 tensor
+    holding the library's uint64 values (all below 2^63)."""
+    torch = _torch()
+    out = torch.empty(max(1, m), dtype=torch.int64, device=device)
+    _check(lib().kb_gen_indices(ctypes.c_void_p(out.data_ptr()), int(m), int(n), int(seed), int(stream_id),
+                                int(sub), _stream_handle(stream)))
+    return out[:m]
+
+
+def kb_gen_perturb(dst, src, op, a=0.0, b=0.0, p=0.0, seed=0, stream_id=0, sub=0, offset=0, stream=None):
+    """dst = op(src) elementwise (contiguous tensors of one dtype; dst may be src)."""
+    if not (dst.is_contiguous() and src.is_contiguous()) or dst.numel() != src.numel() or dst.dtype != src.dtype:
+        raise ValueError("dst and src must be contiguous tensors of one size and dtype")
+    _check(lib().kb_gen_perturb(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), dtype_code(dst),
+                                dst.numel(), int(op), float(a), float(b), float(p), int(seed), int(stream_id),
+                                int(sub), int(offset), _stream_handle(stream)))
+    return dst
+
+
+def kb_gen_scatter(dst, ref, idx, mode, stream=None):
+    """dst[idx] = NaN (KB_SCATTER_NAN) or the infinity with ref's sign (KB_SCATTER_INF_SIGN_OF_REF)."""
+    torch = _torch()
+    if not (dst.is_contiguous() and ref.is_contiguous()) or dst.numel() != ref.numel() or dst.dtype != ref.dtype:
+        raise ValueError("dst and ref must be contiguous tensors of one size and dtype")
+    if idx.dtype != torch.int64 or not idx.is_contiguous():
+        raise ValueError("idx must be a contiguous int64 tensor")
+    _check(lib().kb_gen_scatter(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(ref.data_ptr()), dtype_code(dst),
+                                dst.numel(), ctypes.c_void_p(idx.data_ptr()), idx.numel(), int(mode),
+                                _stream_handle(stream)))
     return dst
 
 

@@ -827,7 +827,7 @@ int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1
                   uint32_t stream_id, uint32_t sub, uint64_t offset, hipStream_t stream) {
     clear_error();
     if (dtype < DT_F32 || dtype > DT_U32) return fail(KB_ERR_DTYPE, "unknown dtype %d", dtype);
-    if (dist < KB_DIST_U32 || dist > KB_DIST_NORMAL)
+    if (dist < KB_DIST_U32 || dist > KB_DIST_STUDENT_T3)
         return fail(KB_ERR_INVALID_ARG, "unknown distribution %d", dist);
     if ((dist == KB_DIST_U32) != (dtype == DT_U32))
         return fail(KB_ERR_DTYPE, "distribution %d does not produce dtype %d", dist, dtype);
@@ -837,8 +837,75 @@ int kb_gen_inputs(void* dst, int dtype, uint64_t n, int dist, float p0, float p1
     if (dst == nullptr) return fail(KB_ERR_INVALID_ARG, "dst is NULL");
     if (!aligned16(dst)) return fail(KB_ERR_ALIGNMENT, "dst not 16-byte aligned");
     if (offset + n < offset) return fail(KB_ERR_INVALID_ARG, "offset + n overflows");
-    hipError_t e = launch_gen(dst, dtype, n, dist, p0, p1, seed, stream_id, sub, offset, stream);
+    hipError_t e = dist == KB_DIST_STUDENT_T3
+                       ? launch_gen_t3(dst, dtype, n, p0, p1, seed, stream_id, sub, offset, stream)
+                       : launch_gen(dst, dtype, n, dist, p0, p1, seed, stream_id, sub, offset, stream);
     if (e != hipSuccess) return fail_hip(e, "kb_gen_inputs: kernel launch");
+    return KB_OK;
+}
+
+int kb_gen_softmax_rows(void* dst, int dtype, uint64_t rows, uint64_t cols, float sigma, uint64_t seed,
+                        uint32_t stream_id, uint32_t sub, hipStream_t stream) {
+    clear_error();
+    if (dtype != DT_F32) return fail(KB_ERR_DTYPE, "kb_gen_softmax_rows: dtype %d is not F32", dtype);
+    if (!std::isfinite(sigma)) return fail(KB_ERR_INVALID_ARG, "kb_gen_softmax_rows: sigma not finite");
+    if (rows == 0) return KB_OK;
+    if (cols == 0) return fail(KB_ERR_INVALID_ARG, "kb_gen_softmax_rows: cols = 0");
+    if (cols > ~0ull / rows) return fail(KB_ERR_INVALID_ARG, "kb_gen_softmax_rows: rows * cols overflows");
+    if (dst == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_gen_softmax_rows: dst is NULL");
+    if (!aligned16(dst)) return fail(KB_ERR_ALIGNMENT, "kb_gen_softmax_rows: dst not 16-byte aligned");
+    hipError_t e = launch_softmax_rows((float*)dst, rows, cols, sigma, seed, stream_id, sub, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_gen_softmax_rows: kernel launch");
+    return KB_OK;
+}
+
+int kb_gen_indices(uint64_t* dst, uint32_t m, uint64_t n, uint64_t seed, uint32_t stream_id, uint32_t sub,
+                   hipStream_t stream) {
+    clear_error();
+    if (m < 1 || m > KB_MAX_INDICES)
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_indices: m = %u not in [1, %d]", m, KB_MAX_INDICES);
+    if (n < 2 * (uint64_t)m)
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_indices: n = %llu < 2 m", (unsigned long long)n);
+    if (dst == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_gen_indices: dst is NULL");
+    if (!aligned16(dst)) return fail(KB_ERR_ALIGNMENT, "kb_gen_indices: dst not 16-byte aligned");
+    hipError_t e = launch_indices(dst, m, n, seed, stream_id, sub, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_gen_indices: kernel launch");
+    return KB_OK;
+}
+
+int kb_gen_perturb(void* dst, const void* src, int dtype, uint64_t n, int op, float a, float b, float p,
+                   uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset, hipStream_t stream) {
+    clear_error();
+    if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "kb_gen_perturb: dtype %d not F32, F16 or BF16", dtype);
+    if (op < KB_PERTURB_ADD_UNIFORM || op > KB_PERTURB_ZERO_SUBNORMAL_REL)
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_perturb: unknown op %d", op);
+    if (op >= KB_PERTURB_SPECIALS && dtype != DT_F32)
+        return fail(KB_ERR_DTYPE, "kb_gen_perturb: op %d takes F32 only", op);
+    if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(p))
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_perturb: a, b and p must be finite");
+    if (n == 0) return KB_OK;
+    if (dst == nullptr || src == nullptr) return fail(KB_ERR_INVALID_ARG, "kb_gen_perturb: dst or src is NULL");
+    if (!aligned16(dst) || !aligned16(src))
+        return fail(KB_ERR_ALIGNMENT, "kb_gen_perturb: dst or src not 16-byte aligned");
+    if (offset + n < offset) return fail(KB_ERR_INVALID_ARG, "kb_gen_perturb: offset + n overflows");
+    hipError_t e = launch_perturb(dst, src, dtype, n, op, a, b, p, seed, stream_id, sub, offset, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_gen_perturb: kernel launch");
+    return KB_OK;
+}
+
+int kb_gen_scatter(void* dst, const void* ref, int dtype, uint64_t n, const uint64_t* idx, uint32_t m, int mode,
+                   hipStream_t stream) {
+    clear_error();
+    if (!is_float_dtype(dtype)) return fail(KB_ERR_DTYPE, "kb_gen_scatter: dtype %d not F32, F16 or BF16", dtype);
+    if (mode != KB_SCATTER_NAN && mode != KB_SCATTER_INF_SIGN_OF_REF)
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_scatter: unknown mode %d", mode);
+    if (m == 0 || n == 0) return KB_OK;
+    if (dst == nullptr || ref == nullptr || idx == nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_gen_scatter: dst, ref or idx is NULL");
+    if (!aligned16(dst) || !aligned16(ref) || ((uintptr_t)idx & 7u))
+        return fail(KB_ERR_ALIGNMENT, "kb_gen_scatter: dst or ref not 16-byte, or idx not 8-byte, aligned");
+    hipError_t e = launch_scatter(dst, ref, dtype, n, idx, m, mode, stream);
+    if (e != hipSuccess) return fail_hip(e, "kb_gen_scatter: kernel launch");
     return KB_OK;
 }
 

@@ -176,5 +176,17 @@ hipError_t launch_fill_u32(void* dst, uint64_t n_words, uint32_t value, hipStrea
 hipError_t launch_gen(void* dst, int dtype, uint64_t n, int dist, float p0, float p1,
                       uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
                       hipStream_t stream);
+// Derived seeded inputs (kb_gen.hip); arguments validated by the caller.
+hipError_t launch_gen_t3(void* dst, int dtype, uint64_t n, float p0, float p1, uint64_t seed,
+                         uint32_t stream_id, uint32_t sub, uint64_t offset, hipStream_t stream);
+hipError_t launch_softmax_rows(float* dst, uint64_t rows, uint64_t cols, float sigma, uint64_t seed,
+                               uint32_t stream_id, uint32_t sub, hipStream_t stream);
+hipError_t launch_indices(uint64_t* dst, uint32_t m, uint64_t n, uint64_t seed, uint32_t stream_id,
+                          uint32_t sub, hipStream_t stream);
+hipError_t launch_perturb(void* dst, const void* src, int dtype, uint64_t n, int op, float a, float b,
+                          float p, uint64_t seed, uint32_t stream_id, uint32_t sub, uint64_t offset,
+                          hipStream_t stream);
+hipError_t launch_scatter(void* dst, const void* ref, int dtype, uint64_t n, const uint64_t* idx,
+                          uint32_t m, int mode, hipStream_t stream);
 
 }  // namespace kb

@@ -1,27 +1,39 @@
-"""Seeded synthetic screening workloads (shared input generator).
+"""Seeded synthetic screening workloads: recipes, and their construction on
+the GPU by the library's own seeded generator.
 
-This module only synthesizes inputs: a reference output and K candidate
-outputs per workload, built with torch's own seeded generator on the device
-they will be screened on.  It holds none of the screening arithmetic and none
-of the library's generator; the parity tests hand the same bytes to the HIP
-library (on the GPU) and to the CPU oracle (after a copy to the host).
+A workload is a reference output and K candidate outputs with planted
+differences (the Verifier checks a candidate's output against the
+reference's on seeded inputs).  Each tensor is described by a recipe -- a
+list of generator steps, each naming a stream (seed, stream_id, sub) of the
+Philox4x32-10 counter-based generator and the parameters of one library
+call -- so that the same recipe can be carried out by two independent
+implementations: `build()` here runs it on the GPU through the library
+(kb_gen_inputs, kb_gen_softmax_rows, kb_gen_indices, kb_gen_perturb,
+kb_gen_scatter; torch only allocates, copies and zero-fills), and the
+oracle package runs it on the CPU (oracle.workloads).  This module holds
+no generator or screening arithmetic of its own: only the recipes (stream
+ids and parameters) and the calls.
+
+Streams: stream_id = (workload << 8) | purpose, purposes REF 0, NOISE 1,
+MASK 2, INDEX 3; sub = the candidate index (0 for the reference); seed 0.
 
 Workloads (the five screening configurations):
 
-  c1  K=4,    N=65,536 fp32,        atol=rtol=1e-5: reference N(0,1); a copy,
-      a copy with U(+-1e-6) noise, one with 5 NaNs at drawn indices, one with
-      1% of its elements scaled by 1.01;
+  c1  K=4,    N=65,536 fp32,        atol=rtol=1e-5: reference N(0,1) (seed 0);
+      c0 a copy; c1 + U(-1e-6, 1e-6); c2 with NaN at 5 drawn indices;
+      c3 x 1.01 where u < 0.01;
   c2  K=16,   4096x4096 bf16,       atol=rtol=1e-2: reference bf16(64 z);
-      candidate k is bf16(r + r eps), eps ~ U(-s_k, s_k), s_k = 2^(-8 + 2k/15),
-      and candidates 0 and 1 also get a drawn 64x64 tile set to 0;
-  c3  K=1024, 256x1024 fp32,        atol=1e-6, rtol=1e-5: softmax rows of
-      2 z (binary64, rounded); candidate k adds s_k z, s_k log-spaced 1e-9..1e-3;
+      candidate k is bf16(fmaf(r, e, r)), e ~ U(-s_k, s_k), s_k = 2^(-8 + 2k/15),
+      and candidates 0 and 1 also get a drawn 64x64 tile set to +0;
+  c3  K=1024, 256x1024 fp32,        atol=1e-6, rtol=1e-5: softmax rows of 2 z
+      (binary64, rounded once); candidate k adds s_k z, s_k = 10^(-9 + 6k/1023);
   c4  K=64,   8x2048x4096 fp16,     atol=rtol=1e-3: reference fp16(z); by k mod
-      4: a copy, last-bit flips on 0.1% of elements, 64 infinities with the
+      4: a copy, last-bit flips where u < 0.001, 64 drawn infinities with the
       sign of r, both;
   c5  K=8,    2^30 fp32,            atol=1e-8, rtol=1e-6: Student-t (3) with
-      subnormals, signed zeros and infinities; per element with probability
-      1/2 a zero-sign flip, a subnormal flush or a 1e-7 relative change.
+      subnormals (2^-10), signed zeros (2^-10) and infinities (2^-20) planted;
+      per element with probability 1/2 a zero-sign flip, a subnormal flush
+      or a relative change of up to 1e-7.
 
 Every workload also has a scaled form (`scale` < 1 shrinks N, keeping the
 recipe) for the oracle-sized parity cases.
@@ -30,26 +42,144 @@ import math
 from dataclasses import dataclass, field
 from typing import List
 
-import torch
-
 SPECS = {
-    "c1": dict(K=4, shape=(65536,), dtype=torch.float32, atol=1e-5, rtol=1e-5),
-    "c2": dict(K=16, shape=(4096, 4096), dtype=torch.bfloat16, atol=1e-2, rtol=1e-2),
-    "c3": dict(K=1024, shape=(256, 1024), dtype=torch.float32, atol=1e-6, rtol=1e-5),
-    "c4": dict(K=64, shape=(8, 2048, 4096), dtype=torch.float16, atol=1e-3, rtol=1e-3),
-    "c5": dict(K=8, shape=(1 << 30,), dtype=torch.float32, atol=1e-8, rtol=1e-6),
+    "c1": dict(K=4, shape=(65536,), dtype="f32", atol=1e-5, rtol=1e-5),
+    "c2": dict(K=16, shape=(4096, 4096), dtype="bf16", atol=1e-2, rtol=1e-2),
+    "c3": dict(K=1024, shape=(256, 1024), dtype="f32", atol=1e-6, rtol=1e-5),
+    "c4": dict(K=64, shape=(8, 2048, 4096), dtype="f16", atol=1e-3, rtol=1e-3),
+    "c5": dict(K=8, shape=(1 << 30,), dtype="f32", atol=1e-8, rtol=1e-6),
 }
+CFG = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 
-# purposes of the independent seeded draws
-REF, NOISE, MASK, INDEX, AUX = 0, 1, 2, 3, 4
-CHUNK = 1 << 26  # elements per construction chunk (bounds temporaries)
+# purposes of the independent seeded streams
+REF, NOISE, MASK, INDEX = 0, 1, 2, 3
 
+# generator codes (the library's and the oracle's, which agree)
+DIST_UNIFORM, DIST_NORMAL, DIST_STUDENT_T3 = 1, 2, 3
+(ADD_UNIFORM, REL_UNIFORM, ADD_NORMAL, SCALE_WHERE, FLIP_LSB_WHERE, SPECIALS,
+ ZERO_SUBNORMAL_REL) = range(1, 8)
+SCATTER_NAN, SCATTER_INF_SIGN_OF_REF = 1, 2
+
+# c5's planted specials: cumulative thresholds on u (subnormal, zero, infinity)
+SUBNORMAL_P = 2.0 ** -10
+ZERO_P = 2.0 ** -9
+INF_P = 2.0 ** -9 + 2.0 ** -20
+
+
+def f32(x):
+    """x rounded to binary32 (the parameters both builders are given)."""
+    import struct
+    return struct.unpack("f", struct.pack("f", x))[0]
+
+
+@dataclass
+class Step:
+    """One generator call of a recipe.
+      gen       the tensor is the stream's `dist` with (p0, p1)
+      softmax   the tensor [rows, cols] is softmax rows of NORMAL(0, sigma)
+      perturb   the tensor is op(tensor) (kb_gen_perturb) on the stream
+      scatter   m distinct indices drawn from the stream get the mode's value
+                (the reference supplies the sign)
+      tile      a 64 x 64 tile of the [rows, cols] tensor, at (w0 mod rows/64,
+                w1 mod cols/64) from words 0 and 1 of the stream's block 0,
+                is set to +0
+    """
+    kind: str
+    stream_id: int
+    sub: int = 0
+    args: dict = field(default_factory=dict)
+
+
+@dataclass
+class Recipe:
+    name: str
+    shape: tuple
+    dtype: str          # "f32", "f16" or "bf16"
+    atol: float
+    rtol: float
+    seed: int
+    ref: List[Step]     # from nothing
+    cands: List[List[Step]]  # each from a copy of the reference
+
+    @property
+    def numel(self):
+        return math.prod(self.shape)
+
+    @property
+    def dtype_bytes(self):
+        return 4 if self.dtype == "f32" else 2
+
+
+def _sid(name, purpose):
+    return (CFG[name] << 8) | purpose
+
+
+def scaled_shape(name, scale):
+    shape = SPECS[name]["shape"]
+    if scale >= 1.0:
+        return tuple(shape)
+    if name == "c2":
+        side = max(64, int(round(math.sqrt(math.prod(shape) * scale))) // 64 * 64)
+        return (side, side)
+    if name == "c3":
+        return (max(1, int(round(shape[0] * scale))), shape[1])
+    return (max(1, int(round(math.prod(shape) * scale))),)
+
+
+def recipe(name, seed=0, scale=1.0, K=None):
+    """The recipe of workload `name` (scale < 1 shrinks N; K=None keeps K)."""
+    spec = SPECS[name]
+    shape = scaled_shape(name, scale)
+    K = spec["K"] if (K is None or name == "c1") else K
+    n = math.prod(shape)
+    ref_s, noise, mask, index = (_sid(name, p) for p in (REF, NOISE, MASK, INDEX))
+    cands = []
+    if name == "c1":
+        ref = [Step("gen", ref_s, 0, dict(dist=DIST_NORMAL, p0=0.0, p1=1.0))]
+        cands = [[],
+                 [Step("perturb", noise, 1, dict(op=ADD_UNIFORM, a=f32(-1e-6), b=f32(1e-6), p=0.0))],
+                 [Step("scatter", index, 2, dict(m=min(5, n // 2), mode=SCATTER_NAN))],
+                 [Step("perturb", mask, 3, dict(op=SCALE_WHERE, a=f32(1.01), b=0.0, p=f32(0.01)))]][:K]
+    elif name == "c2":
+        ref = [Step("gen", ref_s, 0, dict(dist=DIST_NORMAL, p0=0.0, p1=64.0))]
+        for k in range(K):
+            s = f32(2.0 ** (-8.0 + 2.0 * k / 15.0))
+            steps = [Step("perturb", noise, k, dict(op=REL_UNIFORM, a=-s, b=s, p=0.0))]
+            if k < 2 and shape[0] >= 64 and shape[1] >= 64:
+                steps.append(Step("tile", index, k))
+            cands.append(steps)
+    elif name == "c3":
+        ref = [Step("softmax", ref_s, 0, dict(sigma=2.0))]
+        for k in range(K):
+            s = f32(10.0 ** (-9.0 + 6.0 * k / max(1, K - 1)))
+            cands.append([Step("perturb", noise, k, dict(op=ADD_NORMAL, a=s, b=0.0, p=0.0))])
+    elif name == "c4":
+        ref = [Step("gen", ref_s, 0, dict(dist=DIST_NORMAL, p0=0.0, p1=1.0))]
+        for k in range(K):
+            kind, steps = k % 4, []
+            if kind in (1, 3):
+                steps.append(Step("perturb", mask, k, dict(op=FLIP_LSB_WHERE, a=0.0, b=0.0, p=f32(0.001))))
+            if kind in (2, 3):
+                steps.append(Step("scatter", index, k, dict(m=min(64, n // 2), mode=SCATTER_INF_SIGN_OF_REF)))
+            cands.append(steps)
+    elif name == "c5":
+        ref = [Step("gen", ref_s, 0, dict(dist=DIST_STUDENT_T3, p0=0.0, p1=1.0)),
+               Step("perturb", mask, 0, dict(op=SPECIALS, a=SUBNORMAL_P, b=ZERO_P, p=INF_P))]
+        for k in range(K):
+            cands.append([Step("perturb", noise, k, dict(op=ZERO_SUBNORMAL_REL, a=f32(-1e-7), b=f32(1e-7),
+                                                         p=0.5))])
+    else:
+        raise KeyError(name)
+    return Recipe(name, shape, spec["dtype"], spec["atol"], spec["rtol"], seed, ref, cands)
+
+
+# ------------------------------------------------------------ on the GPU ---
 
 @dataclass
 class Workload:
     name: str
-    ref: torch.Tensor
-    cands: List[torch.Tensor]
+    ref: "object"
+    cands: list
     atol: float
     rtol: float
     meta: dict = field(default_factory=dict)
@@ -66,156 +196,57 @@ class Workload:
         return len(self.cands) * self.numel * self.dtype_bytes
 
 
-def _gen(device, seed, cfg, purpose, k=0, chunk=0):
-    g = torch.Generator(device=device)
-    g.manual_seed(seed * 1_000_003 + (cfg << 40) + (purpose << 32) + (k << 12) + chunk)
-    return g
+def _tile_of(kb, rows, cols, seed, stream_id, sub, device):
+    import torch
+    w = torch.empty(4, dtype=torch.int32, device=device)
+    kb.kb_gen_inputs(w, kb.KB_DIST_U32, seed=seed, stream_id=stream_id, sub=sub)
+    w0, w1 = (int(x) & 0xFFFFFFFF for x in w[:2].cpu().tolist())
+    return w0 % (rows // 64), w1 % (cols // 64)
 
 
-def scaled_shape(shape, scale):
-    if scale >= 1.0:
-        return tuple(shape)
-    n = max(1, int(round(math.prod(shape) * scale)))
-    return (n,)
+def _run_gpu(kb, steps, t, ref, rec, device, meta):
+    """Carry out `steps` on device tensor t (ref: the finished reference)."""
+    for st in steps:
+        a = st.args
+        if st.kind == "gen":
+            kb.kb_gen_inputs(t, a["dist"], a["p0"], a["p1"], seed=rec.seed, stream_id=st.stream_id, sub=st.sub)
+        elif st.kind == "softmax":
+            kb.kb_gen_softmax_rows(t.view(rec.shape[0], -1), a["sigma"], seed=rec.seed, stream_id=st.stream_id,
+                                   sub=st.sub)
+        elif st.kind == "perturb":
+            kb.kb_gen_perturb(t, t, a["op"], a["a"], a["b"], a["p"], seed=rec.seed, stream_id=st.stream_id,
+                              sub=st.sub)
+        elif st.kind == "scatter":
+            idx = kb.kb_gen_indices(a["m"], t.numel(), device, seed=rec.seed, stream_id=st.stream_id, sub=st.sub)
+            kb.kb_gen_scatter(t, ref, idx, a["mode"])
+            meta.setdefault("indices", {})[st.sub] = idx.cpu().tolist()
+        elif st.kind == "tile":
+            rows, cols = rec.shape
+            tr, tc = _tile_of(kb, rows, cols, rec.seed, st.stream_id, st.sub, device)
+            t.view(rows, cols)[64 * tr:64 * tr + 64, 64 * tc:64 * tc + 64].zero_()
+            meta.setdefault("tiles", {})[st.sub] = (tr, tc)
+        else:
+            raise ValueError(st.kind)
 
 
-def _distinct(g, n, m, device):
-    """m distinct indices in [0, n)."""
-    m = min(m, n)
-    if n <= (1 << 24):
-        return torch.randperm(n, generator=g, device=device)[:m]
-    picked = torch.unique(torch.randint(0, n, (2 * m + 16,), generator=g, device=device))
-    return picked[torch.randperm(picked.numel(), generator=g, device=device)[:m]]
+def build(name, device="cuda:0", seed=0, scale=1.0, K=None):
+    """Workload `name` built on `device` by the library's generator calls."""
+    import torch
 
-
-# ------------------------------------------------------------------- c1 ---
-
-def _c1(device, seed, shape):
-    n = math.prod(shape)
-    ref = torch.randn(shape, generator=_gen(device, seed, 1, REF), device=device)
-    c0 = ref.clone()
-    noise = torch.rand(shape, generator=_gen(device, seed, 1, NOISE, 1), device=device)
-    c1 = ref + (noise * 2e-6 - 1e-6)
-    c2 = ref.clone()
-    idx = _distinct(_gen(device, seed, 1, INDEX, 2), n, 5, device)
-    c2.view(-1)[idx] = float("nan")
-    mask = torch.rand(shape, generator=_gen(device, seed, 1, MASK, 3), device=device) < 0.01
-    c3 = torch.where(mask, ref * 1.01, ref)
-    return ref, [c0, c1, c2, c3], {"nan_index": idx.cpu().tolist()}
-
-
-# ------------------------------------------------------------------- c2 ---
-
-def _c2(device, seed, shape, K=16):
-    z = torch.randn(shape, generator=_gen(device, seed, 2, REF), device=device)
-    ref = (z * 64.0).to(torch.bfloat16)
-    r32 = ref.float()
-    cands, tiles = [], []
-    for k in range(K):
-        sigma = 2.0 ** (-8.0 + 2.0 * k / 15.0)
-        u = torch.rand(shape, generator=_gen(device, seed, 2, NOISE, k), device=device)
-        eps = (u * 2.0 - 1.0) * sigma
-        c = (r32 + r32 * eps).to(torch.bfloat16)
-        if k < 2 and len(shape) == 2 and shape[0] >= 64 and shape[1] >= 64:
-            g = _gen(device, seed, 2, INDEX, k)
-            tr = int(torch.randint(0, shape[0] // 64, (1,), generator=g, device=device))
-            tc = int(torch.randint(0, shape[1] // 64, (1,), generator=g, device=device))
-            c[64 * tr:64 * tr + 64, 64 * tc:64 * tc + 64] = 0
-            tiles.append((tr, tc))
-        cands.append(c)
-    return ref, cands, {"tiles": tiles}
-
-
-# ------------------------------------------------------------------- c3 ---
-
-def _c3(device, seed, shape, K=1024):
-    logits = torch.randn(shape, generator=_gen(device, seed, 3, REF), device=device) * 2.0
-    ref = torch.softmax(logits.double(), dim=-1).float()
-    cands = []
-    for k in range(K):
-        sigma = 10.0 ** (-9.0 + 6.0 * k / max(1, K - 1))
-        z = torch.randn(shape, generator=_gen(device, seed, 3, NOISE, k), device=device)
-        cands.append(ref + z * sigma)
-    return ref, cands, {}
-
-
-# ------------------------------------------------------------------- c4 ---
-
-def _c4(device, seed, shape, K=64):
-    n = math.prod(shape)
-    ref = torch.randn(shape, generator=_gen(device, seed, 4, REF), device=device).half()
-    bits = ref.view(torch.int16)
-    n_inf = min(64, n)
-    cands = []
-    for k in range(K):
-        kind = k % 4
-        c = ref.clone()
-        if kind in (1, 3):
-            flip = torch.rand(shape, generator=_gen(device, seed, 4, MASK, k), device=device) < 0.001
-            cb = c.view(torch.int16)
-            cb.copy_(torch.where(flip, bits ^ 1, bits))
-        if kind in (2, 3):
-            idx = _distinct(_gen(device, seed, 4, INDEX, k), n, n_inf, device)
-            flat = c.view(-1)
-            flat[idx] = torch.copysign(torch.full_like(flat[idx], float("inf")), ref.view(-1)[idx])
-        cands.append(c)
-    return ref, cands, {}
-
-
-# ------------------------------------------------------------------- c5 ---
-
-SUBNORMAL_P = 2.0 ** -10
-ZERO_P = 2.0 ** -9
-INF_P = 2.0 ** -9 + 2.0 ** -20
-
-
-def _c5_ref_chunk(device, seed, lo, hi, ci):
-    n = hi - lo
-    g = _gen(device, seed, 5, REF, 0, ci)
-    z = torch.randn((4, n), generator=g, device=device)
-    t = z[0] / torch.sqrt((z[1] * z[1] + z[2] * z[2] + z[3] * z[3]) / 3.0)
-    gm = _gen(device, seed, 5, MASK, 0, ci)
-    u = torch.rand(n, generator=gm, device=device)
-    sign = torch.where(torch.rand(n, generator=gm, device=device) < 0.5, -1.0, 1.0)
-    mant = torch.randint(0, 1 << 23, (n,), generator=gm, device=device, dtype=torch.int32) | 1
-    sub = mant.view(torch.float32) * sign  # bit pattern mant with exponent 0: a subnormal
-    t = torch.where(u < SUBNORMAL_P, sub, t)
-    t = torch.where((u >= SUBNORMAL_P) & (u < ZERO_P), sign * 0.0, t)
-    t = torch.where((u >= ZERO_P) & (u < INF_P), sign * float("inf"), t)
-    return t
-
-
-def _c5_cand_chunk(device, seed, r, k, ci):
-    g = _gen(device, seed, 5, NOISE, k, ci)
-    v = torch.rand(r.numel(), generator=g, device=device)
-    delta = torch.rand(r.numel(), generator=g, device=device) * 2e-7 - 1e-7
-    hit = v < 0.5
-    a = r.abs()
-    is_zero = a == 0
-    is_sub = (a > 0) & (a < 2.0 ** -126)
-    is_inf = torch.isinf(r)
-    normal = ~(is_zero | is_sub | is_inf)
-    c = r.clone()
-    c = torch.where(hit & is_zero, -r, c)                      # sign-of-zero flip
-    c = torch.where(hit & is_sub, r * 0.0, c)                   # flush, keeps the sign
-    c = torch.where(hit & normal, r + r * delta, c)             # 1e-7-relative perturbation
-    return c
-
-
-def _c5(device, seed, shape, K=8):
-    n = math.prod(shape)
-    ref = torch.empty(n, dtype=torch.float32, device=device)
-    cands = [torch.empty(n, dtype=torch.float32, device=device) for _ in range(K)]
-    for ci, lo in enumerate(range(0, n, CHUNK)):
-        hi = min(n, lo + CHUNK)
-        r = _c5_ref_chunk(device, seed, lo, hi, ci)
-        ref[lo:hi] = r
-        for k in range(K):
-            cands[k][lo:hi] = _c5_cand_chunk(device, seed, r, k, ci)
-    return ref.view(shape), [c.view(shape) for c in cands], {}
-
-
-BUILDERS = {"c1": _c1, "c2": _c2, "c3": _c3, "c4": _c4, "c5": _c5}
+    import paper_2608_02611_amd as kb
+    rec = recipe(name, seed=seed, scale=scale, K=K)
+    dt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[rec.dtype]
+    device = torch.device(device)
+    meta = {}
+    with torch.no_grad():
+        ref = torch.empty(rec.shape, dtype=dt, device=device)
+        _run_gpu(kb, rec.ref, ref.view(-1), ref.view(-1), rec, device, meta)
+        cands = []
+        for steps in rec.cands:
+            c = ref.clone()
+            _run_gpu(kb, steps, c.view(-1), ref.view(-1), rec, device, meta)
+            cands.append(c)
+    return Workload(name, ref, cands, rec.atol, rec.rtol, meta)
 
 
 # ------------------------------------------------------------ timing samples
@@ -236,6 +267,7 @@ def timing_samples(n_cands, n_shapes, n_iter, seed=0, device="cpu", shape_us=Non
         3%, a spike of 2-25% (tail ratios p99/p50 of about 1.01-1.25, the
         range of Table A.3).
     """
+    import torch
     g = torch.Generator(device="cpu").manual_seed(0x5EED0000 + seed)
     if shape_us is None:
         shape_us = [50.0 * (2 ** s) for s in range(n_shapes)]
@@ -248,18 +280,3 @@ def timing_samples(n_cands, n_shapes, n_iter, seed=0, device="cpu", shape_us=Non
     spike_amt = 0.02 + 0.23 * torch.rand(n_cands, n_shapes, n_iter, generator=g, dtype=torch.float64)
     t = mean * (1.0 + jitter + spike.double() * spike_amt)
     return t.to(device)
-
-
-def build(name, device="cpu", seed=0, scale=1.0, K=None):
-    """Workload `name` on `device`; scale < 1 shrinks N (and K=None keeps K)."""
-    spec = SPECS[name]
-    shape = spec["shape"] if scale >= 1.0 else scaled_shape(spec["shape"], scale)
-    if name == "c2" and scale < 1.0:
-        side = max(64, int(round(math.sqrt(math.prod(spec["shape"]) * scale))) // 64 * 64)
-        shape = (side, side)
-    kwargs = {}
-    if K is not None and name != "c1":
-        kwargs["K"] = K
-    with torch.no_grad():
-        ref, cands, meta = BUILDERS[name](torch.device(device), seed, shape, **kwargs)
-    return Workload(name, ref, cands, spec["atol"], spec["rtol"], meta)

@@ -15,6 +15,28 @@ SUM_RTOL = 1e-6  # relative tolerance of the binary64 sums and the relative L2 e
 THREADS = min(16, os.cpu_count() or 1)
 
 
+def to_device(arr, dt, dev):
+    """numpy storage (float32, or uint16 bits for f16/bf16) -> device tensor of dtype dt."""
+    import torch
+    if dt == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(dev)
+    bits = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint16).view(np.int16)).to(dev)
+    return bits.view({"f16": torch.float16, "bf16": torch.bfloat16}[dt])
+
+
+def oracle_workload(name, dev, seed=0, scale=1.0, K=None):
+    """Workload `name` built by the oracle on the host (oracle.workloads) and
+    copied to device `dev`: the inputs of the screening parity tests, none of
+    whose bytes come from the HIP path.  Returns (synth.Workload of device
+    tensors, the oracle's host workload)."""
+    import synth
+    from oracle import workloads
+    ow = workloads.build(name, seed=seed, scale=scale, K=K)
+    ref = to_device(ow.ref, ow.dtype, dev).view(ow.shape)
+    cands = [to_device(c, ow.dtype, dev).view(ow.shape) for c in ow.cands]
+    return synth.Workload(name, ref, cands, ow.atol, ow.rtol, dict(ow.meta)), ow
+
+
 def ensure_built():
     import __graft_entry__
     __graft_entry__._ensure_built()
@@ -34,21 +56,27 @@ def storage(t):
     return t.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def oracle_records(ref, cands, atol, rtol, flags=0, chunk=1 << 24):
+def oracle_records(ref, cands, atol, rtol, flags=0, chunk=1 << 24, dt=None):
     """Oracle statistics of every candidate (chunked over elements and run on
-    host threads for large tensors; merged in chunk order)."""
-    dt = dtype_name(ref)
-    n = ref.numel()
+    host threads for large tensors; merged in chunk order).  ref and cands
+    are device tensors, or host storage arrays with their dtype name dt."""
+    host = isinstance(ref, np.ndarray)
+    if host:
+        n = ref.size
+        get = lambda t, lo, hi: t.reshape(-1)[lo:hi]
+    else:
+        dt = dtype_name(ref)
+        n = ref.numel()
+        get = lambda t, lo, hi: storage(t.reshape(-1)[lo:hi])
     if n <= chunk:
-        r = storage(ref)
-        return [oracle.screen(r, storage(c), dt, atol, rtol, flags) for c in cands]
+        r = get(ref, 0, n)
+        return [oracle.screen(r, get(c, 0, n), dt, atol, rtol, flags) for c in cands]
     bounds = [(lo, min(n, lo + chunk)) for lo in range(0, n, chunk)]
     partials = [[None] * len(bounds) for _ in cands]
-    rflat = ref.reshape(-1)
     with ThreadPoolExecutor(THREADS) as ex:
         for bi, (lo, hi) in enumerate(bounds):
-            r = storage(rflat[lo:hi])
-            cs = [storage(c.reshape(-1)[lo:hi]) for c in cands]
+            r = get(ref, lo, hi)
+            cs = [get(c, lo, hi) for c in cands]
             futs = [ex.submit(oracle.screen_partial, r, cs[k], dt, atol, rtol, flags)
                     for k in range(len(cands))]
             for k, f in enumerate(futs):

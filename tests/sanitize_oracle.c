@@ -163,8 +163,48 @@ static int rung_cases(void) {
     return 0;
 }
 
+/* The derived inputs: Student-t, softmax rows, index draws, planted changes
+ * on every dtype (in place and not), scatters with out-of-range indices. */
+static int derived_cases(void) {
+    uint32_t w[4] = {0u, 0u, 0xFFFFFFFFu, 0u}; /* a zero chi-square: z0 / 0 */
+    (void)kbo_student_t3(w);
+    for (uint64_t n = 0; n < 40; n += 13) {
+        float* t = exact_alloc(n * 4);
+        CHECK(kbo_gen(t, KBO_F32, n, KBO_DIST_STUDENT_T3, 0.0f, 1.0f, 1, 2, 3, 1ull << 40) == 0);
+        free(t);
+    }
+    for (uint64_t cols = 1; cols < 70; cols += 17) {
+        float* sm = exact_alloc(3 * cols * 4);
+        CHECK(kbo_gen_softmax_rows(sm, 5, 3, cols, 2.0f, 0, 3, 0) == 0);
+        free(sm);
+    }
+    CHECK(kbo_gen_softmax_rows(NULL, 0, 1, 0, 2.0f, 0, 3, 0) == -1);
+    uint64_t* idx = exact_alloc(7 * 8);
+    CHECK(kbo_gen_indices(idx, 7, 7, 0, 9, 1) == 0);
+    CHECK(kbo_gen_indices(idx, 7, 6, 0, 9, 1) == -1);
+    for (int dtype = 0; dtype < 3; ++dtype) {
+        const uint64_t n = 1029;
+        void* src = random_tensor(dtype, n);
+        void* dst = exact_alloc(n * (dtype == KBO_F32 ? 4 : 2));
+        for (int op = 1; op <= 7; ++op) {
+            const int want = (op >= 6 && dtype != KBO_F32) ? -1 : 0;
+            CHECK(kbo_perturb(dst, src, dtype, n, op, -0.5f, 0.5f, 0.5f, 0, 4, op, 3) == want);
+            CHECK(kbo_perturb(src, src, dtype, n, op, 0.25f, 0.5f, 0.75f, 0, 4, op, 0) == want);
+        }
+        CHECK(kbo_perturb(dst, src, dtype, n, 8, 0.0f, 0.0f, 0.0f, 0, 0, 0, 0) == -1);
+        const uint64_t sidx[3] = {0, n - 1, n};
+        CHECK(kbo_scatter(dst, src, dtype, n, sidx, 3, KBO_SCATTER_NAN) == 0);
+        CHECK(kbo_scatter(dst, src, dtype, n, sidx, 3, KBO_SCATTER_INF_SIGN_OF_REF) == 0);
+        CHECK(kbo_scatter(dst, src, dtype, n, sidx, 3, 3) == -1);
+        free(src);
+        free(dst);
+    }
+    free(idx);
+    return 0;
+}
+
 int main(void) {
-    if (screen_cases() || map_cases() || rung_cases()) return 1;
+    if (screen_cases() || map_cases() || rung_cases() || derived_cases()) return 1;
     printf("ok\n");
     return 0;
 }

@@ -188,6 +188,46 @@ def test_noalloc_argument_errors(L):
                                            for dt in (kb.KB_F32, kb.KB_F16, kb.KB_BF16))
 
 
+def test_derived_generator_argument_errors(L):
+    """The derived-input calls refuse bad arguments before any device work."""
+    sm, ix, pt, sc = (kb.lib().kb_gen_softmax_rows, kb.lib().kb_gen_indices, kb.lib().kb_gen_perturb,
+                      kb.lib().kb_gen_scatter)
+    assert sm(0x1000, kb.KB_F16, 4, 4, 2.0, 0, 0, 0, None) == kb.KB_ERR_DTYPE
+    assert sm(0x1000, kb.KB_F32, 4, 0, 2.0, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert sm(0x1000, kb.KB_F32, 4, 4, float("inf"), 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert sm(0x1008, kb.KB_F32, 4, 4, 2.0, 0, 0, 0, None) == kb.KB_ERR_ALIGNMENT
+    assert sm(None, kb.KB_F32, 0, 4, 2.0, 0, 0, 0, None) == kb.KB_OK  # no rows: nothing to do
+    assert ix(0x1000, 0, 100, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert ix(0x1000, 6, 11, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG  # 2 m > n
+    assert ix(0x1000, kb.KB_MAX_INDICES + 1, 1 << 40, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert ix(None, 5, 100, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+    assert ix(0x1008, 5, 100, 0, 0, 0, None) == kb.KB_ERR_ALIGNMENT
+    ok = (0x1000, 0x2000, kb.KB_F32, 16, kb.KB_PERTURB_ADD_UNIFORM, 0.0, 1.0, 0.5, 0, 0, 0, 0, None)
+
+    def perturb(**kw):
+        a = list(ok)
+        for i, k in enumerate(("dst", "src", "dtype", "n", "op", "a", "b", "p")):
+            if k in kw:
+                a[i] = kw[k]
+        return pt(*a)
+
+    assert perturb(op=0) == kb.KB_ERR_INVALID_ARG and perturb(op=8) == kb.KB_ERR_INVALID_ARG
+    assert perturb(dtype=kb.KB_U32) == kb.KB_ERR_DTYPE
+    assert perturb(dtype=kb.KB_F16, op=kb.KB_PERTURB_SPECIALS) == kb.KB_ERR_DTYPE
+    assert perturb(p=float("nan")) == kb.KB_ERR_INVALID_ARG
+    assert perturb(src=None) == kb.KB_ERR_INVALID_ARG
+    assert perturb(dst=0x1004) == kb.KB_ERR_ALIGNMENT
+    assert perturb(dst=None, src=None, n=0) == kb.KB_OK
+    assert pt(0x1000, 0x2000, kb.KB_F32, 16, 1, 0.0, 1.0, 0.0, 0, 0, 0, 2 ** 64 - 8, None) == kb.KB_ERR_INVALID_ARG
+    assert sc(0x1000, 0x2000, kb.KB_F32, 16, 0x3000, 4, 3, None) == kb.KB_ERR_INVALID_ARG
+    assert sc(0x1000, 0x2000, kb.KB_U32, 16, 0x3000, 4, 1, None) == kb.KB_ERR_DTYPE
+    assert sc(0x1000, None, kb.KB_F32, 16, 0x3000, 4, 1, None) == kb.KB_ERR_INVALID_ARG
+    assert sc(0x1000, 0x2000, kb.KB_F32, 16, 0x3004, 4, 1, None) == kb.KB_ERR_ALIGNMENT
+    g = kb.lib().kb_gen_inputs
+    assert g(0x1000, kb.KB_U32, 16, kb.KB_DIST_STUDENT_T3, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_DTYPE
+    assert g(0x1000, kb.KB_F32, 16, 4, 0.0, 1.0, 0, 0, 0, 0, None) == kb.KB_ERR_INVALID_ARG
+
+
 def test_stats_argument_errors(L):
     assert kb.lib().kb_screen_stats(None, 4, None, None, None, None) == kb.KB_ERR_INVALID_ARG
     assert kb.lib().kb_screen_stats(0x1000, -1, None, None, None, None) == kb.KB_ERR_INVALID_ARG

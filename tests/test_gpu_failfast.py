@@ -25,7 +25,7 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 from tests.helpers import (EXACT_FIELDS, SUM_FIELDS, SUM_RTOL, assert_records_match, close,
-                           ensure_built, oracle_records, storage)
+                           ensure_built, oracle_records, oracle_workload, storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -251,8 +251,7 @@ def test_one_group_many_super_groups(dev, dt):
 def test_workload_c2_full_size(dev):
     """The fail-fast screen bench.py times: the 16-candidate 4096 x 4096
     bf16 workload at its full size."""
-    import synth
-    w = synth.build("c2", dev, seed=0)
+    w, _ = oracle_workload("c2", dev, seed=0)
     torch.cuda.synchronize()
     say("fail-fast c2 full size")
     full, fsum = kb.screen(w.ref, w.cands, w.atol, w.rtol, 0)

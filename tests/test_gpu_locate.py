@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import dtype_name, ensure_built, storage
+from tests.helpers import dtype_name, ensure_built, oracle_workload, storage
 
 pytestmark = pytest.mark.gpu
 
@@ -98,7 +98,7 @@ def test_random_ragged(dev, dt):
 @pytest.mark.parametrize("name,scale,K", [("c1", 1.0, 4), ("c2", 1 / 64, 16), ("c3", 1 / 8, 64),
                                           ("c4", 1 / 256, 16), ("c5", 1 / 512, 8)])
 def test_workloads(dev, name, scale, K):
-    w = synth.build(name, dev, seed=0, scale=scale, K=K)
+    w, _ = oracle_workload(name, dev, seed=0, scale=scale, K=K)
     check(w.ref, w.cands, w.atol, w.rtol, 0, name)
 
 
@@ -156,7 +156,7 @@ def test_non_finite_references(dev, dt):
 def test_workload_c2_full_size(dev):
     """The 16-candidate 4096 x 4096 bf16 workload at its full size, the
     position search bench.py times."""
-    w = synth.build("c2", dev, seed=0)
+    w, _ = oracle_workload("c2", dev, seed=0)
     torch.cuda.synchronize()
     locs = check(w.ref, w.cands, w.atol, w.rtol, 0, "c2 full")
     assert sum(l["first_mismatch"] >= 0 for l in locs) > 0 and all(l["max_abs_index"] >= 0 for l in locs)

@@ -16,7 +16,8 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import THREADS, assert_records_match, ensure_built, oracle_records, storage
+from tests.helpers import (THREADS, assert_records_match, ensure_built, oracle_records, oracle_workload,
+                           storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -264,21 +265,23 @@ def test_one_group_many_super_groups(dev, dt):
 @pytest.mark.parametrize("name,scale,K", SCALED)
 def test_workloads_scaled(dev, name, scale, K):
     say("workload", name, "scale", scale)
-    w = synth.build(name, dev, seed=0, scale=scale, K=K)
+    w, _ = oracle_workload(name, dev, seed=0, scale=scale, K=K)
     run_case(w.ref, w.cands, w.atol, w.rtol, 0, name)
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
 def test_workloads_full_size(dev, name):
-    # the exact sizes and launch configuration the benchmark times
-    say("full-size workload", name, kb.kb_screen_launch(synth.SPECS[name]["K"],
-                                                       math.prod(synth.SPECS[name]["shape"]),
-                                                       {torch.float32: 0, torch.float16: 1,
-                                                        torch.bfloat16: 2}[synth.SPECS[name]["dtype"]]))
-    w = synth.build(name, dev, seed=0)
+    """The exact sizes and launch configuration the benchmark times, on the
+    workload the oracle built (the oracle screens its own host arrays)."""
+    spec = synth.SPECS[name]
+    code = {"f32": kb.KB_F32, "f16": kb.KB_F16, "bf16": kb.KB_BF16}[spec["dtype"]]
+    say("full-size workload", name, kb.kb_screen_launch(spec["K"], math.prod(spec["shape"]), code))
+    w, ow = oracle_workload(name, dev, seed=0)
     torch.cuda.synchronize()
-    run_case(w.ref, w.cands, w.atol, w.rtol, 0, name + " full")
-    del w
+    recs, _ = kb.screen(w.ref, w.cands, w.atol, w.rtol)
+    orc = oracle_records(ow.ref, ow.cands, ow.atol, ow.rtol, dt=ow.dtype)
+    assert_records_match(recs, orc, name + " full")
+    del w, ow
     torch.cuda.empty_cache()
 
 
@@ -323,7 +326,7 @@ def test_all_rejected_and_empty(dev):
 
 def test_determinism_and_workspace_reuse(dev):
     say("determinism")
-    w = synth.build("c2", dev, seed=1, scale=1 / 16)
+    w, _ = oracle_workload("c2", dev, seed=1, scale=1 / 16)
     K = len(w.cands)
     ws = kb.alloc_workspace(K, w.numel, kb.KB_BF16, dev)
     st = kb.alloc_stats(K, dev)
@@ -350,8 +353,8 @@ def test_dirty_workspace_is_reported(dev, flags):
     Every call's readback must either be the oracle's records or raise
     KB_ERR_WORKSPACE -- never wrong records -- and the garbage fills must be
     caught.  After kb_screen_workspace_init every call is exact again."""
-    big = synth.build("c4", dev, seed=2, scale=1 / 256, K=40)
-    small = synth.build("c1", dev, seed=2)
+    big, _ = oracle_workload("c4", dev, seed=2, scale=1 / 256, K=40)
+    small, _ = oracle_workload("c1", dev, seed=2)
     plan = kb.kb_screen_launch(40, big.numel, kb.KB_F16)
     say("dirty workspace", flags, plan)
     assert plan["n_groups"] > 1 and plan["blocks_per_group"] > 16, plan  # two-level finish
@@ -395,7 +398,7 @@ def test_dirty_workspace_is_reported(dev, flags):
 
 def test_pinned_host_records_pipeline(dev):
     say("pinned host records")
-    w = synth.build("c2", dev, seed=4, scale=1 / 64)
+    w, _ = oracle_workload("c2", dev, seed=4, scale=1 / 64)
     scr = kb.Screener(w.ref, w.cands, w.atol, w.rtol, host_slots=2)
     ev = [torch.cuda.Event(), torch.cuda.Event()]
     seen = []
@@ -416,7 +419,7 @@ def test_pinned_host_records_pipeline(dev):
 def test_stream_ordering_with_side_stream(dev):
     say("side stream")
     s = torch.cuda.Stream()
-    w = synth.build("c1", dev, seed=3)
+    w, _ = oracle_workload("c1", dev, seed=3)
     with torch.cuda.stream(s):
         recs, _ = kb.screen(w.ref, w.cands, w.atol, w.rtol, stream=s)
     assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), "side stream")
@@ -427,7 +430,7 @@ def test_two_streams_concurrent_screens(dev):
     with its own workspace and ring of pinned record slots, overlapping on
     the device (the pipelined bench loop): every record is the oracle's."""
     say("two streams")
-    w = synth.build("c2", dev, seed=6, scale=1 / 16)
+    w, _ = oracle_workload("c2", dev, seed=6, scale=1 / 16)
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     scrs = [kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, host_slots=4) for st in streams]
     for i in range(16):

@@ -2,7 +2,7 @@
 
 tests/sanitize_oracle.c calls every oracle entry point (screening, merge,
 positions, the maps and the generator, the rung statistics and the
-promotion decision) on special values, empty and ragged sizes and random
+promotion decision, the derived inputs) on special values, empty and ragged sizes and random
 inputs, with every buffer allocated at its exact size; built here with both
 sanitizers and no recovery, any out-of-bounds access, use of freed memory,
 signed overflow or invalid shift ends the run with a report."""
@@ -19,7 +19,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_oracle_clean_under_asan_ubsan(tmp_path):
     exe = str(tmp_path / "sanitize_oracle")
     srcs = [os.path.join(ROOT, "tests", "sanitize_oracle.c"), os.path.join(ROOT, "oracle", "kbo.c"),
-            os.path.join(ROOT, "oracle", "kbo_rung.c")]
+            os.path.join(ROOT, "oracle", "kbo_rung.c"), os.path.join(ROOT, "oracle", "kbo_derived.c")]
     cmd = ["gcc", "-std=c11", "-O1", "-g", "-ffp-contract=off", "-fno-omit-frame-pointer",
            "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "oracle"),
            *srcs, "-o", exe, "-lm"]
