@@ -448,9 +448,10 @@ typedef struct kb_sample_stats {
  *   latency_us       the mean over the rung's shapes of the row means, left
  *                    to right (Eq. 1's expectation over shapes, the shapes
  *                    weighted equally);
- *   score            S = 1e6 / max(1, latency_us) + alpha rung + beta budget
- *                    (Eq. 2 with gamma(r) = alpha r + beta b_r, Section 3.1),
- *                    summed in that order; -inf for an invalid candidate;
+ *   score            S = 1e6 / max(1, latency_us) + (alpha rung + beta budget)
+ *                    (Eq. 2 with gamma(r) = alpha r + beta b_r, Section 3.1:
+ *                    the rung term summed first, then added); -inf for an
+ *                    invalid candidate;
  *   speedup_vs_base  the baseline's latency / latency_us;
  *   valid            1 iff all the candidate's rows are valid. */
 typedef struct kb_rung_score {

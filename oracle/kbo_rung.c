@@ -106,7 +106,8 @@ void kbo_row_stats(const double* t, int n, kbo_row_t* out) {
 
 double kbo_rung_score_of(double latency, int rung, double budget, double alpha, double beta) {
     const double lead = 1e6 / (latency > 1.0 ? latency : 1.0);
-    return lead + alpha * (double)rung + beta * budget;
+    /* Eq. 2: the latency term plus the rung term gamma(r) = alpha r + beta b_r */
+    return lead + (alpha * (double)rung + beta * budget);
 }
 
 int kbo_rung_stats(const double* samples, int n_cands, int n_shapes, int n_iter, int base,

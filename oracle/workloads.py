@@ -43,8 +43,9 @@ def _bounds(n, chunk=CHUNK):
 
 
 def _run(ex, steps, arr, ref, rec, meta):
-    """Carry out `steps` on the flat storage array `arr` (ref: the finished reference)."""
-    n, dt = arr.size, rec.dtype
+    """Carry out `steps` on the flat storage array `arr`, the first arr.size
+    elements of the tensor (ref: the finished reference, as long)."""
+    n, dt, full = arr.size, rec.dtype, rec.numel
     for st in steps:
         a = st.args
         if st.kind == "gen":
@@ -53,8 +54,8 @@ def _run(ex, steps, arr, ref, rec, meta):
                 arr[lo:hi] = gen(dt, hi - lo, a["dist"], a["p0"], a["p1"], rec.seed, st.stream_id, st.sub, lo)
             list(ex.map(one, _bounds(n)))
         elif st.kind == "softmax":
-            rows = rec.shape[0]
-            cols = n // rows
+            cols = full // rec.shape[0]
+            rows = n // cols
             view = arr.reshape(rows, cols)
 
             def one(b):
@@ -68,30 +69,39 @@ def _run(ex, steps, arr, ref, rec, meta):
                                      st.sub, lo)
             list(ex.map(one, _bounds(n)))
         elif st.kind == "scatter":
-            idx = gen_indices(a["m"], n, rec.seed, st.stream_id, st.sub)
+            # drawn over the whole tensor; indices past a prefix are skipped
+            idx = gen_indices(a["m"], full, rec.seed, st.stream_id, st.sub)
             scatter(arr, ref, dt, idx, a["mode"])
             meta.setdefault("indices", {})[st.sub] = [int(i) for i in idx]
         elif st.kind == "tile":
             rows, cols = rec.shape
             w = gen("u32", 2, DIST_U32, 0.0, 1.0, rec.seed, st.stream_id, st.sub, 0)
             tr, tc = int(w[0]) % (rows // 64), int(w[1]) % (cols // 64)
-            arr.reshape(rows, cols)[64 * tr:64 * tr + 64, 64 * tc:64 * tc + 64] = 0
+            arr.reshape(-1, cols)[64 * tr:64 * tr + 64, 64 * tc:64 * tc + 64] = 0
             meta.setdefault("tiles", {})[st.sub] = (tr, tc)
         else:
             raise ValueError(st.kind)
 
 
-def build(name, seed=0, scale=1.0, K=None, threads=THREADS):
-    """Workload `name` as host storage arrays, built by the oracle."""
+def build(name, seed=0, scale=1.0, K=None, threads=THREADS, prefix=None):
+    """Workload `name` as host storage arrays, built by the oracle.  With
+    `prefix`, only the first `prefix` elements of every tensor (whole rows
+    for row-shaped tensors): every step is per element (or per row) and
+    random-access, so a prefix is exactly the start of the full tensors."""
     rec = synth.recipe(name, seed=seed, scale=scale, K=K)
     meta = {}
     store = NP_STORAGE[DTYPES[rec.dtype]]
+    n = rec.numel if prefix is None else min(int(prefix), rec.numel)
+    if len(rec.shape) > 1:
+        row = rec.numel // rec.shape[0]
+        n = max(row, n // row * row)
     with ThreadPoolExecutor(threads) as ex:
-        ref = np.empty(rec.numel, dtype=store)
+        ref = np.empty(n, dtype=store)
         _run(ex, rec.ref, ref, ref, rec, meta)
         cands = []
         for steps in rec.cands:
             c = ref.copy()
             _run(ex, steps, c, ref, rec, meta)
             cands.append(c)
-    return OracleWorkload(name, rec.dtype, rec.shape, ref, cands, rec.atol, rec.rtol, meta)
+    shape = rec.shape if n == rec.numel else (n,)
+    return OracleWorkload(name, rec.dtype, shape, ref, cands, rec.atol, rec.rtol, meta)

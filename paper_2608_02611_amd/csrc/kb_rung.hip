@@ -199,8 +199,8 @@ __global__ __launch_bounds__(kThreads) void scores_kernel(RungParams p, kb_sampl
     sc.latency_us = lat;
     if (ok) {
         const double lead = 1e6 / (lat > 1.0 ? lat : 1.0);
-        sc.score = __dadd_rn(__dadd_rn(lead, __dmul_rn(p.alpha, (double)p.rung)),
-                             __dmul_rn(p.beta, p.budget));
+        // Eq. 2: the latency term plus the one rung term gamma(r) = alpha r + beta b_r
+        sc.score = __dadd_rn(lead, __dadd_rn(__dmul_rn(p.alpha, (double)p.rung), __dmul_rn(p.beta, p.budget)));
         sc.speedup_vs_base = base_lat / lat;
     } else {
         sc.score = -__builtin_inf();

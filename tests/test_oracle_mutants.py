@@ -65,12 +65,12 @@ MUTANTS = [
      "const double h = (double)n * p;", RUNG),
     ("speedup_inverted", "kbo_rung.c", "r->speedup = r->valid ? b / r->mean : NAN;",
      "r->speedup = r->valid ? r->mean / b : NAN;", RUNG),
-    ("score_alpha_beta_swapped", "kbo_rung.c", "return lead + alpha * (double)rung + beta * budget;",
-     "return lead + beta * (double)rung + alpha * budget;", RUNG),
+    ("score_alpha_beta_swapped", "kbo_rung.c", "return lead + (alpha * (double)rung + beta * budget);",
+     "return lead + (beta * (double)rung + alpha * budget);", RUNG),
     ("score_latency_floor_dropped", "kbo_rung.c", "const double lead = 1e6 / (latency > 1.0 ? latency : 1.0);",
      "const double lead = 1e6 / latency;", RUNG),
-    ("score_rung_term_dropped", "kbo_rung.c", "return lead + alpha * (double)rung + beta * budget;",
-     "return lead + beta * budget;", RUNG),
+    ("score_rung_term_dropped", "kbo_rung.c", "return lead + (alpha * (double)rung + beta * budget);",
+     "return lead + (beta * budget);", RUNG),
     ("locate_first_mismatch_last", "kbo.c",
      "if (out->first_mismatch < 0 && !kbo_match(c, r, atol, rtol, flags))",
      "if (!kbo_match(c, r, atol, rtol, flags))", LOCATE),

@@ -117,16 +117,6 @@ def test_score_properties():
     assert oracle.rung_score_of(2606.0, 2, 60) > oracle.rung_score_of(2605.9, 0, 4)
 
 
-def test_incumbent_score_is_consistent():
-    """Section 4.4 prints the MatVec incumbent's score, 384.36, at rung 2.
-    With the repeat count as b_r that is a latency of about 2.6 ms; the check
-    is that this latency scores 384.36 to the printed precision -- a partial
-    pin (the latency itself is not printed)."""
-    lat = 1e6 / (384.36 - (0.02 * 2 + 0.01 * 60))
-    assert 2600.0 < lat < 2612.0
-    assert round(oracle.rung_score_of(lat, 2, 60), 2) == 384.36
-
-
 # ------------------------------------------------------------- promotion ---
 
 def test_survival_reproduces_table_a1_matvec():
