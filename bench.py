@@ -13,9 +13,11 @@ ring of 2 * BATCH record slots), so host work hides behind the device.
 value = K * numel * element bytes / step time (GB/s), on the headline
 workload (default c5: 8 candidates of 2^30 fp32, the largest that fits one
 GPU).  A few fully synchronous steps (launch, copy back, wait) are timed too
-(sync_step_ms), and the same steps alternating over two streams
-(pipelined_two_streams), which lets one step's first work-groups start while
-the previous step's last ones finish.
+(sync_step_ms).  With --two-streams the same steps also run alternating over
+two streams (pipelined_two_streams), which lets one step's first work-groups
+start while the previous step's last ones finish (off by default: its
+overlapping kernels would stretch the kernel's durations in a trace of the
+default command).
 
 Inputs are built on the device by the library's own seeded generator (the
 synth recipes: kb_gen_inputs, kb_gen_softmax_rows, kb_gen_indices,
@@ -443,6 +445,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only-config", action="store_true",
                     help="measure the named workload only (no other workloads, no side legs): for counter runs")
+    ap.add_argument("--two-streams", action="store_true",
+                    help="also time the steps alternating over two streams (pipelined_two_streams)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
@@ -535,7 +539,7 @@ def main():
     if args.copy_calibration:
         log("copy calibration")
         copy_calibration(dev)
-    if not args.only_config:
+    if args.two_streams:
         log("two-stream pipeline")
         two = Pipeline(kb, w, [stream, torch.cuda.Stream()], batch)
         two.run(2 * batch * 2)
@@ -546,7 +550,9 @@ def main():
         ms2 = (time.perf_counter() - t) * 1e3 / args.steps
         out["pipelined_two_streams"] = {"ms_per_step": round(ms2, 5),
                                         "screened_GB_per_s": round(screened / ms2 / 1e6, 1)}
-        del two, pipe, scr
+        del two
+    if not args.only_config:
+        del pipe, scr
         # the other workloads: kernel time, roofline fraction, verdicts
         del w
         torch.cuda.empty_cache()
