@@ -47,9 +47,11 @@ recipe; timed on one core, and on all the host cores the process may use
 (threads over (candidate, 2^22-element chunk), merged in chunk order).  The
 host's core count, CPU model and memory are reported beside it.
 
-Other legs (skipped with --only-config): the position search
-(kb_screen_locate) and the fail-fast screen (KB_FAIL_FAST) on the 16-candidate
-bf16 workload (which has failing candidates), a multi-output screen, the rung
+Other legs (skipped with --only-config): the position search -- found in the
+screening pass (kb_screen_ex with positions) and as a separate pass
+(kb_screen_locate) -- and the fail-fast screen (KB_FAIL_FAST) on the
+16-candidate bf16 workload (which has failing candidates), a multi-output
+screen, the rung
 statistics and promotion decision, the generator's throughput, and plain
 copy/reduction rates of the box for context.
 """
@@ -399,12 +401,44 @@ def rung_stats_leg(dev, kb, synth, C=1024, S=3, N=60):
             "promoted": int(prom.sum().item())}
 
 
+def positions_leg(kb, w, reps=20):
+    """The screen with positions found in the same pass (kb_screen_ex with
+    opts.d_loc) against the plain screen, back to back on one stream: kernel
+    time per launch of each, and the positions, which must equal those of
+    the separate pass (kb_screen_locate)."""
+    import torch
+    st = torch.cuda.Stream()
+    plain = kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st)
+    withpos = kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, positions=True)
+    warm_device(plain.launch, 0.1)
+    plain_ms = event_time(plain.launch, reps, st)
+    warm_device(withpos.launch, 0.1)
+    pos_ms = event_time(withpos.launch, reps, st)
+    plain.read()
+    withpos.read()
+    precs, wrecs = plain.records(), withpos.records()
+    assert [r["passed"] for r in precs] == [r["passed"] for r in wrecs], "verdicts differ with positions"
+    got = withpos.positions()
+    loc = kb.Locator(w.ref, w.cands, w.atol, w.rtol, plain.d_stats, stream=st)
+    loc.launch()
+    want = loc.read()
+    assert got == want, "positions of the screening pass differ from the separate pass"
+    K, n, b = len(w.cands), w.numel, w.dtype_bytes
+    alg = (K + 1) * n * b
+    return {"plain_kernel_ms": round(plain_ms, 5), "with_positions_kernel_ms": round(pos_ms, 5),
+            "ratio": round(pos_ms / plain_ms, 3), "with_positions_frac": round(alg / pos_ms / 1e6 / HBM_PEAK_GBPS, 4),
+            "launch": withpos.launch_plan(), "positions_equal_separate_pass": True,
+            "failed_candidates_first_mismatch": [l["first_mismatch"] for l in got if l["first_mismatch"] >= 0][:4]}
+
+
 def failing_workload_legs(kb, w):
-    """The position search and the fail-fast screen on a workload with
-    failing candidates (the 16-candidate bf16 one)."""
+    """The position search (in the screening pass, and as a separate pass)
+    and the fail-fast screen on a workload with failing candidates (the
+    16-candidate bf16 one)."""
     import torch
     K, n = len(w.cands), w.numel
     st = torch.cuda.current_stream()
+    fused = positions_leg(kb, w)
     full = kb.Screener(w.ref, w.cands, w.atol, w.rtol)
     full.launch()
     full.read()
@@ -425,6 +459,7 @@ def failing_workload_legs(kb, w):
     assert [r["passed"] for r in ffrec] == [r["passed"] for r in frec], "fail-fast verdicts differ"
     return {
         "workload": "c2: " + WORKLOADS["c2"], "screen_kernel_ms": round(full_ms, 5),
+        "screen_with_positions": fused,
         "locate": {"device_ms": round(loc_ms, 5), "vs_screen": round(loc_ms / full_ms, 3),
                    "failed_candidates_first_mismatch": [l["first_mismatch"] for l in locs
                                                         if l["first_mismatch"] >= 0][:4]},
@@ -447,6 +482,8 @@ def main():
                     help="measure the named workload only (no other workloads, no side legs): for counter runs")
     ap.add_argument("--two-streams", action="store_true",
                     help="also time the steps alternating over two streams (pipelined_two_streams)")
+    ap.add_argument("--positions", action="store_true",
+                    help="with --only-config: also time the screen with positions on the named workload")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run 3 plain 1 GiB device copies (for counter calibration)")
     args = ap.parse_args()
@@ -539,6 +576,9 @@ def main():
     if args.copy_calibration:
         log("copy calibration")
         copy_calibration(dev)
+    if args.positions and args.only_config:
+        log("screen with positions")
+        out["screen_with_positions"] = positions_leg(kb, w)
     if args.two_streams:
         log("two-stream pipeline")
         two = Pipeline(kb, w, [stream, torch.cuda.Stream()], batch)

@@ -220,6 +220,12 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
  * arguments (no device query). */
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype);
 
+/* Bytes of device workspace a kb_screen_ex call with positions (opts->d_loc)
+ * needs: kb_screen_workspace_bytes plus the per-work-group position partials
+ * (0 on invalid arguments).  Such a workspace serves calls with and without
+ * positions for the same sizes. */
+size_t kb_screen_positions_workspace_bytes(int n_cands, uint64_t numel, int dtype);
+
 /* Zero-fill a workspace (a fill kernel, stream-ordered; no memset node, so
  * it may be captured in a graph).  A workspace must be zero-filled this way
  * (or otherwise) once after it is allocated, and again before it is used for
@@ -290,6 +296,13 @@ typedef struct kb_screen_opts {
      * earlier, e.g. for the next call, races).  Ignored for smaller calls. */
     void* host_table;
     size_t host_table_bytes;
+    /* NULL, or n_cands kb_locate (device memory or mapped pinned host
+     * memory, 16-byte aligned): the positions that kb_screen_locate would
+     * find, found in the same pass over HBM as the records (the element-level
+     * detail of a failed candidate's feedback, Section 3.4).  Not with
+     * KB_FAIL_FAST.  Every position is the smallest qualifying element index,
+     * so the result does not depend on the launch. */
+    kb_locate* d_loc;
 } kb_screen_opts;
 
 /* Bytes of pinned host memory kb_screen_ex needs for n_cands candidates:
@@ -298,7 +311,10 @@ size_t kb_screen_host_table_bytes(int n_cands);
 
 /* kb_screen with options (opts may be NULL: then exactly kb_screen).
  * Errors as for kb_screen; KB_ERR_WORKSPACE also when a host table is needed
- * and missing or short, KB_ERR_ALIGNMENT when it is misaligned. */
+ * and missing or short, or when d_loc is given and the workspace is smaller
+ * than kb_screen_positions_workspace_bytes; KB_ERR_ALIGNMENT when the host
+ * table or d_loc is misaligned; KB_ERR_INVALID_ARG for d_loc with
+ * KB_FAIL_FAST. */
 int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol,
                  float rtol, uint32_t flags, void* workspace, size_t workspace_bytes,
                  kb_stats* d_stats, const kb_screen_opts* opts, hipStream_t stream);
@@ -397,8 +413,9 @@ size_t kb_screen_multi_host_table_bytes(int n_outputs, int n_cands);
  *   flags       as for kb_screen, applied to every output;
  *   d_stats     n_outputs * n_cands records, output-major: output o of
  *               candidate k at d_stats[o * n_cands + k];
- *   opts        as for kb_screen_ex (may be NULL); a host table must hold
- *               kb_screen_multi_host_table_bytes(n_outputs, n_cands).
+ *   opts        as for kb_screen_ex (may be NULL; d_loc must be NULL); a host
+ *               table must hold kb_screen_multi_host_table_bytes(n_outputs,
+ *               n_cands).
  * One gate over all outputs: candidate k is accepted only if every output
  * passes kb_policy_check against its reference; otherwise no output of it
  * is read and every one of its records has status = the first failing check

@@ -76,7 +76,8 @@ class KbSummary(ctypes.Structure):
 
 
 class KbScreenOpts(ctypes.Structure):
-    _fields_ = [("host_table", ctypes.c_void_p), ("host_table_bytes", ctypes.c_size_t)]
+    _fields_ = [("host_table", ctypes.c_void_p), ("host_table_bytes", ctypes.c_size_t),
+                ("d_loc", ctypes.c_void_p)]
 
 
 KB_INLINE_CANDS = 128
@@ -126,7 +127,8 @@ assert ctypes.sizeof(KbStats) == 80
 assert ctypes.sizeof(KbLocate) == 32
 assert ctypes.sizeof(KbTensor) == 144
 
-EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_workspace_init",
+EXPORTS = ("kb_policy_check", "kb_screen_workspace_bytes", "kb_screen_positions_workspace_bytes",
+           "kb_screen_workspace_init",
            "kb_screen_launch", "kb_screen", "kb_screen_ex", "kb_screen_host_table_bytes",
            "kb_screen_stats", "kb_summarize", "kb_gen_inputs",
            "kb_screen_locate", "kb_rung_stats", "kb_rung_promote", "kb_rung_survival", "kb_screen_multi",
@@ -151,6 +153,8 @@ def lib():
         L.kb_policy_check.restype = i32
         L.kb_screen_workspace_bytes.argtypes = [i32, u64, i32]
         L.kb_screen_workspace_bytes.restype = ctypes.c_size_t
+        L.kb_screen_positions_workspace_bytes.argtypes = [i32, u64, i32]
+        L.kb_screen_positions_workspace_bytes.restype = ctypes.c_size_t
         L.kb_screen_workspace_init.argtypes = [vp, ctypes.c_size_t, vp]
         L.kb_screen_workspace_init.restype = i32
         L.kb_summarize.argtypes = [ctypes.POINTER(KbStats), i32, ctypes.POINTER(KbSummary),
@@ -283,6 +287,10 @@ def kb_screen_workspace_bytes(n_cands, numel, dtype):
     return lib().kb_screen_workspace_bytes(n_cands, numel, dtype)
 
 
+def kb_screen_positions_workspace_bytes(n_cands, numel, dtype):
+    return lib().kb_screen_positions_workspace_bytes(n_cands, numel, dtype)
+
+
 def kb_screen_launch(n_cands, numel, dtype):
     out = KbLaunch()
     _check(lib().kb_screen_launch(n_cands, numel, dtype, ctypes.byref(out)))
@@ -296,10 +304,12 @@ def kb_screen_workspace_init(workspace, stream=None):
     return workspace
 
 
-def alloc_workspace(n_cands, numel, dtype, device, stream=None):
-    """A workspace for these sizes, zero-filled by the library."""
+def alloc_workspace(n_cands, numel, dtype, device, stream=None, positions=False):
+    """A workspace for these sizes (for calls with positions if `positions`),
+    zero-filled by the library."""
     torch = _torch()
-    nbytes = kb_screen_workspace_bytes(n_cands, numel, dtype)
+    nbytes = (kb_screen_positions_workspace_bytes if positions else kb_screen_workspace_bytes)(n_cands, numel,
+                                                                                              dtype)
     if nbytes == 0:
         raise KbError(KB_ERR_INVALID_ARG, "no workspace size for these arguments")
     ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -309,6 +319,25 @@ def alloc_workspace(n_cands, numel, dtype, device, stream=None):
 def alloc_stats(n_cands, device):
     torch = _torch()
     return torch.empty(n_cands * ctypes.sizeof(KbStats), dtype=torch.uint8, device=device)
+
+
+def alloc_locate(n_cands, device):
+    torch = _torch()
+    return torch.empty(n_cands * ctypes.sizeof(KbLocate), dtype=torch.uint8, device=device)
+
+
+def _sync_stream(stream):
+    """Wait for `stream` (torch's current stream when None)."""
+    torch = _torch()
+    (torch.cuda.current_stream() if stream is None else stream).synchronize()
+
+
+def read_locate(buf, n):
+    """Position dicts from a kb_locate buffer (copies a device buffer back on
+    torch's current stream: the caller has waited for the writing stream)."""
+    host = buf.cpu() if buf.device.type != "cpu" else buf
+    locs = (KbLocate * max(1, n)).from_buffer_copy(host.numpy().tobytes())
+    return [locs[k].as_dict() for k in range(n)]
 
 
 class HostTables:
@@ -366,23 +395,27 @@ def _after_one_off(keep, stream):
         _pending_tables.append((tables, tables.events[i]))
 
 
-def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, stream=None):
+def kb_screen(ref, cands, atol, rtol, flags=0, workspace=None, d_stats=None, stream=None, d_loc=None):
     """Enqueue the screen of `cands` (torch tensors or None) against `ref`.
 
     Returns (d_stats, workspace) device buffers; read the records with
     kb_screen_stats.  More than KB_INLINE_CANDS candidates go through
     kb_screen_ex with a pinned host table, kept alive here until the call
-    has passed.
+    has passed.  d_loc (a buffer of len(cands) kb_locate, see alloc_locate)
+    asks for the positions in the same pass (read them with read_locate).
     """
     n = len(cands)
     r = describe(ref)
     arr = (KbTensor * max(1, n))(*[describe(c) for c in cands])
     if workspace is None:
         workspace = alloc_workspace(max(1, n), ref.numel(), r.dtype if r.dtype >= 0 else 0,
-                                    ref.device, stream)
+                                    ref.device, stream, positions=d_loc is not None)
     if d_stats is None:
         d_stats = alloc_stats(max(1, n), ref.device)
     opts, keep = _one_off_opts(lib().kb_screen_host_table_bytes(n), stream)
+    if d_loc is not None:
+        opts = opts if opts is not None else KbScreenOpts(None, 0, None)
+        opts.d_loc = d_loc.data_ptr()
     _check(lib().kb_screen_ex(ctypes.byref(r), arr, n, float(atol), float(rtol), int(flags),
                               ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                               ctypes.c_void_p(d_stats.data_ptr()),
@@ -432,9 +465,8 @@ def kb_screen_locate(ref, cands, atol, rtol, d_stats, flags=0, stream=None):
     _check(lib().kb_screen_locate(ctypes.byref(r), arr, len(cands), float(atol), float(rtol),
                                   int(flags), ctypes.c_void_p(d_stats.data_ptr()),
                                   ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)))
-    host = out.cpu()
-    locs = (KbLocate * max(1, len(cands))).from_buffer_copy(host.numpy().tobytes())
-    return [locs[k].as_dict() for k in range(len(cands))]
+    _sync_stream(stream)
+    return read_locate(out, len(cands))
 
 
 class Locator:
@@ -452,6 +484,7 @@ class Locator:
         self.atol, self.rtol, self.flags = float(atol), float(rtol), int(flags)
         self._stats = ctypes.c_void_p(d_stats.data_ptr())
         self._out = ctypes.c_void_p(self.out.data_ptr())
+        self.stream = stream
         self._stream = _stream_handle(stream)
         self._L = lib()
 
@@ -460,16 +493,24 @@ class Locator:
                                         self.flags, self._stats, self._out, self._stream))
 
     def read(self):
-        host = self.out.cpu()
-        locs = (KbLocate * max(1, self.n)).from_buffer_copy(host.numpy().tobytes())
-        return [locs[k].as_dict() for k in range(self.n)]
+        """Wait for the launch stream, then copy the positions back."""
+        _sync_stream(self.stream)
+        return read_locate(self.out, self.n)
 
 
 def locate(ref, cands, atol, rtol, flags=0, stream=None):
-    """Screen, then locate: (records, positions)."""
+    """Screen, then locate (two passes): (records, positions)."""
     d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream)
     recs, _ = kb_screen_stats(d_stats, len(cands), stream=stream)
     return recs, kb_screen_locate(ref, cands, atol, rtol, d_stats, flags, stream=stream)
+
+
+def screen_positions(ref, cands, atol, rtol, flags=0, stream=None):
+    """Screen with the positions found in the same pass: (records, positions)."""
+    d_loc = alloc_locate(max(1, len(cands)), ref.device)
+    d_stats, _ = kb_screen(ref, cands, atol, rtol, flags, stream=stream, d_loc=d_loc)
+    recs, _ = kb_screen_stats(d_stats, len(cands), stream=stream)
+    return recs, read_locate(d_loc, len(cands))
 
 
 RUNG_MAX_ITER = 4096
@@ -724,9 +765,10 @@ class Screener:
     host_slots > 0 places the records in that many pinned host buffers that
     the kernel writes directly (a pipelined caller launches into one slot and
     summarizes another after an event); otherwise they go to device memory
-    and read() copies them back."""
+    and read() copies them back.  positions=True also finds the positions in
+    the same pass (positions() copies them back)."""
 
-    def __init__(self, ref, cands, atol, rtol, flags=0, stream=None, host_slots=0):
+    def __init__(self, ref, cands, atol, rtol, flags=0, stream=None, host_slots=0, positions=False):
         torch = _torch()
         self.ref, self.cands = ref, list(cands)
         self.n = len(self.cands)
@@ -736,7 +778,8 @@ class Screener:
         self._ref = describe(ref)
         self._arr = (KbTensor * max(1, self.n))(*[describe(c) for c in self.cands])
         self.workspace = alloc_workspace(max(1, self.n), ref.numel(), self._ref.dtype, ref.device,
-                                         stream)
+                                         stream, positions=positions)
+        self.d_loc = alloc_locate(max(1, self.n), ref.device) if positions else None
         self._ws = ctypes.c_void_p(self.workspace.data_ptr())
         nbytes = max(1, self.n) * ctypes.sizeof(KbStats)
         if host_slots > 0:
@@ -756,13 +799,20 @@ class Screener:
         # tables, one per record slot (at least two)
         tb = self._L.kb_screen_host_table_bytes(max(1, self.n))
         self._tables = HostTables(tb, count=max(2, len(self.slots))) if tb > 0 else None
+        self._opts = None
+        if self.d_loc is not None:
+            if self._tables:
+                for o in self._tables.opts:
+                    o.d_loc = self.d_loc.data_ptr()
+            else:
+                self._opts = KbScreenOpts(None, 0, self.d_loc.data_ptr())
 
     @property
     def d_stats(self):
         return self.slots[0]
 
     def launch(self, slot=0):
-        i, opts = self._tables.acquire() if self._tables else (None, None)
+        i, opts = self._tables.acquire() if self._tables else (None, self._opts)
         _check(self._L.kb_screen_ex(ctypes.byref(self._ref), self._arr, self.n, self.atol, self.rtol,
                                     self.flags, self._ws, self.workspace.numel(),
                                     self._slot_ptr[slot], ctypes.byref(opts) if opts is not None else None,
@@ -792,6 +842,12 @@ class Screener:
             src = self._views[slot]
             _check(self._L.kb_summarize(src, self.n, None, self._passed))
         return [src[k].as_dict(self._passed[k]) for k in range(self.n)]
+
+    def positions(self):
+        """Wait for the launch stream, then copy the positions of the last
+        launch back (positions=True only)."""
+        _sync_stream(self.stream)
+        return read_locate(self.d_loc, self.n)
 
     def launch_plan(self):
         return kb_screen_launch(max(1, self.n), self.ref.numel(), self._ref.dtype)

@@ -173,12 +173,12 @@ int dirty_workspace_error(const kb_stats* st, int n) {
 // Work-groups of the screening kernel for (dtype, kg) resident on the
 // current device at once; 0 if the device cannot be queried (then the plan
 // falls back to a fixed total).
-int resident_blocks(int dtype, int kg, bool fail_fast = false, bool wide = false) {
+int resident_blocks(int dtype, int kg, bool fail_fast = false, bool wide = false, bool loc = false) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
-    return cus * screen_blocks_per_cu(dtype, kg, fail_fast, wide);
+    return cus * screen_blocks_per_cu(dtype, kg, fail_fast, wide, loc);
 }
 int plan_group_size(int n_cands, int dtype) {
     // Measured on the five screening workloads: groups of 4 for fp32 and
@@ -278,6 +278,11 @@ bool make_plan(int n_cands, int n_acc, uint64_t numel, int dtype, int resident_b
     off = align_up(off + (size_t)n_cands * super_ws * sizeof(Part2), 256);
     P.off_part2_ssr = off;
     off = align_up(off + (size_t)groups_max * super_ws * 8, 256);
+    P.core_total = off;
+    P.off_part_idx = off;
+    off = align_up(off + (size_t)IX_COUNT * n_cands * Cw * 8, 256);
+    P.off_part2_idx = off;
+    off = align_up(off + (size_t)n_cands * super_ws * sizeof(Part2Idx), 256);
     P.total = off;
     *plan = P;
     return true;
@@ -300,29 +305,37 @@ size_t host_table_bytes(int n_cands) {
 // caller has validated ref, cands, n_cands, atol, rtol and flags.
 // host_table: caller-owned pinned host memory of at least
 // host_table_bytes(n_cands) bytes when the table does not fit the kernel
-// arguments (the kernels then read it there), else ignored.
+// arguments (the kernels then read it there), else ignored.  d_loc: NULL, or
+// the candidates' positions, found in the same pass.
 int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* cands, int n_cands,
                        const int32_t* status, float atol, float rtol, uint32_t flags, void* workspace,
                        size_t workspace_bytes, void* host_table, size_t host_table_size,
-                       kb_stats* d_stats, hipStream_t stream) {
+                       kb_stats* d_stats, kb_locate* d_loc, hipStream_t stream) {
     const bool fail_fast = (flags & KB_FAIL_FAST) != 0;
+    const bool loc = d_loc != nullptr;
+    if (fail_fast && loc)
+        return fail(KB_ERR_INVALID_ARG, "%s: positions are not found under KB_FAIL_FAST", who);
     if (!is_contiguous(*ref)) return fail(KB_ERR_INVALID_ARG, "%s: reference is not contiguous", who);
     const uint64_t numel = tensor_numel(*ref);
     const int dtype = ref->dtype;
+    // the positions variant keeps 512-element chunk numbers (and two tail
+    // codes after them) in 32 bits
+    if (loc && numel / 512 + 2 > 0xFFFFFFFFull)
+        return fail(KB_ERR_INVALID_ARG, "%s: positions need fewer than 2^41 elements", who);
     int n_acc = 0;
     for (int k = 0; k < n_cands; ++k) n_acc += status[k] == KB_STATUS_OK;
 
     ScreenPlan P;
     const int kg = plan_group_size(n_cands, dtype);
-    const bool wide = use_wide_kernel(dtype, kg, fail_fast, numel);
-    if (!make_plan(n_cands, n_acc, numel, dtype, resident_blocks(dtype, kg, fail_fast, wide), fail_fast, &P))
+    const bool wide = use_wide_kernel(dtype, kg, fail_fast, numel, loc);
+    if (!make_plan(n_cands, n_acc, numel, dtype, resident_blocks(dtype, kg, fail_fast, wide, loc), fail_fast, &P))
         return fail(KB_ERR_INVALID_ARG, "%s: no launch plan (numel=%llu)", who,
                     (unsigned long long)numel);
-    if (workspace == nullptr || workspace_bytes < P.total)
-        return fail(KB_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who,
-                    workspace_bytes, P.total);
-    if (!aligned16(ref->data) || !aligned16(workspace) || !aligned16(d_stats))
-        return fail(KB_ERR_ALIGNMENT, "%s: reference, workspace or d_stats not 16-byte aligned", who);
+    const size_t need = loc ? P.total : P.core_total;
+    if (workspace == nullptr || workspace_bytes < need)
+        return fail(KB_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, need);
+    if (!aligned16(ref->data) || !aligned16(workspace) || !aligned16(d_stats) || !aligned16(d_loc))
+        return fail(KB_ERR_ALIGNMENT, "%s: reference, workspace, d_stats or d_loc not 16-byte aligned", who);
     for (int k = 0; k < n_cands; ++k)
         if (status[k] == KB_STATUS_OK && !aligned16(cands[k].data))
             return fail(KB_ERR_ALIGNMENT, "%s: candidate %d data not 16-byte aligned", who, k);
@@ -333,11 +346,11 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     // host memory, which the kernels read directly.
     const int n_table = n_cands;
     const bool table_inline = n_table <= kInlineCands;
-    const size_t need = host_table_bytes(n_cands);
-    if (!table_inline && (host_table == nullptr || host_table_size < need))
+    const size_t need_table = host_table_bytes(n_cands);
+    if (!table_inline && (host_table == nullptr || host_table_size < need_table))
         return fail(KB_ERR_WORKSPACE,
                     "%s: %d candidates need a pinned host table of %zu bytes (kb_screen_ex), %zu given",
-                    who, n_cands, need, host_table == nullptr ? (size_t)0 : host_table_size);
+                    who, n_cands, need_table, host_table == nullptr ? (size_t)0 : host_table_size);
     if (!table_inline && !aligned16(host_table))
         return fail(KB_ERR_ALIGNMENT, "%s: host table not 16-byte aligned", who);
     InlineTable tab;
@@ -354,7 +367,7 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     P.wide = wide ? 1 : 0;
     hipError_t e;
     if (n_acc == 0 || numel == 0) {
-        e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, stream);
+        e = launch_records_only(d_table, tab, table_inline ? 1 : 0, n_table, numel, d_stats, d_loc, stream);
         if (e != hipSuccess) return fail(KB_ERR_HIP, "%s: records launch: %s", who, hipGetErrorString(e));
         return KB_OK;
     }
@@ -385,8 +398,11 @@ int screen_with_status(const char* who, const kb_tensor* ref, const kb_tensor* c
     p.part_ssrc = (double*)(ws + P.off_part_ssrc);
     p.part2 = (Part2*)(ws + P.off_part2);
     p.part2_ssr = (double*)(ws + P.off_part2_ssr);
+    p.part_idx = loc ? (uint64_t*)(ws + P.off_part_idx) : nullptr;
+    p.part2_idx = loc ? (Part2Idx*)(ws + P.off_part2_idx) : nullptr;
     p.stats = d_stats;
-    e = launch_screen(P, p, tab, fail_fast, stream);
+    p.loc = d_loc;
+    e = launch_screen(P, p, tab, fail_fast, loc, stream);
     if (e != hipSuccess) return fail(KB_ERR_HIP, "%s: kernel launch: %s", who, hipGetErrorString(e));
     return KB_OK;
 }
@@ -415,6 +431,12 @@ int kb_policy_check(const kb_tensor* ref, const kb_tensor* cands, int n_cands, i
 }
 
 size_t kb_screen_workspace_bytes(int n_cands, uint64_t numel, int dtype) {
+    ScreenPlan P;
+    if (!make_plan(n_cands, n_cands, numel, dtype, 0, false, &P)) return 0;
+    return P.core_total;
+}
+
+size_t kb_screen_positions_workspace_bytes(int n_cands, uint64_t numel, int dtype) {
     ScreenPlan P;
     if (!make_plan(n_cands, n_cands, numel, dtype, 0, false, &P)) return 0;
     return P.total;
@@ -469,9 +491,9 @@ int kb_screen_noalloc(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
     if (!make_plan(n_cands, n_cands, numel, ref->dtype, 0, false, &P))
         return fail(KB_ERR_INVALID_ARG, "kb_screen_noalloc: no launch plan (numel=%llu)",
                     (unsigned long long)numel);
-    if (P.total > (size_t)KB_NOALLOC_SCRATCH_BYTES)
+    if (P.core_total > (size_t)KB_NOALLOC_SCRATCH_BYTES)
         return fail(KB_ERR_WORKSPACE, "kb_screen_noalloc: the call needs %zu bytes of scratch, the fixed "
-                    "scratch holds %zu", P.total, (size_t)KB_NOALLOC_SCRATCH_BYTES);
+                    "scratch holds %zu", P.core_total, (size_t)KB_NOALLOC_SCRATCH_BYTES);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail_hip(e, "kb_screen_noalloc: hipGetDevice");
@@ -484,7 +506,7 @@ int kb_screen_noalloc(const kb_tensor* ref, const kb_tensor* cands, int n_cands,
     e = launch_zero_fill(ws, P.off_part_u32, stream);
     if (e != hipSuccess) return fail_hip(e, "kb_screen_noalloc: fill launch");
     return screen_with_status("kb_screen_noalloc", ref, cands, n_cands, status, atol, rtol, flags, ws,
-                              (size_t)KB_NOALLOC_SCRATCH_BYTES, nullptr, 0, d_stats, stream);
+                              (size_t)KB_NOALLOC_SCRATCH_BYTES, nullptr, 0, d_stats, nullptr, stream);
 }
 
 int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
@@ -498,7 +520,7 @@ int kb_screen_ex(const kb_tensor* ref, const kb_tensor* cands, int n_cands, floa
     if (rc != KB_OK) return rc;
     return screen_with_status("kb_screen", ref, cands, n_cands, status.data(), atol, rtol, flags,
                               workspace, workspace_bytes, opts ? opts->host_table : nullptr,
-                              opts ? opts->host_table_bytes : 0, d_stats, stream);
+                              opts ? opts->host_table_bytes : 0, d_stats, opts ? opts->d_loc : nullptr, stream);
 }
 
 int kb_screen(const kb_tensor* ref, const kb_tensor* cands, int n_cands, float atol, float rtol,
@@ -551,6 +573,8 @@ int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands
                         o);
     if (flags & ~(uint32_t)(KB_EQUAL_NAN | KB_FAIL_FAST))
         return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: unknown flags 0x%x", flags);
+    if (opts != nullptr && opts->d_loc != nullptr)
+        return fail(KB_ERR_INVALID_ARG, "kb_screen_multi: positions (d_loc) are not found for multi-output screens");
     // One gate over all outputs: a candidate is accepted only if every output
     // passes; otherwise every output's record carries the first failing
     // check, in output order.
@@ -601,7 +625,7 @@ int kb_screen_multi(const kb_tensor* refs, int n_outputs, const kb_tensor* cands
         const int rc = screen_with_status("kb_screen_multi", &refs[o], col.data(), n_cands, combined.data(),
                                           atol[o], rtol[o], flags, ws + offs[o], bytes,
                                           htab ? htab + (size_t)o * tab_bytes : nullptr, tab_bytes,
-                                          d_stats + (size_t)o * n_cands, stream);
+                                          d_stats + (size_t)o * n_cands, nullptr, stream);
         if (rc != KB_OK) return rc;
     }
     return KB_OK;

@@ -165,6 +165,27 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
     return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+    v = min(v, dpp_u32<DPP_QUAD_XOR1>(v));
+    v = min(v, dpp_u32<DPP_QUAD_XOR2>(v));
+    v = min(v, dpp_u32<DPP_ROW_HALF_MIRROR>(v));
+    v = min(v, dpp_u32<DPP_ROW_MIRROR>(v));
+    const uint32_t a = min(readlane_u32(v, 0), readlane_u32(v, 16));
+    const uint32_t b = min(readlane_u32(v, 32), readlane_u32(v, 48));
+    return min(a, b);
+}
+
+__device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+    v = min_u64(v, dpp_u64<DPP_QUAD_XOR1>(v));
+    v = min_u64(v, dpp_u64<DPP_QUAD_XOR2>(v));
+    v = min_u64(v, dpp_u64<DPP_ROW_HALF_MIRROR>(v));
+    v = min_u64(v, dpp_u64<DPP_ROW_MIRROR>(v));
+    return min_u64(min_u64(readlane_u64(v, 0), readlane_u64(v, 16)),
+                   min_u64(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+
 // Reductions within one 16-lane DPP row: the four steps above leave every
 // lane of a row holding the row's result (no cross-row reads), so a
 // work-group can reduce up to 16 independent values, one per row.
@@ -187,6 +208,13 @@ __device__ __forceinline__ uint64_t row_sum_u64(uint64_t v) {
     v += dpp_u64<DPP_QUAD_XOR2>(v);
     v += dpp_u64<DPP_ROW_HALF_MIRROR>(v);
     return v + dpp_u64<DPP_ROW_MIRROR>(v);
+}
+
+__device__ __forceinline__ uint64_t row_min_u64(uint64_t v) {
+    v = min_u64(v, dpp_u64<DPP_QUAD_XOR1>(v));
+    v = min_u64(v, dpp_u64<DPP_QUAD_XOR2>(v));
+    v = min_u64(v, dpp_u64<DPP_ROW_HALF_MIRROR>(v));
+    return min_u64(v, dpp_u64<DPP_ROW_MIRROR>(v));
 }
 
 __device__ __forceinline__ double row_sum_f64(double v) {

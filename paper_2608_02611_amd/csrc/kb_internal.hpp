@@ -50,9 +50,18 @@ struct ScreenPlan {
     int n_super;          // ceil(blocks_per_group / 16): first-level combine groups
     int ff_round;         // fail-fast launch: candidate groups per round
     int wide;             // launch the 5-waves-per-SIMD build (use_wide_kernel)
-    // workspace byte offsets
+    // workspace byte offsets; core_total ends what every call uses, total
+    // adds the position-search partials (calls with positions only)
     size_t off_tickets1, off_tickets2, off_ff_flags, off_table, off_part_u32, off_part_ssd,
-        off_part_ssr, off_part_ssrc, off_part2, off_part2_ssr, total;
+        off_part_ssr, off_part_ssrc, off_part2, off_part2_ssr, core_total, off_part_idx, off_part2_idx, total;
+};
+
+// Position-search partials: per (work-group, candidate), the smallest
+// mismatching element index, and the smallest element index at which the
+// max abs error and the max rel error are reached (all ones: none).
+enum IdxField : int { IX_FIRST_MISMATCH = 0, IX_MAX_ABS, IX_MAX_REL, IX_COUNT };
+struct Part2Idx {
+    uint64_t ix[IX_COUNT];
 };
 
 // Second-level partial of one candidate: the combine of up to 16 work-groups.
@@ -82,13 +91,13 @@ int plan_group_size(int n_cands, int dtype);
 // elements per tensor; 5% slower on 2^18 elements (1024 candidates), whose
 // 2048 work-groups make two whole rounds at 4 per CU but not at 5.
 constexpr uint64_t kWideMinNumel = 1ull << 22;
-inline bool use_wide_kernel(int dtype, int kg, bool fail_fast, uint64_t numel) {
-    return dtype == KB_F32 && kg == 4 && !fail_fast && numel >= kWideMinNumel;
+inline bool use_wide_kernel(int dtype, int kg, bool fail_fast, uint64_t numel, bool loc = false) {
+    return dtype == KB_F32 && kg == 4 && !fail_fast && !loc && numel >= kWideMinNumel;
 }
 
-// Work-groups of the screening kernel for (dtype, kg, fail-fast, wide)
-// resident per CU (occupancy query, cached), or 0 on failure.
-int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide = false);
+// Work-groups of the screening kernel for (dtype, kg, fail-fast, wide,
+// positions) resident per CU (occupancy query, cached), or 0 on failure.
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide = false, bool loc = false);
 
 // Candidate groups per round of a fail-fast launch (see make_plan).
 constexpr int kFailFastRound = 2;
@@ -129,20 +138,26 @@ struct ScreenParams {
     double* part_ssrc;   // fail-fast: [n_acc][blocks_per_group] per-candidate sums of r^2
     Part2* part2;        // [n_acc][n_super]
     double* part2_ssr;   // [n_groups][n_super]
+    uint64_t* part_idx;  // positions: [IX_COUNT][n_acc][blocks_per_group]
+    Part2Idx* part2_idx; // positions: [n_acc][n_super]
     kb_stats* stats;     // caller's records, indexed by CandEntry::index
+    kb_locate* loc;      // positions launch: the caller's positions, indexed like stats
 };
 
 // tab: the launch table when it is inline (n_cands <= kInlineCands), else
-// ignored (p.table points at the uploaded copy).  fail_fast selects the
-// early-reject variant of the kernel.
+// ignored (p.table points at the caller's copy).  fail_fast selects the
+// early-reject variant of the kernel, loc the variant that also finds the
+// positions (p.loc); never both.
 hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
-                         bool fail_fast, hipStream_t stream);
+                         bool fail_fast, bool loc, hipStream_t stream);
 // Zero-fill n bytes of device memory (workspace initialisation).
 hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream);
 // Records for calls with no element to read (numel == 0 or no accepted
-// candidate): every record written from the table alone.
+// candidate): every record written from the table alone (and, with loc,
+// every position -1).
 hipError_t launch_records_only(const CandEntry* table, const InlineTable& tab, int table_inline,
-                               int n_table, uint64_t numel, kb_stats* stats, hipStream_t stream);
+                               int n_table, uint64_t numel, kb_stats* stats, kb_locate* loc,
+                               hipStream_t stream);
 
 // Position search (kb_screen_locate): up to kLocateBatch candidates per
 // launch, their table in the kernel arguments.

@@ -253,11 +253,13 @@ struct NonFinite {
 // candidate (every lane active).  Also the path for the ragged tail.
 // Updates the wave's mismatch count, the lane's max abs error, the wave's
 // max-rel O and non-finite counts, and adds the lane's binary64 squared
-// differences to its LDS slot.
-template <int DT>
+// differences to its LDS slot.  LOC: a rise of the lane's max abs error
+// also records `code` (the chunk) in achunk.
+template <int DT, bool LOC>
 __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_in[kE], float atol,
                                             float rtol, bool equal_nan, double* ssd_slot,
-                                            uint32_t& mism, uint32_t& amax, float& O, NonFinite& nf) {
+                                            uint32_t& mism, uint32_t& amax, uint32_t& achunk, uint32_t code,
+                                            float& O, NonFinite& nf) {
     float r[kE];
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -287,11 +289,75 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
     }
     atomicAdd(ssd_slot, sd);
     mism += nm;
-    amax = max(amax, __float_as_uint(ma));
+    if constexpr (LOC) {
+        if (__float_as_uint(ma) > amax) {
+            amax = __float_as_uint(ma);
+            achunk = code;
+        }
+    } else {
+        amax = max(amax, __float_as_uint(ma));
+    }
     O = fmaxf(O, wave_max_f(qm));
     nf.nan += nnan;
     nf.pinf += npinf;
     nf.ninf += nninf;
+}
+
+// ----------------------------------------------------------- positions ---
+// The fused position search (LOC) keeps, per candidate: the wave's first
+// mismatching element (found in the first chunk that has one: a wave visits
+// its chunks in increasing index order), the chunk in which each lane's
+// running max abs error last rose (strictly, so its first occurrence), and the
+// element of the wave's own max rel error (found when it rises).  All rare
+// paths except the max-abs chunk, two more instructions per chunk.
+constexpr uint64_t kNone = ~0ull;
+
+// Element offset within the chunk of slot i of `lane` (fp32: elements
+// 4 lane .. 4 lane + 3 and 256 + 4 lane ..; 16-bit: 8 lane ..), increasing
+// with i; kE (no slot) maps to all ones.
+template <int DT>
+__device__ __forceinline__ uint32_t slot_offset(int lane, uint32_t i) {
+    if (i >= (uint32_t)kE) return 0xFFFFFFFFu;
+    if constexpr (DT == DT_F32) return i < 4 ? 4u * lane + i : 256u + 4u * lane + (i - 4u);
+    else return 8u * lane + i;
+}
+
+// The lane's first slot whose element does not match (the definition's
+// predicate, special values included), kE if none.
+template <int DT>
+__device__ __forceinline__ uint32_t lane_first_mismatch(const Raw<DT>& cand, const float r[kE], float atol, float rtol,
+                                                        bool equal_nan) {
+    uint32_t slot = kE;
+#pragma unroll
+    for (int i = kE - 1; i >= 0; --i) {
+        const float c = elem<DT>(cand, i);
+        const float d = fabsf(c - r[i]);
+        const float tol = __builtin_isfinite(r[i]) ? __fadd_rn(atol, __fmul_rn(rtol, fabsf(r[i]))) : -1.0f;
+        const bool match = (c == r[i]) || (d <= tol) || (equal_nan && __builtin_isnan(c) && __builtin_isnan(r[i]));
+        if (!match) slot = i;
+    }
+    return slot;
+}
+
+// The lane's first slot whose quotient fl(|c - r| / |r|) equals q (q > 0), kE
+// if none.
+template <int DT>
+__device__ __forceinline__ uint32_t lane_rel_slot(const Raw<DT>& cand, const float r[kE], float q) {
+    uint32_t slot = kE;
+#pragma unroll
+    for (int i = kE - 1; i >= 0; --i)
+        if (fabsf(elem<DT>(cand, i) - r[i]) / fabsf(r[i]) == q) slot = i;
+    return slot;
+}
+
+// The lane's first slot whose |c - r| has the bits m, kE if none.
+template <int DT>
+__device__ __forceinline__ uint32_t lane_abs_slot(const Raw<DT>& cand, const Raw<DT>& ref, uint32_t m) {
+    uint32_t slot = kE;
+#pragma unroll
+    for (int i = kE - 1; i >= 0; --i)
+        if (__float_as_uint(fabsf(elem<DT>(cand, i) - elem<DT>(ref, i))) == m) slot = i;
+    return slot;
 }
 
 // Raises the work-group's max-rel value of one candidate (rare; O >= 0, so
@@ -335,6 +401,16 @@ __device__ __forceinline__ void write_record(kb_stats* dst, uint64_t numel, uint
     *dst = st;
 }
 
+// Positions of one candidate (all ones: none -> -1).
+__device__ __forceinline__ void write_loc(kb_locate* dst, uint64_t fm, uint64_t ai, uint64_t ri) {
+    kb_locate l;
+    l.first_mismatch = fm == kNone ? -1 : (int64_t)fm;
+    l.max_abs_index = ai == kNone ? -1 : (int64_t)ai;
+    l.max_rel_index = ri == kNone ? -1 : (int64_t)ri;
+    l.reserved = -1;
+    *dst = l;
+}
+
 // The launch table: the kernel argument, or the caller's pinned host copy.
 __device__ __forceinline__ const CandEntry* table_of(const ScreenParams& p, const InlineTable& tab) {
     return p.table_inline ? tab.e : p.table;
@@ -351,22 +427,26 @@ __device__ __forceinline__ void report_dirty(const ScreenParams& p, const CandEn
         kb_stats st = {};
         st.status = KB_ERR_WORKSPACE;
         p.stats[table[j0 + j].index] = st;
+        if (p.loc) write_loc(&p.loc[table[j0 + j].index], kNone, kNone, kNone);
     }
     if (g == 0) {
         for (int k = p.rej_start + (int)threadIdx.x; k < p.n_table; k += kThreads) {
             kb_stats st = {};
             st.status = table[k].status;
             p.stats[table[k].index] = st;
+            if (p.loc) write_loc(&p.loc[table[k].index], kNone, kNone, kNone);
         }
     }
 }
 
-// Records of the rejected candidates (written by group 0's finisher).
+// Records (and, with positions, all -1 positions) of the rejected candidates
+// (written by group 0's finisher).
 __device__ __forceinline__ void write_rejected(const ScreenParams& p, const CandEntry* table) {
     for (int k = p.rej_start + (int)threadIdx.x; k < p.n_table; k += kThreads) {
         kb_stats st = {};
         st.status = table[k].status;
         p.stats[table[k].index] = st;
+        if (p.loc) write_loc(&p.loc[table[k].index], kNone, kNone, kNone);
     }
 }
 
@@ -416,9 +496,24 @@ __device__ __forceinline__ void clear_ff_words(const ScreenParams& p, int j0, in
 // have been waited for anyway, so it adds no wait.  A candidate without
 // mismatch is never stopped, and all its sums are formed in the same order
 // as without FF (the same bits).
-template <int DT, int KG, bool FF>
+//
+// LOC: the variant that also finds each candidate's positions (p.loc): the
+// first mismatching element and the first elements at which the max abs and
+// max rel errors are reached.  Per wave and candidate: the first mismatch is
+// searched in the first chunk whose count shows one (the wave's chunks come
+// in increasing index order, so later ones can only be larger); each lane
+// keeps the chunk in which its max abs error last rose (strictly: the first
+// chunk that holds its maximum), and at the end the lanes holding the wave's
+// maximum re-read that chunk for the element; the max-rel element is found
+// in the chunk that raises O.  Waves then do not share O (a shared value
+// would filter out elements that tie it at smaller indices).  The positions
+// are combined like the maxima (the smallest index among the parts that
+// hold the maximum) in the same fixed orders, so they are the smallest
+// qualifying indices whatever the launch.
+template <int DT, int KG, bool FF, bool LOC>
 __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineTable& tab, const int g,
                                             const int stripe) {
+    static_assert(!(FF && LOC), "positions are not found under fail-fast");
     __shared__ double s_ssd[KG][kThreads];  // lane sums of squared differences
     __shared__ WaveOut s_out[kWaves][KG];
     __shared__ double s_ssr[kWaves];
@@ -431,6 +526,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     __shared__ double s_ssrc[FF ? kWaves : 1][FF ? KG : 1];
     __shared__ double s_sr1c[FF ? KG : 1];  // single-level finish, per candidate
     __shared__ uint32_t s_told[FF ? KG : 1];  // fail-fast: the work-group knows candidate j failed
+    __shared__ uint64_t s_idx[LOC ? kWaves : 1][LOC ? KG : 1][IX_COUNT];  // positions per wave
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -453,11 +549,17 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     uint32_t amax[KG];  // lane max abs error (binary32 bits, non-negative)
     uint32_t orel[KG];  // wave-uniform max rel error O (binary32 bits, non-negative)
     uint32_t bitdiff = 0u;  // bit j: candidate j differs somewhere in this wave's range
+    uint64_t fm[KG];        // positions: the wave's first mismatch (wave-uniform)
+    uint64_t ridx[KG];      // positions: the element of O (wave-uniform)
+    uint32_t achunk[KG];    // positions: the chunk of the lane's max abs error
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
         mism[j] = 0u;
         amax[j] = 0u;
         orel[j] = 0u;
+        fm[j] = kNone;
+        ridx[j] = kNone;
+        achunk[j] = 0u;
         s_ssd[j][threadIdx.x] = 0.0;
     }
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
@@ -533,9 +635,12 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             craw[j] = load_chunk<DT, true>(uniform_ptr(cand[j] + cb), o);
         }
         // the work-group's shared max-rel values
+        if constexpr (!LOC) {
 #pragma unroll
-        for (int j = 0; j < KG; ++j)
-            orel[j] = max(orel[j], (uint32_t)__builtin_amdgcn_readfirstlane(s_rel[j]));
+            for (int j = 0; j < KG; ++j)
+                orel[j] = max(orel[j], (uint32_t)__builtin_amdgcn_readfirstlane(s_rel[j]));
+        }
+        const uint64_t ebase = chunk * kChunk;  // the chunk's first element
 
         // Reference side, once per element for all KG candidates.
         float r[kE], tol[kE];
@@ -601,16 +706,35 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             if (ballot(!(acc < __builtin_inff()))) {
                 // NaN, infinity or a squared difference beyond binary32
                 float o = O;
-                exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
-                                amax[j], o, s_nf[wave][j]);
+                const uint32_t mism0 = mism[j];
+                exact_chunk<DT, LOC>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
+                                     amax[j], achunk[j], (uint32_t)chunk, o, s_nf[wave][j]);
                 if (o > O) {
                     orel[j] = __float_as_uint(o);
-                    publish_rel(&s_rel[j], o, lane);
+                    if constexpr (LOC)
+                        ridx[j] = ebase + wave_min_u32(slot_offset<DT>(lane, lane_rel_slot<DT>(cr, r, o)));
+                    else
+                        publish_rel(&s_rel[j], o, lane);
+                }
+                if constexpr (LOC) {
+                    if (fm[j] == kNone && mism[j] != mism0)
+                        fm[j] = ebase + wave_min_u32(slot_offset<DT>(
+                                            lane, lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan)));
                 }
                 continue;
             }
             mism[j] += (uint32_t)kChunk - nmatch;
-            amax[j] = max(amax[j], __float_as_uint(tmax));
+            if constexpr (LOC) {
+                if (fm[j] == kNone && nmatch != (uint32_t)kChunk)
+                    fm[j] = ebase + wave_min_u32(slot_offset<DT>(
+                                        lane, lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan)));
+                if (__float_as_uint(tmax) > amax[j]) {
+                    amax[j] = __float_as_uint(tmax);
+                    achunk[j] = (uint32_t)chunk;
+                }
+            } else {
+                amax[j] = max(amax[j], __float_as_uint(tmax));
+            }
             // lanes whose differences are all tiny but not all zero: binary32
             // squares would underflow, so square in binary64
             const bool tiny = (__float_as_uint(tmax) - 1u) < (__float_as_uint(kTiny) - 1u);
@@ -640,7 +764,10 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 const float q = wave_max_f(qm);
                 if (q > O) {
                     orel[j] = __float_as_uint(q);
-                    publish_rel(&s_rel[j], q, lane);
+                    if constexpr (LOC)
+                        ridx[j] = ebase + wave_min_u32(slot_offset<DT>(lane, lane_rel_slot<DT>(cr, r, q)));
+                    else
+                        publish_rel(&s_rel[j], q, lane);
                 }
             }
         }
@@ -692,8 +819,9 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     // group, one element per thread, exact path (out-of-range lanes and
     // elements 1..7 compare 0 with 0, which changes no statistic).
     uint32_t n_tail = 0u;  // tail elements this wave compared (for every live candidate)
+    const uint64_t tfirst = n_chunks * kChunk;
     if (stripe == 0) {
-        const uint64_t first = n_chunks * kChunk;
+        const uint64_t first = tfirst;
         for (uint64_t base = first; base < p.numel; base += kThreads) {
             const uint64_t e = base + threadIdx.x;
             const bool valid = e < p.numel;
@@ -721,9 +849,21 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 for (int w = 0; w < Raw<DT>::kWords; ++w) cr.w[w] = 0u;
                 cr.w[0] = cb;
                 float o = __uint_as_float(orel[j]);
-                exact_chunk<DT>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
-                                amax[j], o, s_nf[wave][j]);
+                const float o0 = o;
+                const uint32_t mism0 = mism[j];
+                // positions: tail element e is slot 0 of its lane; the max-abs
+                // chunk code of the tail is n_chunks + (base - first) / 256
+                exact_chunk<DT, LOC>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
+                                     amax[j], achunk[j], (uint32_t)(n_chunks + (base - first) / kThreads), o,
+                                     s_nf[wave][j]);
                 orel[j] = __float_as_uint(o);
+                if constexpr (LOC) {
+                    if (o > o0) ridx[j] = wave_min_u64(lane_rel_slot<DT>(cr, r, o) < (uint32_t)kE ? e : kNone);
+                    if (fm[j] == kNone && mism[j] != mism0)
+                        fm[j] = wave_min_u64(lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan) < (uint32_t)kE
+                                                 ? e
+                                                 : kNone);
+                }
             }
         }
     }
@@ -734,6 +874,31 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         if (j >= kg) continue;
         const double sd = wave_sum_f64(s_ssd[j][threadIdx.x]);
         const uint32_t am = wave_max_u32(amax[j]);
+        if constexpr (LOC) {
+            // the element of the wave's max abs error: the lanes that hold it
+            // re-read the chunk in which it first occurred
+            uint64_t ai = kNone;
+            if (am != 0u) {
+                uint64_t mine = kNone;
+                if (amax[j] == am) {
+                    const uint32_t ac = achunk[j];
+                    if (ac < n_chunks) {
+                        const uint64_t cb = (uint64_t)ac * chunk_bytes<DT>();
+                        const Raw<DT> c = load_chunk<DT, false>(cand[j] + cb, off);
+                        const Raw<DT> rr = load_chunk<DT, false>(ref + cb, off);
+                        mine = (uint64_t)ac * kChunk + slot_offset<DT>(lane, lane_abs_slot<DT>(c, rr, am));
+                    } else {
+                        mine = tfirst + (uint64_t)(ac - (uint32_t)n_chunks) * kThreads + threadIdx.x;
+                    }
+                }
+                ai = wave_min_u64(mine);
+            }
+            if (lane == 0) {
+                s_idx[wave][j][IX_FIRST_MISMATCH] = fm[j];
+                s_idx[wave][j][IX_MAX_ABS] = ai;
+                s_idx[wave][j][IX_MAX_REL] = ridx[j];
+            }
+        }
         if (lane == 0) {
             WaveOut& o = s_out[wave][j];
             o.u[PF_MISM] = mism[j];
@@ -796,6 +961,19 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             st_coherent(&p.part_u32[PF_NREAD * plane + row], nr);
             st_coherent(&p.part_ssrc[row], src);
         }
+        if constexpr (LOC) {
+            // the smallest index among the waves that hold each maximum
+            uint64_t i0 = kNone, i1 = kNone, i2 = kNone;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) {
+                i0 = min_u64(i0, s_idx[w][j][IX_FIRST_MISMATCH]);
+                if (s_out[w][j].u[PF_MAXABS] == ma) i1 = min_u64(i1, s_idx[w][j][IX_MAX_ABS]);
+                if (s_out[w][j].u[PF_MAXREL] == mr) i2 = min_u64(i2, s_idx[w][j][IX_MAX_REL]);
+            }
+            st_coherent(&p.part_idx[IX_FIRST_MISMATCH * plane + row], i0);
+            st_coherent(&p.part_idx[IX_MAX_ABS * plane + row], i1);
+            st_coherent(&p.part_idx[IX_MAX_REL * plane + row], i2);
+        }
         st_coherent(&p.part_u32[PF_MISM * plane + row], mi);
         st_coherent(&p.part_u32[PF_NAN * plane + row], na);
         st_coherent(&p.part_u32[PF_PINF * plane + row], pi);
@@ -840,8 +1018,14 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         uint64_t mi = 0, na = 0, pi = 0, ni = 0, nr = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
         double sd = 0.0, src = 0.0;
+        uint64_t i0 = kNone, i1 = kNone, i2 = kNone;  // positions
         if (jj < kg) {
             const size_t idx = (size_t)(j0 + jj) * C + s;
+            if (LOC && have) {
+                i0 = ld_coherent(&p.part_idx[IX_FIRST_MISMATCH * plane + idx]);
+                i1 = ld_coherent(&p.part_idx[IX_MAX_ABS * plane + idx]);
+                i2 = ld_coherent(&p.part_idx[IX_MAX_REL * plane + idx]);
+            }
             if (FF && have) {
                 nr = ld_coherent(&p.part_u32[PF_NREAD * plane + idx]);
                 src = ld_coherent(&p.part_ssrc[idx]);
@@ -860,10 +1044,22 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             na = row_sum_u64(na);
             pi = row_sum_u64(pi);
             ni = row_sum_u64(ni);
+            const uint32_t ma_own = ma, mr_own = mr;
             ma = row_max_u32(ma);
             mr = row_max_u32(mr);
             bd = row_or_u32(bd);
             sd = row_sum_f64(sd);
+            if constexpr (LOC) {
+                i0 = row_min_u64(i0);
+                i1 = row_min_u64(ma_own == ma ? i1 : kNone);
+                i2 = row_min_u64(mr_own == mr ? i2 : kNone);
+                if (sl == 0 && S > 1) {
+                    Part2Idx* q = &p.part2_idx[(size_t)(j0 + jj) * S + m];
+                    st_coherent(&q->ix[IX_FIRST_MISMATCH], i0);
+                    st_coherent(&q->ix[IX_MAX_ABS], i1);
+                    st_coherent(&q->ix[IX_MAX_REL], i2);
+                }
+            }
             if constexpr (FF) {
                 nr = row_sum_u64(nr);
                 src = row_sum_f64(src);
@@ -905,6 +1101,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 else
                     write_record(&p.stats[table[j0 + jj].index], p.numel, mi, na, pi, ni, ma, mr, bd,
                                  sd, s_sr1);
+                if constexpr (LOC) write_loc(&p.loc[table[j0 + jj].index], i0, i1, i2);
             }
             if (g == 0) write_rejected(p, table);
             if (threadIdx.x == 0) st_coherent(&p.tickets1[(size_t)g * S + m], (uint64_t)0);
@@ -927,11 +1124,13 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         uint64_t mi = 0, na = 0, pi = 0, ni = 0, nr = 0;
         uint32_t ma = 0, mr = 0, bd = 0;
         double sd = 0.0, sr = 0.0, src = 0.0;
+        uint64_t i0 = kNone, i1 = kNone, i2 = kNone;  // positions
         const Part2* row = p.part2 + (size_t)(j0 + jj) * S;
         const double* rs = p.part2_ssr + (size_t)g * S;
         for (int q0 = sl; q0 < S; q0 += 64) {
             Part2 v[4];
             double w[4];
+            Part2Idx vi[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int q = q0 + 16 * u;
@@ -954,9 +1153,22 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                     v[u] = Part2{0, 0, 0, 0, 0u, 0u, 0u, 0u, 0.0, 0, 0.0};
                     w[u] = 0.0;
                 }
+                if constexpr (LOC) {
+                    const Part2Idx* e = &p.part2_idx[(size_t)(j0 + jj) * S + q];
+#pragma unroll
+                    for (int x = 0; x < IX_COUNT; ++x) vi[u].ix[x] = q < S ? ld_coherent(&e->ix[x]) : kNone;
+                }
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
+                if constexpr (LOC) {
+                    // (value, smallest index) pairs, before the maxima move
+                    i0 = min_u64(i0, vi[u].ix[IX_FIRST_MISMATCH]);
+                    i1 = v[u].maxabs > ma ? vi[u].ix[IX_MAX_ABS]
+                                          : v[u].maxabs == ma ? min_u64(i1, vi[u].ix[IX_MAX_ABS]) : i1;
+                    i2 = v[u].maxrel > mr ? vi[u].ix[IX_MAX_REL]
+                                          : v[u].maxrel == mr ? min_u64(i2, vi[u].ix[IX_MAX_REL]) : i2;
+                }
                 mi += v[u].mism;
                 na += v[u].nan;
                 pi += v[u].pinf;
@@ -972,11 +1184,18 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         na = row_sum_u64(na);
         pi = row_sum_u64(pi);
         ni = row_sum_u64(ni);
+        const uint32_t ma_own = ma, mr_own = mr;
         ma = row_max_u32(ma);
         mr = row_max_u32(mr);
         bd = row_or_u32(bd);
         sd = row_sum_f64(sd);
         sr = row_sum_f64(sr);
+        if constexpr (LOC) {
+            i0 = row_min_u64(i0);
+            i1 = row_min_u64(ma_own == ma ? i1 : kNone);
+            i2 = row_min_u64(mr_own == mr ? i2 : kNone);
+            if (sl == 0) write_loc(&p.loc[table[j0 + jj].index], i0, i1, i2);
+        }
         if constexpr (FF) {
             nr = row_sum_u64(nr);
             src = row_sum_f64(src);
@@ -1013,8 +1232,8 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
 // once more per round; more groups per round balance less well.
 // WIDE: the same kernel built for 5 waves per SIMD instead of 4 (only fp32
 // with 4 candidates per group, plain launches on large tensors; see
-// use_wide_kernel).
-template <int DT, int KG, bool FF, bool WIDE = false>
+// use_wide_kernel).  LOC: the variant that also finds the positions.
+template <int DT, int KG, bool FF, bool WIDE, bool LOC>
 __global__ __launch_bounds__(kThreads, WIDE ? 5 : min_waves(DT, KG)) void screen_kernel(
     ScreenParams p, InlineTable tab) {
     int id = blockIdx.x, g0 = 0, R = p.n_groups;
@@ -1027,11 +1246,11 @@ __global__ __launch_bounds__(kThreads, WIDE ? 5 : min_waves(DT, KG)) void screen
     }
     const int xcd = id & 7;
     const int slot = id >> 3;
-    screen_part<DT, KG, FF>(p, tab, g0 + slot % R, (slot / R) * 8 + xcd);
+    screen_part<DT, KG, FF, LOC>(p, tab, g0 + slot % R, (slot / R) * 8 + xcd);
 }
 
 __global__ void records_only_kernel(const CandEntry* uploaded, InlineTable tab, int table_inline,
-                                    int n_table, uint64_t numel, kb_stats* stats) {
+                                    int n_table, uint64_t numel, kb_stats* stats, kb_locate* loc) {
     const CandEntry* table = table_inline ? tab.e : uploaded;
     for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n_table; k += gridDim.x * blockDim.x) {
         if (table[k].index < 0) continue;  // padding
@@ -1042,77 +1261,84 @@ __global__ void records_only_kernel(const CandEntry* uploaded, InlineTable tab, 
             st.bitwise_equal = 1;
         }
         stats[table[k].index] = st;
+        if (loc) write_loc(&loc[table[k].index], kNone, kNone, kNone);
     }
 }
 
-template <int DT, int KG, bool FF>
+// Variants: 0 plain, 1 fail-fast, 2 positions.
+enum Variant : int { V_PLAIN = 0, V_FF, V_LOC };
+
+template <int DT, int KG, int V>
 hipError_t launch_kg(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
                      hipStream_t stream) {
+    constexpr bool FF = V == V_FF, LOC = V == V_LOC;
     const unsigned grid = (unsigned)plan.n_groups * (unsigned)plan.blocks_per_group;
-    if constexpr (DT == DT_F32 && KG == 4 && !FF) {
+    if constexpr (DT == DT_F32 && KG == 4 && V == V_PLAIN) {
         if (plan.wide) {
-            hipLaunchKernelGGL((screen_kernel<DT, KG, FF, true>), dim3(grid), dim3(kThreads), 0, stream,
-                               p, tab);
+            hipLaunchKernelGGL((screen_kernel<DT, KG, false, true, false>), dim3(grid), dim3(kThreads), 0,
+                               stream, p, tab);
             return hipGetLastError();
         }
     }
-    hipLaunchKernelGGL((screen_kernel<DT, KG, FF>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
+    hipLaunchKernelGGL((screen_kernel<DT, KG, FF, false, LOC>), dim3(grid), dim3(kThreads), 0, stream, p, tab);
     return hipGetLastError();
 }
 
-template <int DT, int KG, bool FF, bool WIDE = false>
+template <int DT, int KG, int V, bool WIDE = false>
 int occupancy_kg() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, screen_kernel<DT, KG, FF, WIDE>, kThreads, 0) !=
-        hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, screen_kernel<DT, KG, V == V_FF, WIDE, V == V_LOC>, kThreads, 0) != hipSuccess)
         return 0;
     return n;
 }
 
-template <int DT, bool FF>
+template <int DT, int V>
 int occupancy_dt(int kg) {
     switch (kg) {
-        case 1: return occupancy_kg<DT, 1, FF>();
-        case 2: return occupancy_kg<DT, 2, FF>();
-        case 4: return occupancy_kg<DT, 4, FF>();
-        case 8: return occupancy_kg<DT, 8, FF>();
-        default: return occupancy_kg<DT, 16, FF>();
+        case 1: return occupancy_kg<DT, 1, V>();
+        case 2: return occupancy_kg<DT, 2, V>();
+        case 4: return occupancy_kg<DT, 4, V>();
+        case 8: return occupancy_kg<DT, 8, V>();
+        default: return occupancy_kg<DT, 16, V>();
     }
 }
 
-template <int DT, bool FF>
+template <int DT, int V>
 hipError_t launch_dt(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
                      hipStream_t stream) {
     switch (plan.kg) {
-        case 1: return launch_kg<DT, 1, FF>(plan, p, tab, stream);
-        case 2: return launch_kg<DT, 2, FF>(plan, p, tab, stream);
-        case 4: return launch_kg<DT, 4, FF>(plan, p, tab, stream);
-        case 8: return launch_kg<DT, 8, FF>(plan, p, tab, stream);
-        default: return launch_kg<DT, 16, FF>(plan, p, tab, stream);
+        case 1: return launch_kg<DT, 1, V>(plan, p, tab, stream);
+        case 2: return launch_kg<DT, 2, V>(plan, p, tab, stream);
+        case 4: return launch_kg<DT, 4, V>(plan, p, tab, stream);
+        case 8: return launch_kg<DT, 8, V>(plan, p, tab, stream);
+        default: return launch_kg<DT, 16, V>(plan, p, tab, stream);
     }
 }
 
-template <bool FF>
-hipError_t launch_ff(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
-                     hipStream_t stream) {
+template <int V>
+hipError_t launch_v(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
+                    hipStream_t stream) {
     switch (plan.dtype) {
-        case DT_F32: return launch_dt<DT_F32, FF>(plan, p, tab, stream);
-        case DT_F16: return launch_dt<DT_F16, FF>(plan, p, tab, stream);
-        default: return launch_dt<DT_BF16, FF>(plan, p, tab, stream);
+        case DT_F32: return launch_dt<DT_F32, V>(plan, p, tab, stream);
+        case DT_F16: return launch_dt<DT_F16, V>(plan, p, tab, stream);
+        default: return launch_dt<DT_BF16, V>(plan, p, tab, stream);
     }
 }
 
-template <bool FF>
+template <int V>
 int occupancy(int dtype, int kg) {
-    return dtype == DT_F32 ? occupancy_dt<DT_F32, FF>(kg)
-                           : dtype == DT_F16 ? occupancy_dt<DT_F16, FF>(kg) : occupancy_dt<DT_BF16, FF>(kg);
+    return dtype == DT_F32 ? occupancy_dt<DT_F32, V>(kg)
+                           : dtype == DT_F16 ? occupancy_dt<DT_F16, V>(kg) : occupancy_dt<DT_BF16, V>(kg);
 }
 
 }  // namespace
 
 hipError_t launch_screen(const ScreenPlan& plan, const ScreenParams& p, const InlineTable& tab,
-                         bool fail_fast, hipStream_t stream) {
-    return fail_fast ? launch_ff<true>(plan, p, tab, stream) : launch_ff<false>(plan, p, tab, stream);
+                         bool fail_fast, bool loc, hipStream_t stream) {
+    if (fail_fast && loc) return hipErrorInvalidValue;
+    return fail_fast ? launch_v<V_FF>(plan, p, tab, stream)
+                     : loc ? launch_v<V_LOC>(plan, p, tab, stream) : launch_v<V_PLAIN>(plan, p, tab, stream);
 }
 
 __global__ void zero_fill_kernel(uint4* dst, uint64_t n16) {
@@ -1131,27 +1357,30 @@ hipError_t launch_zero_fill(void* dst, size_t n, hipStream_t stream) {
     return hipGetLastError();
 }
 
-int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide) {
+int screen_blocks_per_cu(int dtype, int kg, bool fail_fast, bool wide, bool loc) {
     // The occupancy of a kernel does not change during the process.
-    static int cache[3][3][5] = {};  // value + 1, 0 = not queried yet
+    static int cache[4][3][5] = {};  // value + 1, 0 = not queried yet
     const int ki = kg == 1 ? 0 : kg == 2 ? 1 : kg == 4 ? 2 : kg == 8 ? 3 : 4;
     const int di = dtype == DT_F32 ? 0 : dtype == DT_F16 ? 1 : 2;
-    wide = wide && use_wide_kernel(dtype, kg, fail_fast, ~0ull);
-    int* slot = &cache[fail_fast ? 1 : wide ? 2 : 0][di][ki];
+    if (fail_fast && loc) return 0;
+    wide = wide && use_wide_kernel(dtype, kg, fail_fast, ~0ull, loc);
+    int* slot = &cache[fail_fast ? 1 : wide ? 2 : loc ? 3 : 0][di][ki];
     int v = __atomic_load_n(slot, __ATOMIC_RELAXED) - 1;
     if (v < 0) {
-        v = wide ? occupancy_kg<DT_F32, 4, false, true>()
-                 : fail_fast ? occupancy<true>(dtype, kg) : occupancy<false>(dtype, kg);
+        v = wide ? occupancy_kg<DT_F32, 4, V_PLAIN, true>()
+                 : fail_fast ? occupancy<V_FF>(dtype, kg) : loc ? occupancy<V_LOC>(dtype, kg)
+                                                                : occupancy<V_PLAIN>(dtype, kg);
         __atomic_store_n(slot, v + 1, __ATOMIC_RELAXED);
     }
     return v;
 }
 
 hipError_t launch_records_only(const CandEntry* table, const InlineTable& tab, int table_inline,
-                               int n_table, uint64_t numel, kb_stats* stats, hipStream_t stream) {
+                               int n_table, uint64_t numel, kb_stats* stats, kb_locate* loc,
+                               hipStream_t stream) {
     const int grid = (n_table + 255) / 256;
     hipLaunchKernelGGL(records_only_kernel, dim3(grid), dim3(256), 0, stream, table, tab,
-                       table_inline, n_table, numel, stats);
+                       table_inline, n_table, numel, stats, loc);
     return hipGetLastError();
 }
 

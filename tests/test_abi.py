@@ -270,6 +270,38 @@ def test_large_calls_need_a_host_table(L):
     assert "workspace of 16 bytes" in kb.kb_last_error()
 
 
+def test_positions_argument_errors(L):
+    """kb_screen_ex with positions (opts.d_loc): its own workspace size, and
+    the refusals that come before any device work."""
+    for dt in (kb.KB_F32, kb.KB_F16, kb.KB_BF16):
+        for n, numel in ((1, 1), (16, 1 << 24), (300, 1 << 18), (128, 1 << 32)):
+            plain = kb.kb_screen_workspace_bytes(n, numel, dt)
+            pos = kb.kb_screen_positions_workspace_bytes(n, numel, dt)
+            assert plain > 0 and pos > plain and pos % 256 == 0, (dt, n, numel)
+    assert kb.kb_screen_positions_workspace_bytes(0, 64, kb.KB_F32) == 0
+    assert kb.kb_screen_positions_workspace_bytes(4, 64, kb.KB_U32) == 0
+    ref = desc(0x10000, kb.KB_F32, (4096,))
+    cands = [desc(0x20000 + 0x4000 * k, kb.KB_F32, (4096,)) for k in range(3)]
+    arr = (kb.KbTensor * 3)(*cands)
+    pos = kb.kb_screen_positions_workspace_bytes(3, 4096, kb.KB_F32)
+    plain = kb.kb_screen_workspace_bytes(3, 4096, kb.KB_F32)
+
+    def ex(loc, ws_bytes=pos, flags=0):
+        opts = kb.KbScreenOpts(None, 0, loc)
+        return kb.lib().kb_screen_ex(ctypes.byref(ref), arr, 3, 1e-5, 1e-5, flags, 0x100000, ws_bytes,
+                                     0x200000, ctypes.byref(opts), None)
+
+    assert ex(0x300000, flags=kb.KB_FAIL_FAST) == kb.KB_ERR_INVALID_ARG
+    assert "KB_FAIL_FAST" in kb.kb_last_error()
+    assert ex(0x300000, ws_bytes=plain) == kb.KB_ERR_WORKSPACE
+    assert ex(0x300008) == kb.KB_ERR_ALIGNMENT
+    # multi-output calls take no positions
+    o = kb.KbScreenOpts(None, 0, 0x300000)
+    at = (ctypes.c_float * 1)(1e-5)
+    assert kb.lib().kb_screen_multi(ctypes.byref(ref), 1, arr, 3, at, at, 0, 0x100000, 1 << 30, 0x200000,
+                                    ctypes.byref(o), None) == kb.KB_ERR_INVALID_ARG
+
+
 def test_missing_library_fails_loudly(monkeypatch):
     monkeypatch.setattr(kb, "_lib", None)
     monkeypatch.setattr(kb, "LIB_PATH", "/nonexistent/libkb.so")

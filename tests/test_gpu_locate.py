@@ -1,8 +1,11 @@
-"""Parity of the position search (kb_screen_locate) with the oracle (GPU).
+"""Parity of the position search with the oracle (GPU), in both forms: the
+separate pass (kb_screen, then kb_screen_locate) and the positions found in
+the screening pass itself (kb_screen_ex with opts.d_loc).
 
-The library screens, then locates, on the device; the oracle's kbo_locate
-runs on host copies of the same bytes with the oracle's own maxima (equal to
-the library's by the screening parity).  Every position must be equal."""
+The oracle's kbo_locate runs on host copies of the same bytes with the
+oracle's own maxima (equal to the library's by the screening parity).  Every
+position must be equal, and the records of the screening pass with
+positions must match the oracle's like those of the plain pass."""
 import numpy as np
 import pytest
 import torch
@@ -10,7 +13,8 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import dtype_name, ensure_built, oracle_workload, storage
+from tests.helpers import (assert_records_match, dtype_name, ensure_built, oracle_records, oracle_workload,
+                           storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -31,13 +35,17 @@ def to_dev(arr, dt, dev):
     return bits.view(TORCH_DT[dt])
 
 
-def oracle_positions(ref, cands, atol, rtol, flags=0):
+def oracle_positions(ref, cands, atol, rtol, flags=0, records=None):
+    """The oracle's positions of every candidate (and its records, appended
+    to `records` when given)."""
     dt = dtype_name(ref)
     r = storage(ref)
     out = []
     for c in cands:
         cs = storage(c)
         s = oracle.screen(r, cs, dt, atol, rtol, flags)
+        if records is not None:
+            records.append(s)
         fm, ai, ri = oracle.locate(r, cs, dt, atol, rtol, s["max_abs_err"], s["max_rel_err"], flags)
         out.append({"first_mismatch": fm, "max_abs_index": ai, "max_rel_index": ri})
     return out
@@ -47,12 +55,25 @@ def say(*a):
     print(*a, flush=True)
 
 
-def check(ref, cands, atol, rtol, flags=0, label=""):
+def check(ref, cands, atol, rtol, flags=0, label="", want=None):
+    """Both forms against the oracle's positions (computed here unless given)."""
+    say("positions", label, len(cands), tuple(ref.shape), ref.dtype)
     recs, locs = kb.locate(ref, cands, atol, rtol, flags)
-    want = oracle_positions(ref, cands, atol, rtol, flags)
-    for k, (g, w) in enumerate(zip(locs, want)):
-        assert g == w, (label, k, g, w)
-    return locs
+    frecs, flocs = kb.screen_positions(ref, cands, atol, rtol, flags)
+    orecs = []
+    if want is None:
+        want = oracle_positions(ref, cands, atol, rtol, flags, orecs)
+    for k, (g, f, w) in enumerate(zip(locs, flocs, want)):
+        assert g == w, (label, "separate pass", k, g, w)
+        assert f == w, (label, "screening pass", k, f, w)
+    # the records of the pass with positions: the oracle's, to the same bar as
+    # the plain pass, and every exact field equal to the plain pass's
+    if orecs:
+        assert_records_match(frecs, orecs, label + " (records with positions)")
+    for a, b in zip(frecs, recs):
+        assert {f: a[f] for f in a if f not in ("sum_sq_diff", "sum_sq_ref", "rel_l2")} == \
+            {f: b[f] for f in b if f not in ("sum_sq_diff", "sum_sq_ref", "rel_l2")}, (label, a, b)
+    return flocs
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
@@ -190,6 +211,11 @@ def test_indices_beyond_32_bits(dev):
     assert r["sum_sq_diff"] == 16.0 + 64.0 + 64.0, r
     assert 0.99 * n < r["sum_sq_ref"] < 1.01 * n, r
     assert locs[0] == {"first_mismatch": low, "max_abs_index": high, "max_rel_index": high}, locs
+    say("indices beyond 32 bits, positions in the screening pass")
+    frecs, flocs = kb.screen_positions(ref, [cand], 1e-2, 1e-2)
+    assert flocs == locs, (flocs, locs)
+    assert {f: v for f, v in frecs[0].items() if f != "sum_sq_ref"} == \
+        {f: v for f, v in r.items() if f != "sum_sq_ref"}, (frecs[0], r)
     # fail-fast: a passing copy is read in full (its element count, summed
     # over work-groups, is past 2^32) and its record is the plain one
     same = ref.clone()
@@ -206,7 +232,80 @@ def test_rejected_and_identical(dev):
     r = torch.randn(5000, device=dev)
     cands = [r.clone(), None, r.to(torch.float16), r.clone()]
     cands[3][4321] = float("nan")
-    recs, locs = kb.locate(r, cands, 1e-5, 1e-5)
-    assert locs[0] == {"first_mismatch": -1, "max_abs_index": -1, "max_rel_index": -1}
-    assert locs[1] == locs[0] and locs[2] == locs[0]
-    assert locs[3] == {"first_mismatch": 4321, "max_abs_index": -1, "max_rel_index": -1}
+    for fn in (kb.locate, kb.screen_positions):
+        recs, locs = fn(r, cands, 1e-5, 1e-5)
+        assert locs[0] == {"first_mismatch": -1, "max_abs_index": -1, "max_rel_index": -1}
+        assert locs[1] == locs[0] and locs[2] == locs[0]
+        assert locs[3] == {"first_mismatch": 4321, "max_abs_index": -1, "max_rel_index": -1}
+
+
+def test_positions_without_elements(dev):
+    """No element to read (an empty reference, or every candidate rejected):
+    the records come from the table alone and every position is -1."""
+    none = {"first_mismatch": -1, "max_abs_index": -1, "max_rel_index": -1}
+    e = torch.empty(0, device=dev)
+    recs, locs = kb.screen_positions(e, [e.clone(), None], 1e-5, 1e-5)
+    assert locs == [none, none] and recs[0]["passed"] == 1 and recs[1]["passed"] == 0
+    r = torch.randn(1000, device=dev)
+    recs, locs = kb.screen_positions(r, [None, r.to(torch.float16)], 1e-5, 1e-5)
+    assert locs == [none, none] and not any(x["passed"] for x in recs)
+
+
+def test_positions_many_candidates_host_table(dev):
+    """More candidates than travel in the kernel arguments (the launch table
+    in pinned host memory), rejected ones among them, with ties planted."""
+    rng = np.random.default_rng(77)
+    n = 512 * 9 + 100
+    r32 = rng.uniform(-1.0, 1.0, n).astype(np.float32)
+    ref = to_dev(r32, "f32", dev)
+    cands, host = [], []
+    for k in range(kb.KB_INLINE_CANDS + 72):
+        if k % 41 == 5:
+            cands.append(None)
+            continue
+        c = r32.copy()
+        for p in rng.integers(0, n, 1 + k % 4):
+            c[p] = r32[p] + 0.5
+        c += rng.standard_normal(n).astype(np.float32) * np.float32(1e-6 * (k % 3))
+        cands.append(to_dev(c, "f32", dev))
+    live = [c for c in cands if c is not None]
+    want = oracle_positions(ref, live, 1e-4, 1e-4)
+    recs, locs = kb.screen_positions(ref, cands, 1e-4, 1e-4)
+    it = iter(want)
+    for k, (c, l) in enumerate(zip(cands, locs)):
+        w = {"first_mismatch": -1, "max_abs_index": -1, "max_rel_index": -1} if c is None else next(it)
+        assert l == w, (k, l, w)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_positions_many_super_groups(dev, dt):
+    """One candidate group over 2^24 elements: many stripes, combined in two
+    levels, with the maxima tied in stripes far apart (the smallest index
+    must survive both levels) and the first mismatch late."""
+    n = 1 << 24
+    rng = np.random.default_rng(5)
+    r32 = rng.uniform(1.0, 2.0, n).astype(np.float32)
+    cands = [r32.copy() for _ in range(3)]
+    for p in (n - 1000, n // 3 + 17, n // 2):
+        cands[0][p] = r32[p] + 0.75
+    cands[1][n - 600] = 0.0
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cd = [to_dev(CONV[dt](c), dt, dev) for c in cands]
+    check(ref, cd, 1e-2, 1e-2, 0, "%s many super-groups" % dt)
+
+
+def test_screener_positions_repeated(dev):
+    """Repeated launches of one Screener with positions: the workspace is
+    left clean by each call, and every launch gives the same records and
+    positions."""
+    w, _ = oracle_workload("c2", dev, seed=1, scale=1 / 64, K=16)
+    want = oracle_positions(w.ref, w.cands, w.atol, w.rtol)
+    s = kb.Screener(w.ref, w.cands, w.atol, w.rtol, positions=True)
+    first = None
+    for _ in range(3):
+        s.launch()
+        s.read()
+        recs = s.records()
+        assert s.positions() == want
+        first = first or recs
+        assert recs == first
