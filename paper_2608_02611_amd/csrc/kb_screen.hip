@@ -222,13 +222,17 @@ __device__ __forceinline__ void opaque(float& x) { asm volatile("" : "+v"(x)); }
 // was measured to cost far more than it saves: every work-group contends
 // for the same few words.)
 //
-// The quotients of one lane's elements that pass the filter (0 if none).
-// GUARD: the lane may be in the underflow case, so the sign of d - O a is
-// taken in binary64 (the product of two binary32 values is exact there and
-// one rounding keeps the sign); otherwise the binary32 residual is exact.
+// The largest quotient of one lane's elements that pass the filter (0 if
+// none), and in `slot` the first slot that holds it (kE if none; a slot
+// holding a quotient > O always passes, so this is the lane's first element
+// of that quotient).  GUARD: the lane may be in the underflow case, so the
+// sign of d - O a is taken in binary64 (the product of two binary32 values is
+// exact there and one rounding keeps the sign); otherwise the binary32
+// residual is exact.
 template <bool GUARD>
-__device__ __forceinline__ float rel_quotients(const float s[kE], const float r[kE], float O) {
+__device__ __forceinline__ float rel_quotients(const float s[kE], const float r[kE], float O, uint32_t& slot) {
     float qm = 0.f;
+    slot = kE;
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
         const float d = fabsf(s[i]);
@@ -239,7 +243,13 @@ __device__ __forceinline__ float rel_quotients(const float s[kE], const float r[
         if constexpr (GUARD) opaque(a);
         const bool pass = GUARD ? __builtin_fma(-(double)O, (double)a, (double)d) > 0.0
                                 : fmaf(-O, a, d) > 0.f;
-        if (pass) qm = fmaxf(qm, d / a);
+        if (pass) {
+            const float q = d / a;
+            if (q > qm) {
+                qm = q;
+                slot = i;
+            }
+        }
     }
     return qm;
 }
@@ -255,11 +265,13 @@ struct NonFinite {
 // max-rel O and non-finite counts, and adds the lane's binary64 squared
 // differences to its LDS slot.  LOC: a rise of the lane's max abs error
 // also records `code` (the chunk) in achunk.
+// LOC also gives the lane's largest quotient in qm_out and its first slot in
+// qslot (kE if no quotient is positive).
 template <int DT, bool LOC>
 __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_in[kE], float atol,
                                             float rtol, bool equal_nan, double* ssd_slot,
                                             uint32_t& mism, uint32_t& amax, uint32_t& achunk, uint32_t code,
-                                            float& O, NonFinite& nf) {
+                                            float& O, NonFinite& nf, float& qm_out, uint32_t& qslot) {
     float r[kE];
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
@@ -269,6 +281,7 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
     uint32_t nm = 0, nnan = 0, npinf = 0, nninf = 0;
     float ma = 0.f, qm = 0.f;
     double sd = 0.0;
+    qslot = kE;
 #pragma unroll
     for (int i = 0; i < kE; ++i) {
         const float c = elem<DT>(cand, i);
@@ -284,7 +297,15 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
         const bool match = (c == ri) || (d <= tol) || (equal_nan && cnan && __builtin_isnan(ri));
         nm += popc(ballot(!match));
         ma = fmaxf(ma, d);       // NaN differences are ignored
-        qm = fmaxf(qm, d / a);   // so are 0/0 and inf/inf
+        if constexpr (LOC) {
+            const float q = d / a;
+            if (q > qm) {        // NaN quotients (0/0, inf/inf) never are
+                qm = q;
+                qslot = i;
+            }
+        } else {
+            qm = fmaxf(qm, d / a);   // so are 0/0 and inf/inf
+        }
         if (rfin && __builtin_isfinite(c)) sd = __builtin_fma((double)d, (double)d, sd);
     }
     atomicAdd(ssd_slot, sd);
@@ -298,18 +319,21 @@ __device__ __forceinline__ void exact_chunk(const Raw<DT>& cand, const float r_i
         amax = max(amax, __float_as_uint(ma));
     }
     O = fmaxf(O, wave_max_f(qm));
+    qm_out = qm;
     nf.nan += nnan;
     nf.pinf += npinf;
     nf.ninf += nninf;
 }
 
 // ----------------------------------------------------------- positions ---
-// The fused position search (LOC) keeps, per candidate: the wave's first
-// mismatching element (found in the first chunk that has one: a wave visits
-// its chunks in increasing index order), the chunk in which each lane's
-// running max abs error last rose (strictly, so its first occurrence), and the
-// element of the wave's own max rel error (found when it rises).  All rare
-// paths except the max-abs chunk, two more instructions per chunk.
+// The position search inside the screening pass (LOC) keeps, per wave and
+// candidate: the first chunk whose count shows a mismatch (a wave visits its
+// chunks in increasing index order), searched for the element after the
+// loop; the chunk in which each lane's running max abs error last rose
+// (strictly, so its first occurrence), re-read after the loop; and the element
+// of the wave's own max rel error, found when it rises.  In the common path
+// only the max-abs chunk costs instructions (a compare and two selects in
+// place of a max).
 constexpr uint64_t kNone = ~0ull;
 
 // Element offset within the chunk of slot i of `lane` (fp32: elements
@@ -339,17 +363,6 @@ __device__ __forceinline__ uint32_t lane_first_mismatch(const Raw<DT>& cand, con
     return slot;
 }
 
-// The lane's first slot whose quotient fl(|c - r| / |r|) equals q (q > 0), kE
-// if none.
-template <int DT>
-__device__ __forceinline__ uint32_t lane_rel_slot(const Raw<DT>& cand, const float r[kE], float q) {
-    uint32_t slot = kE;
-#pragma unroll
-    for (int i = kE - 1; i >= 0; --i)
-        if (fabsf(elem<DT>(cand, i) - r[i]) / fabsf(r[i]) == q) slot = i;
-    return slot;
-}
-
 // The lane's first slot whose |c - r| has the bits m, kE if none.
 template <int DT>
 __device__ __forceinline__ uint32_t lane_abs_slot(const Raw<DT>& cand, const Raw<DT>& ref, uint32_t m) {
@@ -358,6 +371,11 @@ __device__ __forceinline__ uint32_t lane_abs_slot(const Raw<DT>& cand, const Raw
     for (int i = kE - 1; i >= 0; --i)
         if (__float_as_uint(fabsf(elem<DT>(cand, i) - elem<DT>(ref, i))) == m) slot = i;
     return slot;
+}
+
+// A wave's position (wave-uniform v) into its LDS slot.
+__device__ __forceinline__ void set_idx(uint64_t* slot, uint64_t v, int lane) {
+    if (lane == 0) *slot = v;
 }
 
 // Raises the work-group's max-rel value of one candidate (rare; O >= 0, so
@@ -500,16 +518,20 @@ __device__ __forceinline__ void clear_ff_words(const ScreenParams& p, int j0, in
 // LOC: the variant that also finds each candidate's positions (p.loc): the
 // first mismatching element and the first elements at which the max abs and
 // max rel errors are reached.  Per wave and candidate: the first mismatch is
-// searched in the first chunk whose count shows one (the wave's chunks come
-// in increasing index order, so later ones can only be larger); each lane
-// keeps the chunk in which its max abs error last rose (strictly: the first
-// chunk that holds its maximum), and at the end the lanes holding the wave's
-// maximum re-read that chunk for the element; the max-rel element is found
-// in the chunk that raises O.  Waves then do not share O (a shared value
-// would filter out elements that tie it at smaller indices).  The positions
-// are combined like the maxima (the smallest index among the parts that
-// hold the maximum) in the same fixed orders, so they are the smallest
-// qualifying indices whatever the launch.
+// searched, after the loop, in the first chunk whose count showed one (the
+// wave's chunks come in increasing index order, so later ones can only be
+// larger); each lane keeps the chunk in which its max abs error last rose
+// (strictly: the first chunk that holds its maximum), and after the loop the
+// lanes holding the wave's maximum re-read that chunk for the element; the
+// max-rel element is found in the chunk that raises the wave's own maximum.
+// The max-rel filter still uses the work-group's shared value, lowered by
+// one binary32 step so that elements tying it pass (see the fast path).  A
+// wave's own maximum then skips values below the shared one, but every
+// element that holds the final maximum passes the filter in its wave, and
+// the first of them in the wave is recorded.  The positions are combined
+// like the maxima (the smallest index among the parts that hold the
+// maximum) in the same fixed orders, so they are the smallest qualifying
+// indices whatever the launch.
 template <int DT, int KG, bool FF, bool LOC>
 __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineTable& tab, const int g,
                                             const int stripe) {
@@ -549,20 +571,24 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     uint32_t amax[KG];  // lane max abs error (binary32 bits, non-negative)
     uint32_t orel[KG];  // wave-uniform max rel error O (binary32 bits, non-negative)
     uint32_t bitdiff = 0u;  // bit j: candidate j differs somewhere in this wave's range
-    uint64_t fm[KG];        // positions: the wave's first mismatch (wave-uniform)
-    uint64_t ridx[KG];      // positions: the element of O (wave-uniform)
+    // positions: bit j set once the wave's first mismatch of candidate j is
+    // known (the index itself and that of O live in s_idx: they change
+    // rarely, and registers are short)
+    uint32_t fm_found = 0u;
     uint32_t achunk[KG];    // positions: the chunk of the lane's max abs error
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
         mism[j] = 0u;
         amax[j] = 0u;
         orel[j] = 0u;
-        fm[j] = kNone;
-        ridx[j] = kNone;
         achunk[j] = 0u;
         s_ssd[j][threadIdx.x] = 0.0;
     }
     if (lane < KG) s_nf[wave][lane] = NonFinite{0u, 0u, 0u};
+    if (LOC && lane < KG) {
+#pragma unroll
+        for (int x = 0; x < IX_COUNT; ++x) s_idx[wave][lane][x] = kNone;
+    }
     if (threadIdx.x < KG) s_rel[threadIdx.x] = 0u;
     if (FF && threadIdx.x < KG) s_told[threadIdx.x] = 0u;
     double ssr = 0.0;
@@ -687,8 +713,19 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 for (int w = 0; w < Raw<DT>::kWords; ++w) x |= cr.w[w] ^ rraw.w[w];
                 if (ballot(x != 0u)) bitdiff |= 1u << j;
             }
-            // fast path
-            const float O = __uint_as_float(orel[j]);
+            // fast path.  O: the max-rel filter's threshold.  Plain: the wave's
+            // max, raised by the work-group's shared value.  Positions: the
+            // larger of the wave's own max (Own) and the binary32 value just
+            // below the shared value -- an element whose quotient ties the
+            // shared value must still pass, as its index may be the smallest
+            // (a quotient that rounds to t is above the value below t).
+            uint32_t obits = orel[j];
+            if constexpr (LOC) {
+                const uint32_t t = __builtin_amdgcn_readfirstlane(s_rel[j]);
+                obits = max(obits, t != 0u ? t - 1u : 0u);
+            }
+            const float O = __uint_as_float(obits);
+            const float Own = __uint_as_float(orel[j]);
             float s[kE], y[kE];
             uint32_t nmatch = 0;
             float tmax = 0.f, acc = 0.f;
@@ -705,29 +742,34 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             for (int i = 1; i < kE; ++i) ymax = fmaxf(ymax, y[i]);
             if (ballot(!(acc < __builtin_inff()))) {
                 // NaN, infinity or a squared difference beyond binary32
-                float o = O;
+                float o = Own;
                 const uint32_t mism0 = mism[j];
+                float qm;
+                uint32_t qs;
                 exact_chunk<DT, LOC>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
-                                     amax[j], achunk[j], (uint32_t)chunk, o, s_nf[wave][j]);
-                if (o > O) {
+                                     amax[j], achunk[j], (uint32_t)chunk, o, s_nf[wave][j], qm, qs);
+                if (o > Own) {
                     orel[j] = __float_as_uint(o);
                     if constexpr (LOC)
-                        ridx[j] = ebase + wave_min_u32(slot_offset<DT>(lane, lane_rel_slot<DT>(cr, r, o)));
-                    else
-                        publish_rel(&s_rel[j], o, lane);
+                        set_idx(&s_idx[wave][j][IX_MAX_REL],
+                                ebase + wave_min_u32(qm == o ? slot_offset<DT>(lane, qs) : 0xFFFFFFFFu), lane);
+                    publish_rel(&s_rel[j], o, lane);
                 }
                 if constexpr (LOC) {
-                    if (fm[j] == kNone && mism[j] != mism0)
-                        fm[j] = ebase + wave_min_u32(slot_offset<DT>(
-                                            lane, lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan)));
+                    // the wave's first mismatching chunk (searched after the loop)
+                    if (!((fm_found >> j) & 1u) && mism[j] != mism0) {
+                        set_idx(&s_idx[wave][j][IX_FIRST_MISMATCH], chunk, lane);
+                        fm_found |= 1u << j;
+                    }
                 }
                 continue;
             }
             mism[j] += (uint32_t)kChunk - nmatch;
             if constexpr (LOC) {
-                if (fm[j] == kNone && nmatch != (uint32_t)kChunk)
-                    fm[j] = ebase + wave_min_u32(slot_offset<DT>(
-                                        lane, lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan)));
+                if (!((fm_found >> j) & 1u) && nmatch != (uint32_t)kChunk) {
+                    set_idx(&s_idx[wave][j][IX_FIRST_MISMATCH], chunk, lane);
+                    fm_found |= 1u << j;
+                }
                 if (__float_as_uint(tmax) > amax[j]) {
                     amax[j] = __float_as_uint(tmax);
                     achunk[j] = (uint32_t)chunk;
@@ -756,18 +798,19 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
             const bool rel = fmaxf(ymax, hz) > 0.f;
             if (ballot(rel)) {
                 float qm = 0.f;
+                uint32_t qs = kE;
                 if (kGuard<DT> && ballot(hz > 0.f)) {
-                    if (rel) qm = rel_quotients<true>(s, r, O);
+                    if (rel) qm = rel_quotients<true>(s, r, O, qs);
                 } else {
-                    if (rel) qm = rel_quotients<false>(s, r, O);
+                    if (rel) qm = rel_quotients<false>(s, r, O, qs);
                 }
                 const float q = wave_max_f(qm);
-                if (q > O) {
+                if (q > Own) {
                     orel[j] = __float_as_uint(q);
                     if constexpr (LOC)
-                        ridx[j] = ebase + wave_min_u32(slot_offset<DT>(lane, lane_rel_slot<DT>(cr, r, q)));
-                    else
-                        publish_rel(&s_rel[j], q, lane);
+                        set_idx(&s_idx[wave][j][IX_MAX_REL],
+                                ebase + wave_min_u32(qm == q ? slot_offset<DT>(lane, qs) : 0xFFFFFFFFu), lane);
+                    publish_rel(&s_rel[j], q, lane);
                 }
             }
         }
@@ -820,6 +863,9 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
     // elements 1..7 compare 0 with 0, which changes no statistic).
     uint32_t n_tail = 0u;  // tail elements this wave compared (for every live candidate)
     const uint64_t tfirst = n_chunks * kChunk;
+    // positions: candidates whose first mismatch was found in a chunk (the
+    // slot holds the chunk number until it is searched, below)
+    const uint32_t fm_chunked = fm_found;
     if (stripe == 0) {
         const uint64_t first = tfirst;
         for (uint64_t base = first; base < p.numel; base += kThreads) {
@@ -853,18 +899,47 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 const uint32_t mism0 = mism[j];
                 // positions: tail element e is slot 0 of its lane; the max-abs
                 // chunk code of the tail is n_chunks + (base - first) / 256
+                float qm;
+                uint32_t qs;
                 exact_chunk<DT, LOC>(cr, r, atol, rtol, equal_nan, &s_ssd[j][threadIdx.x], mism[j],
                                      amax[j], achunk[j], (uint32_t)(n_chunks + (base - first) / kThreads), o,
-                                     s_nf[wave][j]);
+                                     s_nf[wave][j], qm, qs);
                 orel[j] = __float_as_uint(o);
                 if constexpr (LOC) {
-                    if (o > o0) ridx[j] = wave_min_u64(lane_rel_slot<DT>(cr, r, o) < (uint32_t)kE ? e : kNone);
-                    if (fm[j] == kNone && mism[j] != mism0)
-                        fm[j] = wave_min_u64(lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan) < (uint32_t)kE
+                    // (the lane's one element is slot 0)
+                    if (o > o0) set_idx(&s_idx[wave][j][IX_MAX_REL], wave_min_u64(qm == o ? e : kNone), lane);
+                    if (!((fm_found >> j) & 1u) && mism[j] != mism0) {
+                        set_idx(&s_idx[wave][j][IX_FIRST_MISMATCH],
+                                wave_min_u64(lane_first_mismatch<DT>(cr, r, atol, rtol, equal_nan) < (uint32_t)kE
                                                  ? e
-                                                 : kNone);
+                                                 : kNone),
+                                lane);
+                        fm_found |= 1u << j;
+                    }
                 }
             }
+        }
+    }
+
+    // Positions: the first mismatch of each candidate whose first
+    // mismatching chunk of this wave is known, searched in that chunk.
+    if constexpr (LOC) {
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+            if (j >= kg || !((fm_chunked >> j) & 1u)) continue;
+            const uint64_t c = ((uint64_t)__builtin_amdgcn_readfirstlane(
+                                   (uint32_t)(s_idx[wave][j][IX_FIRST_MISMATCH] >> 32))
+                               << 32) |
+                               __builtin_amdgcn_readfirstlane((uint32_t)s_idx[wave][j][IX_FIRST_MISMATCH]);
+            const uint64_t cb = c * chunk_bytes<DT>();
+            const Raw<DT> cv = load_chunk<DT, false>(uniform_ptr(cand[j] + cb), off);
+            const Raw<DT> rv = load_chunk<DT, false>(uniform_ptr(ref + cb), off);
+            float rf[kE];
+#pragma unroll
+            for (int i = 0; i < kE; ++i) rf[i] = elem<DT>(rv, i);
+            const uint32_t m =
+                wave_min_u32(slot_offset<DT>(lane, lane_first_mismatch<DT>(cv, rf, atol, rtol, equal_nan)));
+            set_idx(&s_idx[wave][j][IX_FIRST_MISMATCH], c * kChunk + m, lane);
         }
     }
 
@@ -893,11 +968,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 }
                 ai = wave_min_u64(mine);
             }
-            if (lane == 0) {
-                s_idx[wave][j][IX_FIRST_MISMATCH] = fm[j];
-                s_idx[wave][j][IX_MAX_ABS] = ai;
-                s_idx[wave][j][IX_MAX_REL] = ridx[j];
-            }
+            if (lane == 0) s_idx[wave][j][IX_MAX_ABS] = ai;
         }
         if (lane == 0) {
             WaveOut& o = s_out[wave][j];

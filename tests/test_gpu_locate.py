@@ -147,6 +147,30 @@ def test_max_rel_filter_near_misses(dev):
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_maxima_tied_in_every_chunk(dev, dt):
+    """One element per chunk (at a drawn slot) with the same abs and rel
+    error, so every wave meets the maximum in its first chunk and the waves
+    of a work-group share it at once: the wave holding the smallest index
+    must still record it (in the screening pass the shared value filters the
+    other elements)."""
+    n_chunks = 300
+    n = 512 * n_chunks + 33
+    rng = np.random.default_rng(23)
+    r32 = np.ones(n, np.float32)
+    c32 = r32.copy()
+    hits = np.arange(n_chunks) * 512 + rng.integers(0, 512, n_chunks)
+    c32[hits] = 1.5
+    # a larger abs error, but a smaller rel one, late in the array
+    r32[n - 700] = 4.0
+    c32[n - 700] = 5.0
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cand = to_dev(CONV[dt](c32), dt, dev)
+    locs = check(ref, [cand, ref.clone()], 1e-3, 1e-3, 0, "%s ties" % dt)
+    assert locs[0] == {"first_mismatch": int(hits[0]), "max_abs_index": n - 700,
+                       "max_rel_index": int(hits[0])}, locs
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_non_finite_references(dev, dt):
     """References with +-inf and NaN scattered through many chunks.  The
     cheap pass sends every such element to the exact pass, which applies the
