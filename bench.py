@@ -401,19 +401,21 @@ def rung_stats_leg(dev, kb, synth, C=1024, S=3, N=60):
             "promoted": int(prom.sum().item())}
 
 
-def positions_leg(kb, w, reps=20):
+def positions_leg(kb, w, reps=20, rounds=3):
     """The screen with positions found in the same pass (kb_screen_ex with
     opts.d_loc) against the plain screen, back to back on one stream: kernel
-    time per launch of each, and the positions, which must equal those of
-    the separate pass (kb_screen_locate)."""
+    time per launch of each (the best of `rounds` alternating measurements),
+    and the positions, which must equal those of the separate pass
+    (kb_screen_locate)."""
     import torch
     st = torch.cuda.Stream()
     plain = kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st)
     withpos = kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st, positions=True)
     warm_device(plain.launch, 0.1)
-    plain_ms = event_time(plain.launch, reps, st)
-    warm_device(withpos.launch, 0.1)
-    pos_ms = event_time(withpos.launch, reps, st)
+    plain_ms = pos_ms = float("inf")
+    for _ in range(rounds):
+        plain_ms = min(plain_ms, event_time(plain.launch, reps, st))
+        pos_ms = min(pos_ms, event_time(withpos.launch, reps, st))
     plain.read()
     withpos.read()
     precs, wrecs = plain.records(), withpos.records()

@@ -16,15 +16,22 @@
  *
  * Three subsystems:
  *   kb_gen_inputs   seeded inputs: a Philox4x32-10 counter-based stream
- *                   (Salmon et al., SC'11) mapped to u32, uniform or normal
- *                   values (fp32, fp16, bf16);
+ *                   (Salmon et al., SC'11) mapped to u32, uniform, normal or
+ *                   Student-t values (fp32, fp16, bf16), and the derived
+ *                   inputs of the screening workloads (kb_gen_softmax_rows,
+ *                   kb_gen_indices, kb_gen_perturb, kb_gen_scatter);
  *   kb_screen       policy gate + one pass over the reference and the K
  *                   candidates computing, per candidate, the mismatch count
  *                   under |c - r| <= atol + rtol*|r|, max abs and max rel
  *                   error, NaN / +Inf / -Inf counts, a bitwise-identity flag
- *                   and the relative L2 error;
+ *                   and the relative L2 error (kb_screen_ex: also the
+ *                   positions of the first mismatch and of the maxima);
  *   kb_screen_stats reads the per-candidate records back and gives the
  *                   pass/fail verdict of each candidate.
+ * Around them: the separate position pass (kb_screen_locate), multi-output
+ * candidates (kb_screen_multi), the rung benchmarker's statistics and
+ * promotion decision (kb_rung_stats, kb_rung_promote, kb_rung_survival), and
+ * kb_screen_noalloc for callers that cannot allocate.
  *
  * Conventions
  *   - Every function is extern "C" and returns an int status: KB_OK (0) or a
@@ -176,8 +183,9 @@ typedef struct kb_summary {
     int32_t first_failed; /* lowest index rejected or failed, -1 if none */
 } kb_summary;
 
-/* Positions in one candidate (kb_screen_locate): element indices in the
- * flattened tensor, -1 where no element qualifies.
+/* Positions in one candidate (kb_screen_locate, or kb_screen_ex with
+ * opts.d_loc): element indices in the flattened tensor, -1 where no element
+ * qualifies.
  *   first_mismatch  smallest i that does not match;
  *   max_abs_index   smallest i with |fl(c_i - r_i)| == max_abs_err
  *                   (-1 when max_abs_err is 0);
