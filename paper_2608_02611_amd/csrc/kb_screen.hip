@@ -1198,12 +1198,16 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         uint64_t i0 = kNone, i1 = kNone, i2 = kNone;  // positions
         const Part2* row = p.part2 + (size_t)(j0 + jj) * S;
         const double* rs = p.part2_ssr + (size_t)g * S;
-        for (int q0 = sl; q0 < S; q0 += 64) {
-            Part2 v[4];
-            double w[4];
-            Part2Idx vi[4];
+        // U super-groups per lane in flight (fewer with positions, whose
+        // partials are larger: this loop sets the kernel's register peak);
+        // either way each lane adds its super-groups in increasing order
+        constexpr int U = LOC ? 2 : 4;
+        for (int q0 = sl; q0 < S; q0 += 16 * U) {
+            Part2 v[U];
+            double w[U];
+            Part2Idx vi[U];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < U; ++u) {
                 const int q = q0 + 16 * u;
                 if (FF && q < S) {
                     nr += ld_coherent(&row[q].nread);
@@ -1231,7 +1235,7 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
                 }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < U; ++u) {
                 if constexpr (LOC) {
                     // (value, smallest index) pairs, before the maxima move
                     i0 = min_u64(i0, vi[u].ix[IX_FIRST_MISMATCH]);
