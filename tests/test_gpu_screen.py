@@ -16,8 +16,8 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import (THREADS, assert_records_match, ensure_built, oracle_records, oracle_workload,
-                           storage)
+from tests.helpers import (THREADS, assert_records_match, dtype_name, ensure_built, oracle_records,
+                           oracle_workload, storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -345,34 +345,48 @@ def test_determinism_and_workspace_reuse(dev):
     assert_records_match(first, oracle_records(w.ref, w.cands, w.atol, w.rtol), "c2 1/16")
 
 
-@pytest.mark.parametrize("flags", [0, kb.KB_FAIL_FAST])
-def test_dirty_workspace_is_reported(dev, flags):
+@pytest.mark.parametrize("mode", ["plain", "fail_fast", "positions"])
+def test_dirty_workspace_is_reported(dev, mode):
     """Workspaces that break the zero-fill contract: filled with 0xFF bytes,
     with random bytes, and used for other sizes without a new zero-fill
     (the partials of one call then lie where the next call's counters are).
-    Every call's readback must either be the oracle's records or raise
-    KB_ERR_WORKSPACE -- never wrong records -- and the garbage fills must be
-    caught.  After kb_screen_workspace_init every call is exact again."""
+    Every call's readback must either be the oracle's records (and, with
+    positions, the oracle's positions) or raise KB_ERR_WORKSPACE -- never
+    wrong records -- and the garbage fills must be caught.  After
+    kb_screen_workspace_init every call is exact again."""
+    flags = kb.KB_FAIL_FAST if mode == "fail_fast" else 0
     big, _ = oracle_workload("c4", dev, seed=2, scale=1 / 256, K=40)
     small, _ = oracle_workload("c1", dev, seed=2)
     plan = kb.kb_screen_launch(40, big.numel, kb.KB_F16)
-    say("dirty workspace", flags, plan)
+    say("dirty workspace", mode, plan)
     assert plan["n_groups"] > 1 and plan["blocks_per_group"] > 16, plan  # two-level finish
-    nbytes = max(kb.kb_screen_workspace_bytes(40, big.numel, kb.KB_F16),
-                 kb.kb_screen_workspace_bytes(4, small.numel, kb.KB_F32))
+    size = kb.kb_screen_positions_workspace_bytes if mode == "positions" else kb.kb_screen_workspace_bytes
+    nbytes = max(size(40, big.numel, kb.KB_F16), size(4, small.numel, kb.KB_F32))
     ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     orcs = {w.name: oracle_records(w.ref, w.cands, w.atol, w.rtol) for w in (big, small)}
+    locs = {}
+    if mode == "positions":
+        for w in (big, small):
+            r = storage(w.ref)
+            locs[w.name] = []
+            for c, o in zip(w.cands, orcs[w.name]):
+                fm, ai, ri = oracle.locate(r, storage(c), dtype_name(w.ref), w.atol, w.rtol, o["max_abs_err"],
+                                           o["max_rel_err"])
+                locs[w.name].append({"first_mismatch": fm, "max_abs_index": ai, "max_rel_index": ri})
     g = torch.Generator(device=dev).manual_seed(99)
 
     def run(w):
         st = kb.alloc_stats(len(w.cands), dev)
-        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, flags, ws, st)
+        d_loc = kb.alloc_locate(len(w.cands), dev) if mode == "positions" else None
+        kb.kb_screen(w.ref, w.cands, w.atol, w.rtol, flags, ws, st, d_loc=d_loc)
         try:
             recs, _ = kb.kb_screen_stats(st, len(w.cands))
         except kb.KbError as e:
             assert e.code == kb.KB_ERR_WORKSPACE, e
             return None
         orc = orcs[w.name]
+        if d_loc is not None:
+            assert kb.read_locate(d_loc, len(w.cands)) == locs[w.name], w.name
         if flags == 0:
             assert_records_match(recs, orc, w.name)
         else:
