@@ -117,7 +117,7 @@ def test_random_ragged(dev, dt):
 
 
 @pytest.mark.parametrize("name,scale,K", [("c1", 1.0, 4), ("c2", 1 / 64, 16), ("c3", 1 / 8, 64),
-                                          ("c4", 1 / 256, 16), ("c5", 1 / 512, 8)])
+                                          ("c4", 1 / 256, 16), ("c4", 1 / 256, 40), ("c5", 1 / 512, 8)])
 def test_workloads(dev, name, scale, K):
     w, _ = oracle_workload(name, dev, seed=0, scale=scale, K=K)
     check(w.ref, w.cands, w.atol, w.rtol, 0, name)
