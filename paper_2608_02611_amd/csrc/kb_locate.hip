@@ -12,11 +12,11 @@
 // position as soon as one of its lanes has found it: every later chunk of
 // the wave holds larger indices.  On a failing candidate the first mismatch
 // is usually in a wave's first chunk.  Each wave loads two chunks ahead of
-// the two it scans.  Per element a cheap, branch-free pass only ORs wave ballots (the
-// mismatch filter, d == max abs, the max-rel filter) into scalar masks; a
-// chunk whose masks show a hit is evaluated again from the
-// definitions into 8-bit lane masks, and its index formed (the lane's lowest
-// set bit, then a wave minimum by DPP).  The wave's finds are merged into
+// the two it scans.  A cheap, branch-free pass takes per lane the maxima of
+// three filters over its elements (the mismatch filter, d against max abs,
+// the max-rel filter) and one wave ballot of each; a chunk with a hit is
+// evaluated again from the definitions into 8-bit lane masks, and its index
+// formed (the lane's lowest set bit, then a wave minimum by DPP).  The wave's finds are merged into
 // the output with a 64-bit atomic minimum ("none" is all-ones, which reads
 // as -1).  Work-group ids are mapped like the screen's, so that the
 // candidates of one stripe run on one XCD and share the reference stripe in
@@ -137,68 +137,83 @@ __device__ __forceinline__ Hit classify(float c, float r, float atol, float rtol
     return h;
 }
 
-// How the max-rel predicate is filtered for one candidate (wave-uniform):
-// REL_NONE  no max-rel position wanted (max_rel is 0 or NaN, or found);
-// REL_INF   max_rel = +inf: a zero reference, an infinite difference or a
-//           quotient beyond 2^100 can give it;
-// REL_ALL   max_rel < 2^-100, where T below might round back up to max_rel:
-//           every element is checked by division;
-// REL_FMA   d - T a >= 0 with T = fl(max_rel (1 - 2^-20)): fl(d / a) ==
-//           max_rel needs d / a >= max_rel (1 - 2^-24), and the fma keeps
-//           the sign (an underflow to zero passes).
-enum { REL_NONE = 0, REL_INF = 1, REL_ALL = 2, REL_FMA = 3 };
-
-template <int RM>
-__device__ __forceinline__ bool rel_candidate(float d, float a, float T) {
-    if constexpr (RM == REL_NONE) return false;
-    else if constexpr (RM == REL_INF) return (a == 0.f) | (d == __builtin_inff()) | (d >= a * 0x1p100f);
-    else if constexpr (RM == REL_ALL) return true;
-    else return fmaf(-T, a, d) >= 0.f;
-}
-
-// One chunk's cheap pass: per element only the wave ballots of the
-// mismatch filter (M: still looked for), of d == max_abs and of the
-// max-rel filter, OR-ed over the lane's elements (scalar masks, no per-lane
-// state).  A nonzero mask sends the wave to the exact pass.
+// One chunk's cheap pass: per lane, maxima over its elements, then one wave
+// ballot per predicate; a nonzero ballot sends the wave to the exact pass.
+// Each filter lets through every element the definition accepts (and some
+// it rejects), with no branch and no scalar work per element:
 //
-// The mismatch filter is d > tol, or a reference that is not finite (class
-// test).  For a finite reference it is the predicate itself: c == r gives
-// d = 0 <= tol, and a NaN candidate gives a NaN d, which fails d <= tol; an
-// infinite or NaN reference always goes to the exact pass, which applies
-// the definition (tol = -1, and the equal_nan clause).  Written with
-// bitwise ORs of ballots, so that no element needs a branch.
+//  * mismatch (M: still looked for): the NaN-propagating maximum of
+//    fl(d - tol).  For finite d and tol, fl(d - tol) > 0 exactly when
+//    d > tol (a difference of two binary32 values rounds to zero only when
+//    it is zero); a NaN candidate or a reference that is not finite (tol is
+//    then +inf or NaN, d infinite or NaN) gives NaN.  So a lane whose
+//    maximum is positive or NaN may hold a mismatch, and one whose maximum
+//    is <= 0 holds none (d <= tol is a match);
+//  * max abs: the maximum of d (NaN ignored) >= max_abs; an element with
+//    d == max_abs makes it so;
+//  * max rel: the maximum (NaN ignored) of fma(-T, |r|, d) >= 0, with T per
+//    candidate (rel_threshold): fl(d / a) == max_rel needs d >= T a.
 struct AnyHits {
     uint64_t m, a, r;
 };
 
-template <int DT, bool M, int RM>
-__device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const LaneChunk<DT>& cc, float atol,
-                                              float rtol, float max_abs, float T) {
-    AnyHits h{0u, 0u, 0u};
-#pragma unroll
-    for (int i = 0; i < kE; ++i) {
-        const float c = widen_bits<DT>(cc.bits(i));
-        const float r = widen_bits<DT>(rc.bits(i));
-        const float d = fabsf(c - r);
-        const float a = fabsf(r);
-        if constexpr (M) {
-            const float tol = __fadd_rn(atol, __fmul_rn(rtol, a));
-            // class mask: signaling NaN, quiet NaN, -inf, +inf
-            h.m |= ballot(!(d <= tol)) | ballot(__builtin_amdgcn_classf(r, 0x207));
-        }
-        h.a |= ballot(d == max_abs);
-        if constexpr (RM != REL_NONE) h.r |= ballot(rel_candidate<RM>(d, a, T));
-    }
-    return h;
+// T of the max-rel filter.  A finite max_rel >= 2^-100: fl(d / a) ==
+// max_rel needs d / a >= max_rel (1 - 2^-24), so d - T a > 0 for T =
+// fl(max_rel (1 - 2^-20)) (the fma keeps the sign; an underflow to zero
+// passes).  max_rel = +inf: the quotient overflows, or a is zero, or d is
+// infinite; each gives d - 2^100 a >= 0 (exact inside the fma) or a NaN
+// that the definition rejects too (inf / inf).  max_rel < 2^-100, where T
+// might round back up to max_rel: T = 0 lets every element with a finite
+// reference through.
+__device__ __forceinline__ float rel_threshold(float max_rel) {
+    if (__builtin_isinf(max_rel)) return 0x1p100f;
+    if (max_rel < 0x1p-100f) return 0.f;
+    return max_rel * 0x1.ffffep-1f;
 }
 
 template <int DT, bool M>
-__device__ __forceinline__ AnyHits cheap_pass_rm(int rm, const LaneChunk<DT>& rc, const LaneChunk<DT>& cc,
-                                                 float atol, float rtol, float max_abs, float T) {
-    if (rm == REL_FMA) return cheap_pass<DT, M, REL_FMA>(rc, cc, atol, rtol, max_abs, T);
-    if (rm == REL_NONE) return cheap_pass<DT, M, REL_NONE>(rc, cc, atol, rtol, max_abs, T);
-    if (rm == REL_INF) return cheap_pass<DT, M, REL_INF>(rc, cc, atol, rtol, max_abs, T);
-    return cheap_pass<DT, M, REL_ALL>(rc, cc, atol, rtol, max_abs, T);
+__device__ __forceinline__ AnyHits cheap_pass(const LaneChunk<DT>& rc, const LaneChunk<DT>& cc, float atol,
+                                              float rtol, float max_abs, float T) {
+    float ta = 0.f, tr = 0.f;  // (set from the first pair)
+#pragma unroll
+    for (int i = 0; i < kE; i += 2) {
+        float d[2], x[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float r = widen_bits<DT>(rc.bits(i + j));
+            d[j] = fabsf(widen_bits<DT>(cc.bits(i + j)) - r);
+            x[j] = fmaf(-T, fabsf(r), d[j]);
+        }
+        ta = i == 0 ? fmaxf(d[0], d[1]) : fmaxf(ta, fmaxf(d[0], d[1]));
+        tr = i == 0 ? fmaxf(x[0], x[1]) : fmaxf(tr, fmaxf(x[0], x[1]));
+    }
+    AnyHits h;
+    h.m = 0u;
+    h.a = ballot(ta >= max_abs);
+    h.r = ballot(tr >= 0.f);
+    if constexpr (M) {
+        // (the words pass through an empty asm, so that this pass widens
+        // them again instead of keeping the values above live: it runs only
+        // until a wave has found its mismatch, and would otherwise set the
+        // kernel's register peak)
+        LaneChunk<DT> rx = rc, cx = cc;
+#pragma unroll
+        for (int k = 0; k < (DT == DT_F32 ? 8 : 4); ++k) asm volatile("" : "+v"(rx.w[k]), "+v"(cx.w[k]));
+        float tm = 0.f;
+#pragma unroll
+        for (int i = 0; i < kE; i += 2) {
+            float x[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const float r = widen_bits<DT>(rx.bits(i + j));
+                x[j] = fabsf(widen_bits<DT>(cx.bits(i + j)) - r) - __fadd_rn(atol, __fmul_rn(rtol, fabsf(r)));
+            }
+            const float y = __builtin_elementwise_maximum(x[0], x[1]);
+            tm = i == 0 ? y : __builtin_elementwise_maximum(tm, y);
+        }
+        h.m = ballot(!(tm <= 0.f));
+    }
+    return h;
 }
 
 // A pointer made explicitly wave-uniform (held in scalar registers), so that
@@ -210,8 +225,14 @@ __device__ __forceinline__ const char* uniform_base(const void* p) {
     return (const char*)(((uint64_t)hi << 32) | lo);
 }
 
+// Waves per SIMD the kernel is built for: fp32 needs 96 registers for 5;
+// bf16 fits 8 either way, and the bound measured faster (its schedule);
+// the fp16 build would spill scalar registers under an 8-wave bound, which
+// measured slower than its 7 waves.
+constexpr int locate_min_waves(int dt) { return dt == DT_F32 ? 5 : dt == DT_BF16 ? 8 : 1; }
+
 template <int DT>
-__global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTable tab) {
+__global__ __launch_bounds__(kThreads, locate_min_waves(DT)) void locate_kernel(LocateParams p, LocTable tab) {
     const int lane = threadIdx.x & 63;
     // (explicitly wave-uniform, so that the chunk index, the loads' bases and
     // the per-chunk choices stay in scalar registers and branches)
@@ -231,10 +252,7 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
     const bool want_abs = max_abs > 0.f;  // false for 0 and NaN
     const bool want_rel = max_rel > 0.f;
     const bool equal_nan = (p.flags & KB_EQUAL_NAN) != 0;
-    const int rel_mode = !want_rel ? REL_NONE
-                         : __builtin_isinf(max_rel) ? REL_INF
-                         : max_rel < 0x1p-100f ? REL_ALL : REL_FMA;
-    const float T = max_rel * 0x1.ffffep-1f;
+    const float T = rel_threshold(max_rel);
 
     // the wave's finds (wave-uniform), all-ones until found; a candidate
     // whose record counts no mismatch has none to look for (the record was
@@ -247,32 +265,37 @@ __global__ __launch_bounds__(kThreads) void locate_kernel(LocateParams p, LocTab
     // One chunk: the cheap pass, and the exact pass when a ballot is set.
     auto scan = [&](uint64_t chunk, const LaneChunk<DT>& rc, const LaneChunk<DT>& cc) {
         // (readfirstlane: the choice of variant is a scalar branch)
-        const int rm = __builtin_amdgcn_readfirstlane(need_rel ? rel_mode : REL_NONE);
         const AnyHits h = __builtin_amdgcn_readfirstlane(need_mism ? 1 : 0)
-                              ? cheap_pass_rm<DT, true>(rm, rc, cc, p.atol, p.rtol, max_abs, T)
-                              : cheap_pass_rm<DT, false>(rm, rc, cc, p.atol, p.rtol, max_abs, T);
-        const uint64_t any_m = h.m, any_a = need_abs ? h.a : 0u, any_r = h.r;
+                              ? cheap_pass<DT, true>(rc, cc, p.atol, p.rtol, max_abs, T)
+                              : cheap_pass<DT, false>(rc, cc, p.atol, p.rtol, max_abs, T);
+        const uint64_t any_m = h.m, any_a = need_abs ? h.a : 0u, any_r = need_rel ? h.r : 0u;
         if ((any_m | any_a | any_r) == 0) return;
         // Exact pass (rare): the definitions, element by element, into 8-bit
         // lane masks (bit i: element i of this lane qualifies); a position
         // found anywhere in this chunk is below everything later.
+        // (the chunk's words pass through an empty asm, so that the widened
+        // values of the cheap pass are not kept live for this rare path)
+        LaneChunk<DT> rx = rc, cx = cc;
+#pragma unroll
+        for (int k = 0; k < (DT == DT_F32 ? 8 : 4); ++k) asm volatile("" : "+v"(rx.w[k]), "+v"(cx.w[k]));
         uint32_t mm = 0u, ma = 0u, mr = 0u;
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
-            const Hit h = classify(widen_bits<DT>(cc.bits(i)), widen_bits<DT>(rc.bits(i)), p.atol, p.rtol,
+            const Hit h = classify(widen_bits<DT>(cx.bits(i)), widen_bits<DT>(rx.bits(i)), p.atol, p.rtol,
                                    equal_nan, max_abs, max_rel, any_a != 0, any_r != 0);
             mm |= (uint32_t)h.mism << i;
             ma |= (uint32_t)h.abs << i;
             mr |= (uint32_t)h.rel << i;
         }
         const uint64_t base = chunk * kChunk;
-        // (the mismatch and max-rel filters let through elements that the
-        // definitions then reject: a position only if a lane confirmed one)
+        // (every filter lets through elements that the definitions then
+        // reject -- the max-abs one all d above max_abs: a position only if
+        // a lane confirmed one)
         if (any_m != 0 && ballot(mm != 0u)) {
             f_mism = base + wave_min_u32(first_in_lane<DT>(mm, lane));
             need_mism = false;
         }
-        if (any_a != 0) {
+        if (any_a != 0 && ballot(ma != 0u)) {
             f_abs = base + wave_min_u32(first_in_lane<DT>(ma, lane));
             need_abs = false;
         }

@@ -333,3 +333,52 @@ def test_screener_positions_repeated(dev):
         assert s.positions() == want
         first = first or recs
         assert recs == first
+
+
+WIDEN = {"f32": lambda s: s.view(np.float32), "f16": oracle.f16_to_f32_n, "bf16": oracle.bf16_to_f32_n}
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_separate_pass_given_maxima(dev, dt):
+    """kb_screen_locate takes the maxima from the records it is given.  With
+    maxima other than the candidate's own -- a value many elements exceed,
+    one no element has, +inf, a tiny subnormal, a max rel below 2^-100 --
+    the cheap pass must still let through every element that equals them:
+    the positions equal the oracle's kbo_locate for the same maxima."""
+    n = 512 * 64 + 129
+    rng = np.random.default_rng(57)
+    r32 = rng.standard_normal(n).astype(np.float32)
+    zeros = rng.choice(n, 40, replace=False)
+    r32[zeros] = 0.0  # d / 0 = +inf where the candidate differs
+    c32 = (r32 * (1 + rng.uniform(-2e-2, 2e-2, n))).astype(np.float32)
+    c32[zeros[:20]] = 0.5
+    c32[rng.choice(n, 5, replace=False)] = np.inf  # d = +inf
+    ref = to_dev(CONV[dt](r32), dt, dev)
+    cand = to_dev(CONV[dt](c32), dt, dev)
+    rs, cs = storage(ref), storage(cand)
+    r, c = WIDEN[dt](rs), WIDEN[dt](cs)
+    with np.errstate(all="ignore"):
+        d = np.abs(c - r)
+        q = d / np.abs(r)
+    fin_d = np.flatnonzero(np.isfinite(d) & (d > 0))
+    fin_q = np.flatnonzero(np.isfinite(q) & (q > 0))
+    k1, k2 = int(fin_d[len(fin_d) // 3]), int(fin_q[len(fin_q) // 2])
+    absent = np.nextafter(d[k1], np.float32(np.inf))
+    while np.any(d == absent):
+        absent = np.nextafter(absent, np.float32(np.inf))
+    atol, rtol = 1e-3, 1e-3
+    d_stats, _ = kb.kb_screen(ref, [cand], atol, rtol, 0)
+    torch.cuda.synchronize()
+    base = (kb.KbStats * 1).from_buffer_copy(d_stats.cpu().numpy().tobytes())
+    assert base[0].mismatches > 0
+    cases = [(d[k1], q[k2]), (absent, q[k2]), (np.inf, np.inf), (np.float32(2.0 ** -140), np.float32(2.0 ** -110)),
+             (np.nanmax(d[np.isfinite(d)]), np.float32(2.0 ** -101)), (d[k1], np.inf)]
+    for max_abs, max_rel in cases:
+        rec = (kb.KbStats * 1).from_buffer_copy(bytes(base))
+        rec[0].max_abs_err, rec[0].max_rel_err = float(max_abs), float(max_rel)
+        given = torch.frombuffer(bytearray(bytes(rec)), dtype=torch.uint8).to(dev)
+        say("given maxima", dt, float(max_abs), float(max_rel))
+        got = kb.kb_screen_locate(ref, [cand], atol, rtol, given)
+        fm, ai, ri = oracle.locate(rs, cs, dt, atol, rtol, float(max_abs), float(max_rel))
+        assert got[0] == {"first_mismatch": fm, "max_abs_index": ai, "max_rel_index": ri}, \
+            (dt, float(max_abs), float(max_rel), got[0], (fm, ai, ri))
