@@ -406,7 +406,8 @@ def positions_leg(kb, w, reps=20, rounds=3):
     opts.d_loc) against the plain screen, back to back on one stream: kernel
     time per launch of each (the best of `rounds` alternating measurements),
     and the positions, which must equal those of the separate pass
-    (kb_screen_locate)."""
+    (kb_screen_locate).  The separate pass is timed too: device time per call
+    (its fill of the positions and its kernel), calls back to back."""
     import torch
     st = torch.cuda.Stream()
     plain = kb.Screener(w.ref, w.cands, w.atol, w.rtol, stream=st)
@@ -425,10 +426,13 @@ def positions_leg(kb, w, reps=20, rounds=3):
     loc.launch()
     want = loc.read()
     assert got == want, "positions of the screening pass differ from the separate pass"
+    sep_ms = min(event_time(loc.launch, reps, st) for _ in range(rounds))
+    assert loc.read() == want, "repeated separate passes differ"
     K, n, b = len(w.cands), w.numel, w.dtype_bytes
     alg = (K + 1) * n * b
     return {"plain_kernel_ms": round(plain_ms, 5), "with_positions_kernel_ms": round(pos_ms, 5),
             "ratio": round(pos_ms / plain_ms, 3), "with_positions_frac": round(alg / pos_ms / 1e6 / HBM_PEAK_GBPS, 4),
+            "separate_pass_ms": round(sep_ms, 5), "separate_pass_vs_plain": round(sep_ms / plain_ms, 3),
             "launch": withpos.launch_plan(), "positions_equal_separate_pass": True,
             "failed_candidates_first_mismatch": [l["first_mismatch"] for l in got if l["first_mismatch"] >= 0][:4]}
 
