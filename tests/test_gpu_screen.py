@@ -118,7 +118,10 @@ def random_pair(rng, dt, n, K):
         mode = k % 5
         if dt == "f32":
             if mode == 1:
-                c = (r * (1 + rng.uniform(-1e-5, 1e-5, n))).astype(np.float32)
+                # (a reference near the binary32 maximum may round to an
+                # infinity here: one more special value)
+                with np.errstate(over="ignore"):
+                    c = (r * (1 + rng.uniform(-1e-5, 1e-5, n))).astype(np.float32)
             elif mode == 2:
                 c = (r + rng.standard_normal(n).astype(np.float32) * np.float32(1e-3)).astype(np.float32)
             elif mode == 3:
