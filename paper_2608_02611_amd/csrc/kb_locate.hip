@@ -311,12 +311,24 @@ __global__ __launch_bounds__(kThreads, locate_min_waves(DT)) void locate_kernel(
     // index stays inside the tensor), and its data is not scanned.
     uint64_t chunk = (uint64_t)stripe * kWaves + wave;
     if (chunk < n_chunks) {
+        // Priority: 3 until the last eighth of the wave's chunk pairs, then
+        // 0, so that in the last eighth the waves still behind are issued
+        // first (among equal priorities the arbiter favours the oldest
+        // wave).  Measured: 64 fp16 candidates of 2^26 elements 10%
+        // faster, 16 bf16 of 2^24 and 8 fp32 of 2^27 unchanged, 1024 fp32
+        // of 2^18 1.5% slower; the screen's three-step schedule cost the
+        // 16 bf16 candidates 7-17% here.
+        const uint64_t n_it = (n_chunks - chunk + 2 * wstride - 1) / (2 * wstride);
+        const uint64_t drop = n_it * 7 / 8;
+        uint64_t n_seen = 0;
+        __builtin_amdgcn_s_setprio(3);
         const uint64_t c1 = chunk + wstride < n_chunks ? chunk + wstride : chunk;
         LaneChunk<DT> ra = load_lane<DT, false>(ref, chunk, off);
         LaneChunk<DT> ca = load_lane<DT>(cand, chunk, off);
         LaneChunk<DT> rb = load_lane<DT, false>(ref, c1, off);
         LaneChunk<DT> cb = load_lane<DT>(cand, c1, off);
         for (; chunk < n_chunks && (need_mism || need_abs || need_rel); chunk += 2 * wstride) {
+            if (n_seen++ == drop) __builtin_amdgcn_s_setprio(0);
             const uint64_t n0 = chunk + 2 * wstride, n1 = chunk + 3 * wstride;
             const uint64_t l0 = n0 < n_chunks ? n0 : chunk, l1 = n1 < n_chunks ? n1 : chunk;
             const LaneChunk<DT> rn0 = load_lane<DT, false>(ref, l0, off);
@@ -331,6 +343,7 @@ __global__ __launch_bounds__(kThreads, locate_min_waves(DT)) void locate_kernel(
             cb = cn1;
         }
     }
+    __builtin_amdgcn_s_setprio(0);
     // Ragged tail (numel mod 512 elements): stripe 0, one element per thread.
     if (stripe == 0) {
         for (uint64_t e = n_chunks * kChunk + threadIdx.x; e < p.numel; e += kThreads) {
