@@ -145,10 +145,11 @@ __device__ __forceinline__ Hit classify(float c, float r, float atol, float rtol
 //  * mismatch (M: still looked for): the NaN-propagating maximum of
 //    fl(d - tol).  For finite d and tol, fl(d - tol) > 0 exactly when
 //    d > tol (a difference of two binary32 values rounds to zero only when
-//    it is zero); a NaN candidate or a reference that is not finite (tol is
-//    then +inf or NaN, d infinite or NaN) gives NaN.  So a lane whose
-//    maximum is positive or NaN may hold a mismatch, and one whose maximum
-//    is <= 0 holds none (d <= tol is a match);
+//    it is zero); not (d <= tol) with an infinite or NaN operand gives +inf
+//    or NaN, and so does a reference that is not finite (d is then NaN or
+//    infinite, tol infinite or NaN), which the exact pass decides.  So a
+//    lane whose maximum is positive or NaN may hold a mismatch, and one
+//    whose maximum is <= 0 holds none (d <= tol, a match);
 //  * max abs: the maximum of d (NaN ignored) >= max_abs; an element with
 //    d == max_abs makes it so;
 //  * max rel: the maximum (NaN ignored) of fma(-T, |r|, d) >= 0, with T per
