@@ -84,6 +84,18 @@ def oracle_records(ref, cands, atol, rtol, flags=0, chunk=1 << 24, dt=None):
     return [oracle.finalize(oracle.merge(p)) for p in partials]
 
 
+def oracle_positions_host(ref, cands, dt, atol, rtol, records, flags=0):
+    """The oracle's positions (kbo_locate) of every candidate, on host
+    storage arrays, with the maxima of the oracle's own records; one host
+    thread per candidate."""
+    def one(k):
+        fm, ai, ri = oracle.locate(ref, cands[k], dt, atol, rtol, records[k]["max_abs_err"],
+                                   records[k]["max_rel_err"], flags)
+        return {"first_mismatch": fm, "max_abs_index": ai, "max_rel_index": ri}
+    with ThreadPoolExecutor(THREADS) as ex:
+        return list(ex.map(one, range(len(cands))))
+
+
 def close(a, b, rtol=SUM_RTOL):
     if math.isnan(a) or math.isnan(b):
         return math.isnan(a) and math.isnan(b)

@@ -16,8 +16,8 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import (THREADS, assert_records_match, dtype_name, ensure_built, oracle_records,
-                           oracle_workload, storage)
+from tests.helpers import (THREADS, assert_records_match, dtype_name, ensure_built, oracle_positions_host,
+                           oracle_records, oracle_workload, storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -275,7 +275,8 @@ def test_workloads_scaled(dev, name, scale, K):
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
 def test_workloads_full_size(dev, name):
     """The exact sizes and launch configuration the benchmark times, on the
-    workload the oracle built (the oracle screens its own host arrays)."""
+    workload the oracle built (the oracle screens its own host arrays); and
+    the positions of every candidate at those sizes, in both forms."""
     spec = synth.SPECS[name]
     code = {"f32": kb.KB_F32, "f16": kb.KB_F16, "bf16": kb.KB_BF16}[spec["dtype"]]
     say("full-size workload", name, kb.kb_screen_launch(spec["K"], math.prod(spec["shape"]), code))
@@ -284,6 +285,16 @@ def test_workloads_full_size(dev, name):
     recs, _ = kb.screen(w.ref, w.cands, w.atol, w.rtol)
     orc = oracle_records(ow.ref, ow.cands, ow.atol, ow.rtol, dt=ow.dtype)
     assert_records_match(recs, orc, name + " full")
+    # the positions at the same sizes, in both forms (the separate pass, and
+    # the screening pass with positions), against kbo_locate with the
+    # oracle's own maxima
+    say("full-size positions", name)
+    want = oracle_positions_host(ow.ref, ow.cands, ow.dtype, ow.atol, ow.rtol, orc)
+    _, sep = kb.locate(w.ref, w.cands, w.atol, w.rtol)
+    frecs, fused = kb.screen_positions(w.ref, w.cands, w.atol, w.rtol)
+    assert_records_match(frecs, orc, name + " full, with positions")
+    bad = [(k, s_, f, o) for k, (s_, f, o) in enumerate(zip(sep, fused, want)) if s_ != o or f != o]
+    assert not bad, (name, len(bad), bad[:4])
     del w, ow
     torch.cuda.empty_cache()
 
