@@ -24,8 +24,8 @@ import torch
 
 import oracle
 import paper_2608_02611_amd as kb
-from tests.helpers import (EXACT_FIELDS, SUM_FIELDS, SUM_RTOL, assert_records_match, close,
-                           ensure_built, oracle_records, oracle_workload, storage)
+from tests.helpers import (assert_records_match, check_partial, ensure_built, oracle_records, oracle_workload,
+                           same_record, storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -60,38 +60,6 @@ def same_bits(a, b):
         if x != y and not (isinstance(x, float) and x != x and y != y):
             return False
     return True
-
-
-def same_record(a, b):
-    """A passing candidate's fail-fast record against its plain record:
-    counts, flags and maxima identical, the sums within SUM_RTOL."""
-    for f in a:
-        if f in SUM_FIELDS:
-            if not close(a[f], b[f]):
-                return False
-        elif a[f] != b[f]:
-            return False
-    return True
-
-
-def check_partial(g, o, label):
-    """A fail-fast record of a failing candidate against the oracle's record
-    over the whole tensor."""
-    assert g["status"] == 0, (label, g)
-    assert o["mismatches"] > 0, (label, o)
-    assert 1 <= g["mismatches"] <= o["mismatches"], (label, g, o)
-    assert g["passed"] == 0, (label, g)
-    assert 0 < g["numel"] <= o["numel"], (label, g, o)
-    assert g["mismatches"] <= g["numel"], (label, g)
-    for f in ("nan_count", "pos_inf_count", "neg_inf_count"):
-        assert g[f] <= o[f], (label, f, g, o)
-    for f in ("max_abs_err", "max_rel_err"):
-        assert g[f] <= o[f] or o[f] != o[f], (label, f, g, o)
-    for f in ("sum_sq_diff", "sum_sq_ref"):
-        assert g[f] <= o[f] * (1 + SUM_RTOL), (label, f, g, o)
-    if g["numel"] == o["numel"]:
-        # nothing was skipped: the whole record
-        assert_records_match([g], [o], label)
 
 
 def make_case(dt, n, seed):

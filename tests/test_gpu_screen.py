@@ -16,8 +16,8 @@ import torch
 import oracle
 import paper_2608_02611_amd as kb
 import synth
-from tests.helpers import (THREADS, assert_records_match, dtype_name, ensure_built, oracle_positions_host,
-                           oracle_records, oracle_workload, storage)
+from tests.helpers import (THREADS, assert_records_match, check_partial, dtype_name, ensure_built,
+                           oracle_positions_host, oracle_records, oracle_workload, same_record, storage)
 
 pytestmark = pytest.mark.gpu
 
@@ -275,8 +275,9 @@ def test_workloads_scaled(dev, name, scale, K):
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
 def test_workloads_full_size(dev, name):
     """The exact sizes and launch configuration the benchmark times, on the
-    workload the oracle built (the oracle screens its own host arrays); and
-    the positions of every candidate at those sizes, in both forms."""
+    workload the oracle built (the oracle screens its own host arrays); and,
+    at those sizes, the positions of every candidate in both forms and the
+    fail-fast screen."""
     spec = synth.SPECS[name]
     code = {"f32": kb.KB_F32, "f16": kb.KB_F16, "bf16": kb.KB_BF16}[spec["dtype"]]
     say("full-size workload", name, kb.kb_screen_launch(spec["K"], math.prod(spec["shape"]), code))
@@ -295,6 +296,16 @@ def test_workloads_full_size(dev, name):
     assert_records_match(frecs, orc, name + " full, with positions")
     bad = [(k, s_, f, o) for k, (s_, f, o) in enumerate(zip(sep, fused, want)) if s_ != o or f != o]
     assert not bad, (name, len(bad), bad[:4])
+    # the fail-fast screen at the same sizes: a passing candidate's record
+    # is its plain record (sums within 1e-6), a failing one's is bounded by
+    # the oracle's over the whole tensor
+    say("full-size fail-fast", name)
+    fast, ssum = kb.screen(w.ref, w.cands, w.atol, w.rtol, kb.KB_FAIL_FAST)
+    for k, (g, f, o) in enumerate(zip(fast, recs, orc)):
+        if o["mismatches"] == 0:
+            assert same_record(g, f), (name, k, g, f)
+        else:
+            check_partial(g, o, "%s full cand %d" % (name, k))
     del w, ow
     torch.cuda.empty_cache()
 
