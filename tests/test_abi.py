@@ -503,3 +503,35 @@ def test_gate_matches_the_oracle_on_random_views(L):
                       [desc_of(m) for m in cands])
         assert rc == kb.KB_OK
         assert list(st) == [oracle.gate_status(ref_m, m) for m in cands], (ref_m, cands)
+
+
+def test_error_text_belongs_to_the_calling_thread(L):
+    """The error text is the only state a call leaves, and it is per thread:
+    threads that fail with their own message, interleaved with threads whose
+    successful calls clear theirs, each read back exactly their own."""
+    from concurrent.futures import ThreadPoolExecutor
+    L.kb_last_error.restype = ctypes.c_char_p
+    arr = (kb.KbStats * 4)()
+    passed = (ctypes.c_int32 * 4)()
+
+    def failing(t):
+        dtype = 100 + t
+        want = ("unknown dtype %d" % dtype).encode()
+        for _ in range(3000):
+            rc = L.kb_gen_inputs(None, dtype, ctypes.c_uint64(10), 1, ctypes.c_float(0.0), ctypes.c_float(1.0),
+                                 ctypes.c_uint64(0), 0, 0, ctypes.c_uint64(0), None)
+            msg = L.kb_last_error()
+            if rc != kb.KB_ERR_DTYPE or want not in msg:
+                return (t, rc, msg)
+        return None
+
+    def succeeding(t):
+        for _ in range(3000):
+            if L.kb_summarize(arr, 4, None, passed) != kb.KB_OK or L.kb_last_error() not in (b"", None):
+                return (t, L.kb_last_error())
+        return None
+
+    with ThreadPoolExecutor(8) as ex:
+        futs = [ex.submit(failing if t % 2 == 0 else succeeding, t) for t in range(8)]
+        bad = [f.result() for f in futs if f.result() is not None]
+    assert not bad, bad
