@@ -481,6 +481,45 @@ def test_two_streams_concurrent_screens(dev):
             assert_records_match(sc.records(slot), orc, "two streams slot %d" % slot)
 
 
+def test_host_threads_each_on_its_own_stream(dev):
+    """Four host threads use the library at once, each on its own stream with
+    its own workload (one of more than 128 candidates, so a host launch
+    table; one with positions in the screening pass): every call of every
+    thread gives the records and positions of a call made alone."""
+    say("host threads")
+    cases = [("c2", 1 / 64, 16, False), ("c3", 1 / 16, 200, False), ("c4", 1 / 256, 40, True),
+             ("c5", 1 / 1024, 8, False)]
+    work, alone = [], []
+    for name, scale, K, pos in cases:
+        w, _ = oracle_workload(name, dev, seed=9, scale=scale, K=K)
+        if pos:
+            recs, locs = kb.screen_positions(w.ref, w.cands, w.atol, w.rtol)
+        else:
+            (recs, _), locs = kb.screen(w.ref, w.cands, w.atol, w.rtol), None
+        assert_records_match(recs, oracle_records(w.ref, w.cands, w.atol, w.rtol), name + " alone")
+        work.append((w, pos))
+        alone.append((recs, locs))
+    torch.cuda.synchronize()
+
+    def run(t):
+        w, pos = work[t]
+        st = torch.cuda.Stream()
+        with torch.cuda.stream(st):
+            for i in range(12):
+                if pos:
+                    recs, locs = kb.screen_positions(w.ref, w.cands, w.atol, w.rtol, stream=st)
+                else:
+                    (recs, _), locs = kb.screen(w.ref, w.cands, w.atol, w.rtol, stream=st), None
+                # (repr: the same bits, NaN fields included)
+                if repr((recs, locs)) != repr(alone[t]):
+                    return (t, i)
+        return None
+
+    with ThreadPoolExecutor(len(cases)) as ex:
+        bad = [r for r in ex.map(run, range(len(cases))) if r is not None]
+    assert not bad, bad
+
+
 # ------------------------------------------------ exhaustive 16-bit pairs ---
 
 @pytest.mark.parametrize("dt,tol", [("f16", 1e-3), ("bf16", 1e-2)])
