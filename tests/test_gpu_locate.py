@@ -209,16 +209,18 @@ def test_workload_c2_full_size(dev):
     torch.cuda.empty_cache()
 
 
-def test_indices_beyond_32_bits(dev):
-    """2^32 + 777 bf16 elements (8.6 GB per tensor): element indices and
-    counts past 32 bits in the screen and the position search.  The
-    candidate is the reference except at three planted elements, so the
-    expected record and positions follow from the construction (the oracle
-    would take minutes over 4 G elements): a difference of 4 below 2^32,
-    and a tie of the largest difference 8 (relative error 8) at 2^32 + 5,
-    in the last whole chunk, and in the ragged tail."""
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_indices_beyond_32_bits(dev, dt):
+    """2^32 + 777 elements (8.6 GB per bf16 tensor, 17.2 GB per fp32 one,
+    byte offsets past 2^34): element indices and counts past 32 bits in the
+    screen and the position search.  The candidate is the reference except
+    at three planted elements, so the expected record and positions follow
+    from the construction (the oracle would take minutes over 4 G elements):
+    a difference of 4 below 2^32, and a tie of the largest difference 8
+    (relative error 8) at 2^32 + 5, in the last whole chunk, and in the
+    ragged tail."""
     n = (1 << 32) + 777
-    ref = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    ref = torch.empty(n, dtype=TORCH_DT[dt], device=dev)
     kb.kb_gen_inputs(ref, kb.KB_DIST_NORMAL, 0.0, 1.0, seed=5, stream_id=0x3232)
     cand = ref.clone()
     low, high, tail = 3 << 30, (1 << 32) + 5, n - 3
@@ -227,7 +229,7 @@ def test_indices_beyond_32_bits(dev):
         ref[i] = 1.0
         cand[i] = c
     torch.cuda.synchronize()
-    say("indices beyond 32 bits")
+    say("indices beyond 32 bits", dt)
     recs, locs = kb.locate(ref, [cand], 1e-2, 1e-2)
     r = recs[0]
     assert r["numel"] == n and r["mismatches"] == 3 and r["nan_count"] == 0, r
