@@ -209,9 +209,9 @@ def test_workload_c2_full_size(dev):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
 def test_indices_beyond_32_bits(dev, dt):
-    """2^32 + 777 elements (8.6 GB per bf16 tensor, 17.2 GB per fp32 one,
+    """2^32 + 777 elements (8.6 GB per 16-bit tensor, 17.2 GB per fp32 one,
     byte offsets past 2^34): element indices and counts past 32 bits in the
     screen and the position search.  The candidate is the reference except
     at three planted elements, so the expected record and positions follow
