@@ -950,17 +950,22 @@ __device__ __forceinline__ void screen_part(const ScreenParams& p, const InlineT
         const double sd = wave_sum_f64(s_ssd[j][threadIdx.x]);
         const uint32_t am = wave_max_u32(amax[j]);
         if constexpr (LOC) {
-            // the element of the wave's max abs error: the lanes that hold it
-            // re-read the chunk in which it first occurred
+            // the element of the wave's max abs error.  Every element of a
+            // chunk lies below every element of a later chunk (and the tail
+            // codes follow the chunks in index order), so the smallest index
+            // holding the maximum is in the earliest chunk in which a lane
+            // first reached it: only the lanes whose first occurrence is in
+            // that chunk re-read it -- one chunk, coalesced, however many
+            // lanes tie
             uint64_t ai = kNone;
             if (am != 0u) {
+                const uint32_t ac = wave_min_u32(amax[j] == am ? achunk[j] : ~0u);
                 uint64_t mine = kNone;
-                if (amax[j] == am) {
-                    const uint32_t ac = achunk[j];
+                if (amax[j] == am && achunk[j] == ac) {
                     if (ac < n_chunks) {
                         const uint64_t cb = (uint64_t)ac * chunk_bytes<DT>();
-                        const Raw<DT> c = load_chunk<DT, false>(cand[j] + cb, off);
-                        const Raw<DT> rr = load_chunk<DT, false>(ref + cb, off);
+                        const Raw<DT> c = load_chunk<DT, false>(uniform_ptr(cand[j] + cb), off);
+                        const Raw<DT> rr = load_chunk<DT, false>(uniform_ptr(ref + cb), off);
                         mine = (uint64_t)ac * kChunk + slot_offset<DT>(lane, lane_abs_slot<DT>(c, rr, am));
                     } else {
                         mine = tfirst + (uint64_t)(ac - (uint32_t)n_chunks) * kThreads + threadIdx.x;
